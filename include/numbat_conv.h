@@ -1,0 +1,178 @@
+/*
+ * numbat_conv.h -- C ABI of the Conv2d + BatchNorm(train) + SiLU hot path for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operations are those of the Conv -> BN -> SiLU block that makes up the
+ * YOLOv8m-class detector of the paper's case study (Sec. 6.1), trained with
+ * mixed precision as in Sec. 3.2 and Table 1 (precision row): convolutions in
+ * 16-bit floating point (here bf16) with fp32 accumulation, batch
+ * normalisation and its statistics in fp32, fp32 weight gradients (master
+ * weights are fp32).  Operator semantics follow the reference defaults of
+ * Sec. 3 (iv): the convolution is a cross-correlation with zero padding and no
+ * bias, BN uses the biased batch variance to normalise and the unbiased one
+ * for running statistics, SiLU(z) = z * sigmoid(z).
+ *
+ * Boundary conventions (Sec. 4, the C ABI layer): plain pointers and sizes,
+ * runtime-checked problem descriptors carrying their own struct_size (the ABI
+ * is versioned and only ever grows), status codes with thread-local detail
+ * text, caller-owned memory.  The library allocates no device memory: every
+ * buffer, including scratch workspace, is passed in by the caller.  Interfaces
+ * refuse before touching data (Sec. 5): every check completes before anything
+ * is enqueued, so a call that returns an error has launched nothing.
+ *
+ * Memory layouts
+ *   activations  NHWC bf16.  A tensor is N*H*W "pixels"; pixel i starts at
+ *                element i * pixel_stride, its channels are contiguous.  A
+ *                pixel stride larger than the channel count describes a
+ *                channel slice of a wider tensor (split / concat views).
+ *   conv weights OHWI bf16 [c_out][kh][kw][c_in], dense.
+ *   weight grads OHWI fp32 [c_out][kh][kw][c_in], dense.
+ *   BN vectors   fp32 [c].
+ * Alignment: every bf16 tensor pointer and pixel stride must allow 16-byte
+ * vector access: pointers 16-byte aligned, pixel strides and channel counts
+ * multiples of 8 (the one exception is a 3-channel image input to the
+ * convolution, for which x may be 2-byte aligned with pixel stride >= 3).
+ *
+ * Streams: `stream` is a hipStream_t passed as void* (NULL = default stream).
+ * All work is enqueued on it, nothing synchronises; results are valid once the
+ * stream reaches the enqueued work.  Device-side faults surface at the
+ * caller's next synchronisation.
+ *
+ * Determinism: for the same inputs, problem and device model every output is
+ * bitwise identical from run to run (all reductions use a fixed order; no
+ * floating-point atomics), in the spirit of the paper's bitwise-reproducible
+ * gradient reduction (Sec. 3.2, DDP).
+ */
+#ifndef NUMBAT_CONV_H
+#define NUMBAT_CONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define NUMBAT_ABI_VERSION 1u
+
+typedef enum {
+  NUMBAT_OK = 0,
+  NUMBAT_ERR_NULL = 1,        /* a required pointer is NULL */
+  NUMBAT_ERR_BAD_DESC = 2,    /* a descriptor field is out of range or inconsistent */
+  NUMBAT_ERR_UNSUPPORTED = 3, /* well-formed but not provided (e.g. channels not a multiple of 8) */
+  NUMBAT_ERR_ALIGN = 4,       /* pointer or pixel stride breaks the alignment rules above */
+  NUMBAT_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than numbat_workspace_size() */
+  NUMBAT_ERR_DEVICE = 6,      /* a HIP runtime call failed; detail holds the HIP error text */
+  NUMBAT_ERR_VERSION = 7      /* struct_size does not match this library's descriptor */
+} numbat_status;
+
+typedef enum {
+  NUMBAT_OP_CONV_FWD = 0,
+  NUMBAT_OP_CONV_BWD_DATA = 1,
+  NUMBAT_OP_CONV_BWD_WEIGHT = 2,
+  NUMBAT_OP_BN_SILU_FWD = 3,
+  NUMBAT_OP_BN_SILU_BWD = 4
+} numbat_op;
+
+/* One 2-D convolution (dilation 1, one group).  Output size
+ * ho = (h + 2*pad_h - kh) / stride_h + 1, wo likewise. */
+typedef struct {
+  uint32_t struct_size;   /* = sizeof(numbat_conv_problem) */
+  int32_t n, h, w;        /* batch and input spatial size */
+  int32_t c_in, c_out;
+  int32_t kh, kw;
+  int32_t stride_h, stride_w;
+  int32_t pad_h, pad_w;
+  int64_t x_pixel_stride; /* elements between pixels of x and dx; 0 means c_in */
+  int64_t y_pixel_stride; /* elements between pixels of y and dy; 0 means c_out */
+} numbat_conv_problem;
+
+/* Batch normalisation over m rows (pixels) of c channels, followed by SiLU. */
+typedef struct {
+  uint32_t struct_size;    /* = sizeof(numbat_bn_problem) */
+  int32_t c;               /* channels */
+  int64_t m;               /* rows = N*H*W, at least 2 */
+  float eps;               /* added to the variance inside the square root */
+  float momentum;          /* running-statistics factor; used only when running_* != NULL */
+  int64_t y_pixel_stride;  /* pixels of y (the BN input); 0 means c */
+  int64_t a_pixel_stride;  /* pixels of out (forward) and g (backward); 0 means c */
+  int64_t r_pixel_stride;  /* pixels of residual (forward) and residual_grad (backward); 0 means c */
+  int64_t dy_pixel_stride; /* pixels of dy (backward); 0 means c */
+} numbat_bn_problem;
+
+/* NUMBAT_ABI_VERSION of the loaded library. */
+uint32_t numbat_abi_version(void);
+
+/* Detail text of the last failing call on this thread ("" after success). Owned by
+ * the library; valid until the next call on the same thread. */
+const char* numbat_last_error(void);
+
+/* Short name of a status code; never NULL. */
+const char* numbat_status_string(numbat_status status);
+
+/* Output spatial size of a convolution problem.  Fails like the entry points on a
+ * malformed descriptor. */
+numbat_status numbat_conv_output_shape(const numbat_conv_problem* p, int32_t* ho, int32_t* wo);
+
+/* Workspace bytes that entry point `op` needs for `problem` (a numbat_conv_problem* for
+ * the three convolution ops, a numbat_bn_problem* for the two BN ops).  Depends only on
+ * the problem, never on the device.  May be 0; then ws may be NULL. */
+numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* bytes);
+
+/* Forward convolution, the defining sum of a cross-correlation (Sec. 6.1 conv block):
+ *   y[n,p,q,o] = sum_{r,s,c} w[o,r,s,c] * x[n, p*stride_h - pad_h + r, q*stride_w - pad_w + s, c]
+ * with x = 0 outside the image.  x: bf16 NHWC (pixel stride x_pixel_stride); w: bf16 OHWI;
+ * y: bf16 NHWC (pixel stride y_pixel_stride), fp32 accumulation rounded to nearest even.
+ * batch_stats: NULL, or fp32 [2*c_out] receiving the batch mean (first c_out entries) and
+ * biased batch variance (next c_out) of every output channel over the n*ho*wo rows, taken
+ * from the fp32 accumulators before rounding (BN statistics in fp32, Sec. 3.2). */
+numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
+                              float* batch_stats, void* ws, size_t ws_bytes, void* stream);
+
+/* Data gradient of the forward convolution (its adjoint in x):
+ *   dx[n,h,w,c] = sum over (p,q,r,s,o) with p*stride_h - pad_h + r = h and
+ *                 q*stride_w - pad_w + s = w of  w[o,r,s,c] * dy[n,p,q,o].
+ * dy: bf16 NHWC [n,ho,wo,c_out] (y_pixel_stride); dx: bf16 NHWC [n,h,w,c_in] (x_pixel_stride).
+ * accumulate != 0: dx += result (sum formed in fp32, rounded once), else dx = result. */
+numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
+                                   int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/* Weight gradient of the forward convolution (its adjoint in w), fp32 (gradients of the
+ * fp32 master weights, Table 1 precision row):
+ *   dw[o,r,s,c] = sum_{n,p,q} dy[n,p,q,o] * x[n, p*stride_h - pad_h + r, q*stride_w - pad_w + s, c].
+ * accumulate != 0: dw += result, else dw = result.  The sum over n*ho*wo rows is split into
+ * fixed ranges reduced in a fixed order, so the result is bitwise reproducible. */
+numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x, const void* dy, float* dw,
+                                     int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/* Batch normalisation (training mode) + SiLU, forward (BN after Ioffe and Szegedy in fp32,
+ * Sec. 3.2; SiLU, Sec. 6.1):
+ *   mean, var  = batch_stats if given, else the batch mean and biased variance of the bf16 y
+ *   rstd       = 1 / sqrt(var + eps)
+ *   out        = SiLU(gamma * (y - mean) * rstd + beta) [+ residual]      (bf16, RNE)
+ * y, residual, out: bf16 [m rows][c] with their pixel strides; residual may be NULL.
+ * gamma, beta: fp32 [c].  save_mean, save_rstd: fp32 [c] outputs, required (the backward
+ * reads them).  running_mean/running_var: both NULL, or fp32 [c] updated in place as
+ * running = (1 - momentum) * running + momentum * batch (variance term unbiased, * m/(m-1)). */
+numbat_status numbat_bn_silu_fwd(const numbat_bn_problem* p, const void* y, const float* batch_stats,
+                                 const float* gamma, const float* beta, const void* residual, void* out,
+                                 float* save_mean, float* save_rstd, float* running_mean, float* running_var,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of numbat_bn_silu_fwd with batch statistics, given g = dL/d(out):
+ *   z = gamma * xhat + beta,  xhat = (y - save_mean) * save_rstd
+ *   dz = g * sigmoid(z) * (1 + z * (1 - sigmoid(z)))
+ *   dbeta = sum_rows dz,  dgamma = sum_rows dz * xhat                      (fp32 [c])
+ *   dy = gamma * save_rstd * (dz - dbeta / m - xhat * dgamma / m)            (bf16, RNE)
+ * residual_grad: NULL, or bf16 [m][c] (r_pixel_stride) that receives += g, the gradient of
+ * a residual added in the forward.  g, y, dy: bf16 with their pixel strides. */
+numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, const void* y,
+                                 const float* save_mean, const float* save_rstd, const float* gamma,
+                                 const float* beta, void* dy, float* dgamma, float* dbeta, void* residual_grad,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NUMBAT_CONV_H */

@@ -1,0 +1,112 @@
+"""Conv -> BN -> SiLU blocks driven through the C ABI on one GPU.
+
+Device memory comes from PyTorch (caching allocator) and every computation is a
+call into ``libnumbat_conv.so``; this module only allocates buffers and orders the
+calls: forward = conv_fwd (with fused batch statistics) then bn_silu_fwd; backward
+= bn_silu_bwd, then conv_bwd_weight and conv_bwd_data.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import numbat as nb
+
+DEV = "cuda"
+
+
+def dev_bf16(bits: np.ndarray, device=DEV) -> torch.Tensor:
+    """Upload bf16 bit patterns (numpy uint16) as a bf16 tensor."""
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def dev_f32(a: np.ndarray, device=DEV) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+
+def host_f64(t: torch.Tensor) -> np.ndarray:
+    """Exact widening of a bf16 / fp32 device tensor to float64 on the host."""
+    return t.detach().to(torch.float32).cpu().numpy().astype(np.float64)
+
+
+def workspace(nbytes: int, device=DEV) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+@dataclass
+class ConvBlock:
+    """One Conv+BN+SiLU layer: geometry, parameters and the buffers of one step."""
+
+    n: int
+    h: int
+    w: int
+    ci: int
+    co: int
+    k: int
+    s: int
+    eps: float = 1e-3
+    momentum: float = 0.03
+    x_pixel_stride: int = 0
+    y_pixel_stride: int = 0
+    bufs: dict = field(default_factory=dict)
+
+    def __post_init__(self):
+        self.p = self.k // 2
+        self.prob = nb.conv_problem(self.n, self.h, self.w, self.ci, self.co, self.k, stride=self.s, pad=self.p,
+                                    x_pixel_stride=self.x_pixel_stride, y_pixel_stride=self.y_pixel_stride)
+        self.ho, self.wo = nb.numbat_conv_output_shape(self.prob)
+        self.m = self.n * self.ho * self.wo
+        self.ws_fwd = nb.numbat_workspace_size(nb.OP_CONV_FWD, self.prob)
+        self.ws_dgrad = nb.numbat_workspace_size(nb.OP_CONV_BWD_DATA, self.prob)
+        self.ws_wgrad = nb.numbat_workspace_size(nb.OP_CONV_BWD_WEIGHT, self.prob)
+
+    def bn(self, a_pixel_stride=0, r_pixel_stride=0, dy_pixel_stride=0):
+        return nb.bn_problem(self.m, self.co, self.eps, self.momentum, y_pixel_stride=self.y_pixel_stride,
+                             a_pixel_stride=a_pixel_stride, r_pixel_stride=r_pixel_stride,
+                             dy_pixel_stride=dy_pixel_stride)
+
+    def ws_bytes(self) -> int:
+        b = self.bn()
+        return max(self.ws_fwd, self.ws_dgrad, self.ws_wgrad, nb.numbat_workspace_size(nb.OP_BN_SILU_FWD, b),
+                   nb.numbat_workspace_size(nb.OP_BN_SILU_BWD, b))
+
+    # ---- forward: y = conv(x, w) with fused stats, a = SiLU(BN(y)) [+ residual]
+    def forward(self, x, w, gamma, beta, y=None, a=None, residual=None, ws=None, a_pixel_stride=0,
+                r_pixel_stride=0, stream=None):
+        y = y if y is not None else torch.empty((self.n, self.ho, self.wo, self.co), dtype=torch.bfloat16,
+                                                  device=x.device)
+        a = a if a is not None else torch.empty((self.n, self.ho, self.wo, self.co), dtype=torch.bfloat16,
+                                                  device=x.device)
+        ws = ws if ws is not None else workspace(self.ws_bytes(), x.device)
+        stats = torch.empty(2 * self.co, dtype=torch.float32, device=x.device)
+        save_mean = torch.empty(self.co, dtype=torch.float32, device=x.device)
+        save_rstd = torch.empty(self.co, dtype=torch.float32, device=x.device)
+        nb.numbat_conv_fwd(self.prob, x, w, y, stats, ws, stream=stream)
+        nb.numbat_bn_silu_fwd(self.bn(a_pixel_stride, r_pixel_stride), y, stats, gamma, beta, residual, a, save_mean,
+                              save_rstd, ws=ws, stream=stream)
+        return {"y": y, "a": a, "stats": stats, "save_mean": save_mean, "save_rstd": save_rstd}
+
+    # ---- backward
+    def backward(self, g, x, w, gamma, beta, fwd, dx=None, accumulate_dx=False, residual_grad=None, ws=None,
+                 g_pixel_stride=0, r_pixel_stride=0, want_dx=True, stream=None):
+        dev = g.device
+        ws = ws if ws is not None else workspace(self.ws_bytes(), dev)
+        dy = torch.empty((self.n, self.ho, self.wo, self.co), dtype=torch.bfloat16, device=dev)
+        dgamma = torch.empty(self.co, dtype=torch.float32, device=dev)
+        dbeta = torch.empty(self.co, dtype=torch.float32, device=dev)
+        nb.numbat_bn_silu_bwd(self.bn(g_pixel_stride, r_pixel_stride), g, fwd["y"], fwd["save_mean"],
+                              fwd["save_rstd"], gamma, beta, dy, dgamma, dbeta, residual_grad, ws=ws, stream=stream)
+        dw = torch.empty((self.co, self.k, self.k, self.ci), dtype=torch.float32, device=dev)
+        nb.numbat_conv_bwd_weight(self.prob, x, dy, dw, False, ws, stream=stream)
+        out = {"dy": dy, "dgamma": dgamma, "dbeta": dbeta, "dw": dw}
+        if want_dx:
+            if dx is None:
+                dx = torch.empty((self.n, self.h, self.w, self.ci), dtype=torch.bfloat16, device=dev)
+            nb.numbat_conv_bwd_data(self.prob, dy, w, dx, accumulate_dx, ws, stream=stream)
+            out["dx"] = dx
+        return out

@@ -1,0 +1,484 @@
+// C ABI of the conv / BN / SiLU hot path: descriptor validation, workspace sizing and
+// kernel dispatch.  Every check runs before anything is enqueued; a call that returns
+// an error has launched nothing.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/numbat_conv.h"
+#include "kernels.h"
+
+using namespace numbat;
+
+namespace {
+
+thread_local std::string g_err;
+
+numbat_status fail(numbat_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+numbat_status ok() {
+  g_err.clear();
+  return NUMBAT_OK;
+}
+
+numbat_status hip_fail(hipError_t e, const char* what) {
+  return fail(NUMBAT_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+constexpr int64_t kMaxIndex = (1ll << 31) - 1;
+
+// ---------------------------------------------------------------------------
+struct ConvDesc {
+  int32_t n, h, w, ci, co, kh, kw, sh, sw, ph, pw, ho, wo;
+  int64_t x_pix, y_pix;
+  int64_t m;  // n*ho*wo
+};
+
+numbat_status check_conv(const numbat_conv_problem* p, ConvDesc* d) {
+  if (p == nullptr) return fail(NUMBAT_ERR_NULL, "problem descriptor is NULL");
+  if (p->struct_size != sizeof(numbat_conv_problem))
+    return fail(NUMBAT_ERR_VERSION, "numbat_conv_problem.struct_size is %u, this library expects %zu",
+                p->struct_size, sizeof(numbat_conv_problem));
+  if (p->n < 1 || p->h < 1 || p->w < 1 || p->c_in < 1 || p->c_out < 1 || p->kh < 1 || p->kw < 1)
+    return fail(NUMBAT_ERR_BAD_DESC, "sizes must be >= 1 (n=%d h=%d w=%d c_in=%d c_out=%d kh=%d kw=%d)", p->n, p->h,
+                p->w, p->c_in, p->c_out, p->kh, p->kw);
+  if (p->stride_h < 1 || p->stride_w < 1)
+    return fail(NUMBAT_ERR_BAD_DESC, "strides must be >= 1 (%d, %d)", p->stride_h, p->stride_w);
+  if (p->pad_h < 0 || p->pad_w < 0)
+    return fail(NUMBAT_ERR_BAD_DESC, "padding must be >= 0 (%d, %d)", p->pad_h, p->pad_w);
+  if (p->pad_h >= p->kh || p->pad_w >= p->kw)
+    return fail(NUMBAT_ERR_UNSUPPORTED, "padding must be smaller than the kernel (pad %d,%d kernel %d,%d)", p->pad_h,
+                p->pad_w, p->kh, p->kw);
+  const int64_t hp = (int64_t)p->h + 2 * p->pad_h - p->kh, wp = (int64_t)p->w + 2 * p->pad_w - p->kw;
+  if (hp < 0 || wp < 0) return fail(NUMBAT_ERR_BAD_DESC, "kernel larger than the padded input");
+  if ((int64_t)p->kh * p->kw > kMaxTaps)
+    return fail(NUMBAT_ERR_UNSUPPORTED, "kh*kw = %d exceeds %d taps", p->kh * p->kw, kMaxTaps);
+  if (p->stride_h > 4 || p->stride_w > 4) return fail(NUMBAT_ERR_UNSUPPORTED, "strides above 4 are not provided");
+  if (p->c_out % 8 != 0) return fail(NUMBAT_ERR_UNSUPPORTED, "c_out = %d is not a multiple of 8", p->c_out);
+  if (p->c_in % 8 != 0 && p->c_in > 8)
+    return fail(NUMBAT_ERR_UNSUPPORTED, "c_in = %d: only multiples of 8, or fewer than 8 channels", p->c_in);
+  d->n = p->n;
+  d->h = p->h;
+  d->w = p->w;
+  d->ci = p->c_in;
+  d->co = p->c_out;
+  d->kh = p->kh;
+  d->kw = p->kw;
+  d->sh = p->stride_h;
+  d->sw = p->stride_w;
+  d->ph = p->pad_h;
+  d->pw = p->pad_w;
+  d->ho = (int32_t)(hp / p->stride_h + 1);
+  d->wo = (int32_t)(wp / p->stride_w + 1);
+  d->x_pix = p->x_pixel_stride ? p->x_pixel_stride : p->c_in;
+  d->y_pix = p->y_pixel_stride ? p->y_pixel_stride : p->c_out;
+  if (d->x_pix < d->ci) return fail(NUMBAT_ERR_BAD_DESC, "x_pixel_stride %lld < c_in %d", (long long)d->x_pix, d->ci);
+  if (d->y_pix < d->co) return fail(NUMBAT_ERR_BAD_DESC, "y_pixel_stride %lld < c_out %d", (long long)d->y_pix, d->co);
+  if (d->ci % 8 == 0 && d->x_pix % 8 != 0)
+    return fail(NUMBAT_ERR_ALIGN, "x_pixel_stride %lld is not a multiple of 8", (long long)d->x_pix);
+  if (d->y_pix % 8 != 0) return fail(NUMBAT_ERR_ALIGN, "y_pixel_stride %lld is not a multiple of 8", (long long)d->y_pix);
+  d->m = (int64_t)d->n * d->ho * d->wo;
+  const int64_t npix_in = (int64_t)d->n * d->h * d->w;
+  if (d->m > kMaxIndex || npix_in > kMaxIndex)
+    return fail(NUMBAT_ERR_UNSUPPORTED, "more than 2^31-1 pixels (in %lld, out %lld)", (long long)npix_in,
+                (long long)d->m);
+  if ((int64_t)d->co * d->kh * d->kw * d->ci > kMaxIndex) return fail(NUMBAT_ERR_UNSUPPORTED, "weight too large");
+  return NUMBAT_OK;
+}
+
+TileCfg fwd_tile(const ConvDesc& d) { return igemm_pick(d.m, d.co, d.ci); }
+
+size_t fwd_ws(const ConvDesc& d) {
+  const TileCfg t = fwd_tile(d);
+  const int64_t mt = (d.m + t.bm - 1) / t.bm;
+  return round_up((size_t)mt * d.co * sizeof(float2), 256);
+}
+
+size_t bwd_data_ws(const ConvDesc& d) { return round_up((size_t)d.kh * d.kw * d.ci * d.co * 2, 256); }
+
+size_t bwd_weight_ws(const ConvDesc& d, int* splits, int64_t* rps) {
+  const int ktot = d.kh * d.kw * d.ci;
+  int64_t r = 0;
+  const int s = wgrad_pick_splits(d.m, d.co, ktot, &r);
+  if (splits) *splits = s;
+  if (rps) *rps = r;
+  return s > 1 ? round_up((size_t)s * d.co * ktot * sizeof(float), 256) : 0;
+}
+
+// ---------------------------------------------------------------------------
+struct BnDesc {
+  BnArgs a;
+};
+
+numbat_status check_bn(const numbat_bn_problem* p, BnDesc* d) {
+  if (p == nullptr) return fail(NUMBAT_ERR_NULL, "problem descriptor is NULL");
+  if (p->struct_size != sizeof(numbat_bn_problem))
+    return fail(NUMBAT_ERR_VERSION, "numbat_bn_problem.struct_size is %u, this library expects %zu", p->struct_size,
+                sizeof(numbat_bn_problem));
+  if (p->c < 1 || p->m < 2) return fail(NUMBAT_ERR_BAD_DESC, "need c >= 1 and m >= 2 (c=%d m=%lld)", p->c, (long long)p->m);
+  if (!(p->eps >= 0.0f)) return fail(NUMBAT_ERR_BAD_DESC, "eps must be >= 0");
+  if (!(p->momentum >= 0.0f && p->momentum <= 1.0f)) return fail(NUMBAT_ERR_BAD_DESC, "momentum must be in [0, 1]");
+  if (p->c % 8 != 0) return fail(NUMBAT_ERR_UNSUPPORTED, "c = %d is not a multiple of 8", p->c);
+  if (p->c > 2048) return fail(NUMBAT_ERR_UNSUPPORTED, "c = %d exceeds 2048", p->c);
+  if (p->m * (p->c / 8) > kMaxIndex) return fail(NUMBAT_ERR_UNSUPPORTED, "m * c / 8 exceeds 2^31-1");
+  BnArgs& a = d->a;
+  a.c = p->c;
+  a.m = p->m;
+  a.eps = p->eps;
+  a.momentum = p->momentum;
+  a.y_pix = p->y_pixel_stride ? p->y_pixel_stride : p->c;
+  a.a_pix = p->a_pixel_stride ? p->a_pixel_stride : p->c;
+  a.r_pix = p->r_pixel_stride ? p->r_pixel_stride : p->c;
+  a.dy_pix = p->dy_pixel_stride ? p->dy_pixel_stride : p->c;
+  const int64_t s[4] = {a.y_pix, a.a_pix, a.r_pix, a.dy_pix};
+  for (int i = 0; i < 4; ++i) {
+    if (s[i] < a.c) return fail(NUMBAT_ERR_BAD_DESC, "a pixel stride (%lld) is smaller than c (%d)", (long long)s[i], a.c);
+    if (s[i] % 8 != 0) return fail(NUMBAT_ERR_ALIGN, "pixel stride %lld is not a multiple of 8", (long long)s[i]);
+  }
+  return NUMBAT_OK;
+}
+
+size_t bn_fwd_ws(const BnDesc& d) {
+  const int nb = bn_reduce_blocks(d.a.m, d.a.c);
+  return round_up((size_t)nb * d.a.c * sizeof(float2), 256) + round_up(2 * d.a.c * sizeof(float), 256);
+}
+
+size_t bn_bwd_ws(const BnDesc& d) {
+  const int nb = bn_reduce_blocks(d.a.m, d.a.c);
+  return round_up((size_t)nb * d.a.c * sizeof(float2), 256) + round_up(3 * d.a.c * sizeof(float), 256);
+}
+
+numbat_status check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return NUMBAT_OK;
+  if (ws == nullptr) return fail(NUMBAT_ERR_WORKSPACE, "workspace of %zu bytes required, got NULL", need);
+  if (have < need) return fail(NUMBAT_ERR_WORKSPACE, "workspace of %zu bytes required, got %zu", need, have);
+  if (!aligned16(ws)) return fail(NUMBAT_ERR_ALIGN, "workspace must be 16-byte aligned");
+  return NUMBAT_OK;
+}
+
+IgemmArgs base_args() {
+  IgemmArgs a;
+  std::memset(&a, 0, sizeof a);
+  return a;
+}
+
+void set_grid(IgemmArgs& a, int nimg, int gh, int gw) {
+  a.nimg = nimg;
+  a.gh = gh;
+  a.gw = gw;
+  a.m = nimg * gh * gw;
+  a.div_gw = make_fastdiv((uint32_t)gw);
+  a.div_ghw = make_fastdiv((uint32_t)(gh * gw));
+}
+
+}  // namespace
+
+extern "C" {
+
+uint32_t numbat_abi_version(void) { return NUMBAT_ABI_VERSION; }
+
+const char* numbat_last_error(void) { return g_err.c_str(); }
+
+const char* numbat_status_string(numbat_status s) {
+  switch (s) {
+    case NUMBAT_OK: return "NUMBAT_OK";
+    case NUMBAT_ERR_NULL: return "NUMBAT_ERR_NULL";
+    case NUMBAT_ERR_BAD_DESC: return "NUMBAT_ERR_BAD_DESC";
+    case NUMBAT_ERR_UNSUPPORTED: return "NUMBAT_ERR_UNSUPPORTED";
+    case NUMBAT_ERR_ALIGN: return "NUMBAT_ERR_ALIGN";
+    case NUMBAT_ERR_WORKSPACE: return "NUMBAT_ERR_WORKSPACE";
+    case NUMBAT_ERR_DEVICE: return "NUMBAT_ERR_DEVICE";
+    case NUMBAT_ERR_VERSION: return "NUMBAT_ERR_VERSION";
+  }
+  return "NUMBAT_STATUS_UNKNOWN";
+}
+
+numbat_status numbat_conv_output_shape(const numbat_conv_problem* p, int32_t* ho, int32_t* wo) {
+  ConvDesc d;
+  numbat_status st = check_conv(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (ho == nullptr || wo == nullptr) return fail(NUMBAT_ERR_NULL, "ho / wo output pointer is NULL");
+  *ho = d.ho;
+  *wo = d.wo;
+  return ok();
+}
+
+numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* bytes) {
+  if (bytes == nullptr) return fail(NUMBAT_ERR_NULL, "bytes output pointer is NULL");
+  switch (op) {
+    case NUMBAT_OP_CONV_FWD:
+    case NUMBAT_OP_CONV_BWD_DATA:
+    case NUMBAT_OP_CONV_BWD_WEIGHT: {
+      ConvDesc d;
+      numbat_status st = check_conv(static_cast<const numbat_conv_problem*>(problem), &d);
+      if (st != NUMBAT_OK) return st;
+      *bytes = op == NUMBAT_OP_CONV_FWD ? fwd_ws(d) : op == NUMBAT_OP_CONV_BWD_DATA ? bwd_data_ws(d)
+                                                                                    : bwd_weight_ws(d, nullptr, nullptr);
+      return ok();
+    }
+    case NUMBAT_OP_BN_SILU_FWD:
+    case NUMBAT_OP_BN_SILU_BWD: {
+      BnDesc d;
+      numbat_status st = check_bn(static_cast<const numbat_bn_problem*>(problem), &d);
+      if (st != NUMBAT_OK) return st;
+      *bytes = op == NUMBAT_OP_BN_SILU_FWD ? bn_fwd_ws(d) : bn_bwd_ws(d);
+      return ok();
+    }
+  }
+  return fail(NUMBAT_ERR_BAD_DESC, "unknown op %d", (int)op);
+}
+
+numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
+                              float* batch_stats, void* ws, size_t ws_bytes, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (x == nullptr || w == nullptr || y == nullptr) return fail(NUMBAT_ERR_NULL, "x, w and y are required");
+  const bool vec_in = d.ci % 8 == 0;
+  if ((vec_in && (!aligned16(x) || !aligned16(w))) || !aligned16(y))
+    return fail(NUMBAT_ERR_ALIGN, "x, w, y must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w)) & 1u)
+    return fail(NUMBAT_ERR_ALIGN, "x and w must be 2-byte aligned");
+  if (batch_stats != nullptr && (reinterpret_cast<uintptr_t>(batch_stats) & 3u))
+    return fail(NUMBAT_ERR_ALIGN, "batch_stats must be 4-byte aligned");
+  const size_t need = batch_stats ? fwd_ws(d) : 0;
+  st = check_ws(ws, ws_bytes, need);
+  if (st != NUMBAT_OK) return st;
+
+  const TileCfg t = fwd_tile(d);
+  IgemmArgs a = base_args();
+  a.src = static_cast<const bf16_t*>(x);
+  a.src_pix = d.x_pix;
+  a.hs = d.h;
+  a.ws = d.w;
+  a.cs = d.ci;
+  a.wt = static_cast<const bf16_t*>(w);
+  a.nout = d.co;
+  a.taps = d.kh * d.kw;
+  a.ktot = a.taps * d.ci;
+  a.gstride_h = d.sh;
+  a.gstride_w = d.sw;
+  for (int r = 0; r < d.kh; ++r)
+    for (int s = 0; s < d.kw; ++s) {
+      const int dh = r - d.ph, dw = s - d.pw;
+      a.off[r * d.kw + s] = (int32_t)((uint32_t)(uint16_t)(int16_t)dh | ((uint32_t)dw << 16));
+    }
+  set_grid(a, d.n, d.ho, d.wo);
+  a.dst = static_cast<bf16_t*>(y);
+  a.dst_pix = d.y_pix;
+  a.hd = d.ho;
+  a.wd = d.wo;
+  a.dstep_h = a.dstep_w = 1;
+  a.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = igemm_launch(a, t, s);
+  if (e != hipSuccess) return hip_fail(e, "conv forward launch");
+  if (batch_stats) {
+    const int mt = (int)((d.m + t.bm - 1) / t.bm);
+    e = stats_merge_launch(static_cast<const float2*>(ws), mt, t.bm, d.m, d.co, batch_stats, s);
+    if (e != hipSuccess) return hip_fail(e, "batch statistics merge launch");
+  }
+  return ok();
+}
+
+numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
+                                   int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (dy == nullptr || w == nullptr || dx == nullptr) return fail(NUMBAT_ERR_NULL, "dy, w and dx are required");
+  if (!aligned16(dy)) return fail(NUMBAT_ERR_ALIGN, "dy must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(w) | reinterpret_cast<uintptr_t>(dx)) & 1u)
+    return fail(NUMBAT_ERR_ALIGN, "w and dx must be 2-byte aligned");
+  st = check_ws(ws, ws_bytes, bwd_data_ws(d));
+  if (st != NUMBAT_OK) return st;
+
+  // stride phases (a, b): input rows h = a + sh*i read output rows p = i + (a + ph - r) / sh
+  PhaseTaps ph[16];
+  int first[16];
+  int nphase = 0, total = 0;
+  int offh[16][kMaxTaps], offw[16][kMaxTaps];
+  for (int pa = 0; pa < d.sh; ++pa)
+    for (int pb = 0; pb < d.sw; ++pb) {
+      PhaseTaps& f = ph[nphase];
+      f.count = 0;
+      for (int r = 0; r < d.kh; ++r) {
+        const int th = pa + d.ph - r;
+        if (((th % d.sh) + d.sh) % d.sh != 0) continue;
+        for (int s = 0; s < d.kw; ++s) {
+          const int tw = pb + d.pw - s;
+          if (((tw % d.sw) + d.sw) % d.sw != 0) continue;
+          f.r[f.count] = r;
+          f.s[f.count] = s;
+          offh[nphase][f.count] = (th - ((th % d.sh) + d.sh) % d.sh) / d.sh;  // exact
+          offw[nphase][f.count] = (tw - ((tw % d.sw) + d.sw) % d.sw) / d.sw;
+          ++f.count;
+        }
+      }
+      first[nphase] = total * d.ci * d.co;
+      total += f.count;
+      ++nphase;
+    }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  bf16_t* wt = static_cast<bf16_t*>(ws);
+  hipError_t e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, first, ph, nphase, s);
+  if (e != hipSuccess) return hip_fail(e, "data-gradient weight re-layout launch");
+  int f = 0;
+  for (int pa = 0; pa < d.sh; ++pa)
+    for (int pb = 0; pb < d.sw; ++pb, ++f) {
+      const int gh = pa < d.h ? (d.h - pa + d.sh - 1) / d.sh : 0;
+      const int gw = pb < d.w ? (d.w - pb + d.sw - 1) / d.sw : 0;
+      if (gh == 0 || gw == 0) continue;
+      IgemmArgs a = base_args();
+      a.src = static_cast<const bf16_t*>(dy);
+      a.src_pix = d.y_pix;
+      a.hs = d.ho;
+      a.ws = d.wo;
+      a.cs = d.co;
+      a.wt = wt + first[f];
+      a.nout = d.ci;
+      a.taps = ph[f].count;
+      a.ktot = a.taps * d.co;
+      a.gstride_h = a.gstride_w = 1;
+      for (int t = 0; t < ph[f].count; ++t)
+        a.off[t] = (int32_t)((uint32_t)(uint16_t)(int16_t)offh[f][t] | ((uint32_t)offw[f][t] << 16));
+      set_grid(a, d.n, gh, gw);
+      a.dst = static_cast<bf16_t*>(dx);
+      a.dst_pix = d.x_pix;
+      a.hd = d.h;
+      a.wd = d.w;
+      a.dstep_h = d.sh;
+      a.dstep_w = d.sw;
+      a.doff_h = pa;
+      a.doff_w = pb;
+      a.accumulate = accumulate ? 1 : 0;
+      const TileCfg t = igemm_pick(a.m, a.nout, a.cs);
+      e = igemm_launch(a, t, s);
+      if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+    }
+  return ok();
+}
+
+numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x, const void* dy, float* dw,
+                                     int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (x == nullptr || dy == nullptr || dw == nullptr) return fail(NUMBAT_ERR_NULL, "x, dy and dw are required");
+  if ((d.ci % 8 == 0 && !aligned16(x)) || !aligned16(dy)) return fail(NUMBAT_ERR_ALIGN, "x and dy must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(x) & 1u) || (reinterpret_cast<uintptr_t>(dw) & 3u))
+    return fail(NUMBAT_ERR_ALIGN, "x must be 2-byte and dw 4-byte aligned");
+  int splits = 1;
+  int64_t rps = 0;
+  const size_t need = bwd_weight_ws(d, &splits, &rps);
+  st = check_ws(ws, ws_bytes, need);
+  if (st != NUMBAT_OK) return st;
+  WgradArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.x = static_cast<const bf16_t*>(x);
+  a.x_pix = d.x_pix;
+  a.dy = static_cast<const bf16_t*>(dy);
+  a.dy_pix = d.y_pix;
+  a.n = d.n;
+  a.h = d.h;
+  a.w = d.w;
+  a.ci = d.ci;
+  a.co = d.co;
+  a.kh = d.kh;
+  a.kw = d.kw;
+  a.sh = d.sh;
+  a.sw = d.sw;
+  a.ph = d.ph;
+  a.pw = d.pw;
+  a.ho = d.ho;
+  a.wo = d.wo;
+  a.m = d.m;
+  a.ktot = d.kh * d.kw * d.ci;
+  a.splits = splits;
+  a.rows_per_split = rps;
+  a.out = splits > 1 ? static_cast<float*>(ws) : dw;
+  a.accumulate = accumulate ? 1 : 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = wgrad_launch(a, s);
+  if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
+  if (splits > 1) {
+    e = splitk_reduce_launch(static_cast<const float*>(ws), splits, (int64_t)d.co * a.ktot, dw, a.accumulate, s);
+    if (e != hipSuccess) return hip_fail(e, "weight-gradient reduction launch");
+  }
+  return ok();
+}
+
+numbat_status numbat_bn_silu_fwd(const numbat_bn_problem* p, const void* y, const float* batch_stats,
+                                 const float* gamma, const float* beta, const void* residual, void* out,
+                                 float* save_mean, float* save_rstd, float* running_mean, float* running_var,
+                                 void* ws, size_t ws_bytes, void* stream) {
+  BnDesc d;
+  numbat_status st = check_bn(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (y == nullptr || gamma == nullptr || beta == nullptr || out == nullptr || save_mean == nullptr ||
+      save_rstd == nullptr)
+    return fail(NUMBAT_ERR_NULL, "y, gamma, beta, out, save_mean and save_rstd are required");
+  if ((running_mean == nullptr) != (running_var == nullptr))
+    return fail(NUMBAT_ERR_NULL, "running_mean and running_var must both be given or both be NULL");
+  if (!aligned16(y) || !aligned16(out) || (residual && !aligned16(residual)))
+    return fail(NUMBAT_ERR_ALIGN, "y, out and residual must be 16-byte aligned");
+  const size_t need = batch_stats ? 0 : bn_fwd_ws(d);
+  st = check_ws(ws, ws_bytes, need);
+  if (st != NUMBAT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float* mv = batch_stats;
+  if (mv == nullptr) {
+    const int nb = bn_reduce_blocks(d.a.m, d.a.c);
+    float* part = static_cast<float*>(ws);
+    float* mean_var = reinterpret_cast<float*>(static_cast<char*>(ws) + round_up((size_t)nb * d.a.c * sizeof(float2), 256));
+    hipError_t e = bn_stats_launch(d.a, static_cast<const bf16_t*>(y), part, nb, mean_var, s);
+    if (e != hipSuccess) return hip_fail(e, "batch statistics launch");
+    mv = mean_var;
+  }
+  hipError_t e = bn_fwd_launch(d.a, static_cast<const bf16_t*>(y), mv, gamma, beta, static_cast<const bf16_t*>(residual),
+                               static_cast<bf16_t*>(out), save_mean, save_rstd, running_mean, running_var, s);
+  if (e != hipSuccess) return hip_fail(e, "BN+SiLU forward launch");
+  return ok();
+}
+
+numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, const void* y,
+                                 const float* save_mean, const float* save_rstd, const float* gamma,
+                                 const float* beta, void* dy, float* dgamma, float* dbeta, void* residual_grad,
+                                 void* ws, size_t ws_bytes, void* stream) {
+  BnDesc d;
+  numbat_status st = check_bn(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (g == nullptr || y == nullptr || save_mean == nullptr || save_rstd == nullptr || gamma == nullptr ||
+      beta == nullptr || dy == nullptr || dgamma == nullptr || dbeta == nullptr)
+    return fail(NUMBAT_ERR_NULL, "g, y, save_mean, save_rstd, gamma, beta, dy, dgamma and dbeta are required");
+  if (!aligned16(g) || !aligned16(y) || !aligned16(dy) || (residual_grad && !aligned16(residual_grad)))
+    return fail(NUMBAT_ERR_ALIGN, "g, y, dy and residual_grad must be 16-byte aligned");
+  st = check_ws(ws, ws_bytes, bn_bwd_ws(d));
+  if (st != NUMBAT_OK) return st;
+  const int nb = bn_reduce_blocks(d.a.m, d.a.c);
+  float* part = static_cast<float*>(ws);
+  float* coef = reinterpret_cast<float*>(static_cast<char*>(ws) + round_up((size_t)nb * d.a.c * sizeof(float2), 256));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = bn_bwd_launch(d.a, static_cast<const bf16_t*>(g), static_cast<const bf16_t*>(y), save_mean, save_rstd,
+                               gamma, beta, static_cast<bf16_t*>(dy), dgamma, dbeta, static_cast<bf16_t*>(residual_grad),
+                               part, nb, coef, s);
+  if (e != hipSuccess) return hip_fail(e, "BN+SiLU backward launch");
+  return ok();
+}
+
+}  // extern "C"

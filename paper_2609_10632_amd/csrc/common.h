@@ -1,0 +1,77 @@
+// Device-side helpers shared by the gfx950 kernels of the conv / BN / SiLU path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace numbat {
+
+typedef uint16_t bf16_t;  // bf16 bit pattern
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// bf16 bits -> fp32 (exact)
+__device__ __forceinline__ float bf2f(uint32_t h) { return __uint_as_float(h << 16); }
+
+// fp32 -> bf16 bits, round to nearest even, NaN kept (quiet)
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return f2bf(lo) | (f2bf(hi) << 16); }
+
+// unpack a 16-byte vector of 8 bf16 into fp32
+__device__ __forceinline__ void unpack8(const uint4& v, float f[8]) {
+  f[0] = bf2f(v.x & 0xffffu); f[1] = bf2f(v.x >> 16);
+  f[2] = bf2f(v.y & 0xffffu); f[3] = bf2f(v.y >> 16);
+  f[4] = bf2f(v.z & 0xffffu); f[5] = bf2f(v.z >> 16);
+  f[6] = bf2f(v.w & 0xffffu); f[7] = bf2f(v.w >> 16);
+}
+
+__device__ __forceinline__ uint4 pack8(const float f[8]) {
+  uint4 v;
+  v.x = pack2(f[0], f[1]);
+  v.y = pack2(f[2], f[3]);
+  v.z = pack2(f[4], f[5]);
+  v.w = pack2(f[6], f[7]);
+  return v;
+}
+
+// Unsigned division by a run-time constant d >= 1 (Granlund-Montgomery), exact for n < 2^31.
+struct FastDiv {
+  uint32_t d, mul, shift;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  uint32_t s = 0;
+  while ((1ull << s) < d) ++s;
+  f.shift = s;
+  f.mul = (uint32_t)((((1ull << 32) * ((1ull << s) - d)) / d) + 1);
+  return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  uint32_t t = __umulhi(n, f.mul);
+  return (t + n) >> f.shift;
+}
+
+// 16x16x32 bf16 MFMA, fp32 accumulate: D = A(16x32) * B(32x16) + C.
+// Lane l supplies A row (l % 16) and B column (l % 16), each with the 8 reduction
+// elements of group (l / 16); it receives D rows 4*(l/16) .. +3 of column (l % 16).
+__device__ __forceinline__ f32x4 mfma16x16x32(const uint4& a, const uint4& b, f32x4 c) {
+  bf16x8 av, bv;
+  __builtin_memcpy(&av, &a, 16);
+  __builtin_memcpy(&bv, &b, 16);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float sigmoidf_fast(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+}  // namespace numbat

@@ -1,0 +1,96 @@
+// Host-side launch interface between the C ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace numbat {
+
+constexpr int kMaxTaps = 25;
+
+// One implicit GEMM D[M][N] = A[M][K] * B[N][K]^T where
+//   row m   = (img, gi, gj) on a gh x gw grid per image,
+//   col     = output channel of the GEMM (N = nout),
+//   k       = (tap, c), c < cs, K = taps * cs,
+//   A[m][k] = src[img, gi*gstride_h + off_h[tap], gj*gstride_w + off_w[tap], c]  (0 outside hs x ws),
+//   B[n][k] = wt[n * ktot + k],
+// and D is written (bf16) to dst[img, gi*dstep_h + doff_h, gj*dstep_w + doff_w, col].
+// The forward convolution and every stride phase of the data gradient are such GEMMs.
+struct IgemmArgs {
+  const bf16_t* src;
+  int64_t src_pix;
+  int32_t hs, ws, cs;
+  const bf16_t* wt;
+  int32_t nout, taps, ktot;
+  int32_t gstride_h, gstride_w;
+  int32_t off[kMaxTaps];  // (off_h & 0xffff) | (off_w << 16), both signed 16-bit
+  int32_t nimg, gh, gw, m;
+  FastDiv div_gw, div_ghw;
+  bf16_t* dst;
+  int64_t dst_pix;
+  int32_t hd, wd;
+  int32_t dstep_h, dstep_w, doff_h, doff_w;
+  int32_t accumulate;
+  float2* stats_part;  // [m tiles][nout] (tile mean, tile M2) or nullptr
+};
+
+struct TileCfg {
+  int bm, bn;
+  int id;  // instantiation id
+};
+
+// choose a tile for an igemm problem (depends on the problem only)
+TileCfg igemm_pick(int64_t m, int nout, int cs);
+hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s);
+
+// merge per-tile (mean, M2) partials into batch mean / biased variance, fixed order
+hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,
+                              hipStream_t s);
+
+// dgrad weight re-layout: for each stride phase, wt[c][tap][o] = w[o][r][s][c]
+struct PhaseTaps {
+  int count;
+  int r[kMaxTaps], s[kMaxTaps];
+};
+hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int kw, int ci, const int* phase_first,
+                                const PhaseTaps* phases, int nphase, hipStream_t s);
+
+// weight gradient: split-K implicit GEMM and its fixed-order reduction
+struct WgradArgs {
+  const bf16_t* x;
+  int64_t x_pix;
+  const bf16_t* dy;
+  int64_t dy_pix;
+  int32_t n, h, w, ci, co, kh, kw, sh, sw, ph, pw, ho, wo;
+  int64_t m;            // n * ho * wo
+  int32_t ktot;         // kh * kw * ci
+  int32_t splits;       // number of reduction ranges
+  int64_t rows_per_split;  // multiple of the reduction step
+  float* out;           // splits == 1: dw (accumulate honoured); else partials [splits][co][ktot]
+  int32_t accumulate;
+};
+int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split);
+hipError_t wgrad_launch(const WgradArgs& a, hipStream_t s);
+hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
+                                hipStream_t s);
+
+// BN + SiLU
+struct BnArgs {
+  int32_t c;
+  int64_t m;
+  float eps, momentum;
+  int64_t y_pix, a_pix, r_pix, dy_pix;
+};
+int bn_reduce_blocks(int64_t m, int c);
+hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int nblocks, float* mean_var,
+                           hipStream_t s);
+hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var, const float* gamma,
+                         const float* beta, const bf16_t* res, bf16_t* out, float* save_mean, float* save_rstd,
+                         float* run_mean, float* run_var, hipStream_t s);
+hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,
+                         const float* save_rstd, const float* gamma, const float* beta, bf16_t* dy, float* dgamma,
+                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, float* coef, hipStream_t s);
+
+}  // namespace numbat

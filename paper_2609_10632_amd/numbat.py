@@ -1,0 +1,189 @@
+"""Thin Python binding of the C ABI in ``include/numbat_conv.h`` (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and does nothing but
+turn Python arguments into C arguments: tensors become device pointers (their
+``data_ptr()``), ``None`` becomes NULL, the stream defaults to PyTorch's current
+stream.  All computation happens in the gfx950 kernels of ``libnumbat_conv.so``;
+there is no fallback: if the library is missing, importing it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnumbat_conv.so")
+
+NUMBAT_ABI_VERSION = 1
+
+OK, ERR_NULL, ERR_BAD_DESC, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE, ERR_DEVICE, ERR_VERSION = range(8)
+OP_CONV_FWD, OP_CONV_BWD_DATA, OP_CONV_BWD_WEIGHT, OP_BN_SILU_FWD, OP_BN_SILU_BWD = range(5)
+
+EXPORTED = (
+    "numbat_abi_version", "numbat_last_error", "numbat_status_string", "numbat_conv_output_shape",
+    "numbat_workspace_size", "numbat_conv_fwd", "numbat_conv_bwd_data", "numbat_conv_bwd_weight",
+    "numbat_bn_silu_fwd", "numbat_bn_silu_bwd",
+)
+
+
+class numbat_conv_problem(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32)] + [
+        (f, ctypes.c_int32)
+        for f in ("n", "h", "w", "c_in", "c_out", "kh", "kw", "stride_h", "stride_w", "pad_h", "pad_w")
+    ] + [("x_pixel_stride", ctypes.c_int64), ("y_pixel_stride", ctypes.c_int64)]
+
+
+class numbat_bn_problem(ctypes.Structure):
+    _fields_ = [
+        ("struct_size", ctypes.c_uint32), ("c", ctypes.c_int32), ("m", ctypes.c_int64), ("eps", ctypes.c_float),
+        ("momentum", ctypes.c_float), ("y_pixel_stride", ctypes.c_int64), ("a_pixel_stride", ctypes.c_int64),
+        ("r_pixel_stride", ctypes.c_int64), ("dy_pixel_stride", ctypes.c_int64),
+    ]
+
+
+class NumbatError(RuntimeError):
+    def __init__(self, status: int, name: str, detail: str, call: str):
+        super().__init__(f"{call}: {name}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load the HIP library.  Raises if it has not been built (no fallback path exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                              "(python -m paper_2609_10632_amd.build); there is no non-HIP fallback")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, S = ctypes.c_void_p, ctypes.c_size_t
+        CP, BP = ctypes.POINTER(numbat_conv_problem), ctypes.POINTER(numbat_bn_problem)
+        sig = {
+            "numbat_abi_version": (ctypes.c_uint32, []),
+            "numbat_last_error": (ctypes.c_char_p, []),
+            "numbat_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "numbat_conv_output_shape": (ctypes.c_int, [CP, ctypes.POINTER(ctypes.c_int32),
+                                                         ctypes.POINTER(ctypes.c_int32)]),
+            "numbat_workspace_size": (ctypes.c_int, [ctypes.c_int, P, ctypes.POINTER(S)]),
+            "numbat_conv_fwd": (ctypes.c_int, [CP, P, P, P, P, P, S, P]),
+            "numbat_conv_bwd_data": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
+            "numbat_conv_bwd_weight": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
+            "numbat_bn_silu_fwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
+            "numbat_bn_silu_bwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _nbytes(t) -> int:
+    if t is None:
+        return 0
+    if isinstance(t, int):
+        raise TypeError("pass the workspace as a tensor, or as (pointer, size) through ws_bytes")
+    return t.numel() * t.element_size()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+
+    if not torch.cuda.is_available():
+        return None  # NULL stream; only validation failures can happen without a GPU
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(status: int, call: str) -> None:
+    if status != OK:
+        lib = load()
+        raise NumbatError(status, lib.numbat_status_string(status).decode(), lib.numbat_last_error().decode(), call)
+
+
+def conv_problem(n, h, w, c_in, c_out, kh, kw=None, stride=1, pad=None, x_pixel_stride=0, y_pixel_stride=0):
+    kw = kh if kw is None else kw
+    pad = kh // 2 if pad is None else pad
+    return numbat_conv_problem(ctypes.sizeof(numbat_conv_problem), n, h, w, c_in, c_out, kh, kw, stride, stride, pad,
+                               pad, x_pixel_stride, y_pixel_stride)
+
+
+def bn_problem(m, c, eps=1e-3, momentum=0.03, y_pixel_stride=0, a_pixel_stride=0, r_pixel_stride=0,
+               dy_pixel_stride=0):
+    return numbat_bn_problem(ctypes.sizeof(numbat_bn_problem), c, m, eps, momentum, y_pixel_stride, a_pixel_stride,
+                             r_pixel_stride, dy_pixel_stride)
+
+
+def numbat_abi_version() -> int:
+    return int(load().numbat_abi_version())
+
+
+def numbat_last_error() -> str:
+    return load().numbat_last_error().decode()
+
+
+def numbat_status_string(status: int) -> str:
+    return load().numbat_status_string(status).decode()
+
+
+def numbat_conv_output_shape(p: numbat_conv_problem):
+    ho, wo = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().numbat_conv_output_shape(ctypes.byref(p), ctypes.byref(ho), ctypes.byref(wo)),
+           "numbat_conv_output_shape")
+    return ho.value, wo.value
+
+
+def numbat_workspace_size(op: int, p) -> int:
+    n = ctypes.c_size_t()
+    _check(load().numbat_workspace_size(op, ctypes.cast(ctypes.pointer(p), ctypes.c_void_p), ctypes.byref(n)),
+           "numbat_workspace_size")
+    return n.value
+
+
+def numbat_conv_fwd(p, x, w, y, batch_stats=None, ws=None, stream=None, ws_bytes=None):
+    _check(load().numbat_conv_fwd(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(y), _ptr(batch_stats), _ptr(ws),
+                                  _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+           "numbat_conv_fwd")
+
+
+def numbat_conv_bwd_data(p, dy, w, dx, accumulate=False, ws=None, stream=None, ws_bytes=None):
+    _check(load().numbat_conv_bwd_data(ctypes.byref(p), _ptr(dy), _ptr(w), _ptr(dx), int(bool(accumulate)), _ptr(ws),
+                                       _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+           "numbat_conv_bwd_data")
+
+
+def numbat_conv_bwd_weight(p, x, dy, dw, accumulate=False, ws=None, stream=None, ws_bytes=None):
+    _check(load().numbat_conv_bwd_weight(ctypes.byref(p), _ptr(x), _ptr(dy), _ptr(dw), int(bool(accumulate)),
+                                         _ptr(ws), _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+           "numbat_conv_bwd_weight")
+
+
+def numbat_bn_silu_fwd(p, y, batch_stats, gamma, beta, residual, out, save_mean, save_rstd, running_mean=None,
+                       running_var=None, ws=None, stream=None, ws_bytes=None):
+    _check(load().numbat_bn_silu_fwd(ctypes.byref(p), _ptr(y), _ptr(batch_stats), _ptr(gamma), _ptr(beta),
+                                     _ptr(residual), _ptr(out), _ptr(save_mean), _ptr(save_rstd), _ptr(running_mean),
+                                     _ptr(running_var), _ptr(ws), _nbytes(ws) if ws_bytes is None else ws_bytes,
+                                     _stream(stream)),
+           "numbat_bn_silu_fwd")
+
+
+def numbat_bn_silu_bwd(p, g, y, save_mean, save_rstd, gamma, beta, dy, dgamma, dbeta, residual_grad=None, ws=None,
+                       stream=None, ws_bytes=None):
+    _check(load().numbat_bn_silu_bwd(ctypes.byref(p), _ptr(g), _ptr(y), _ptr(save_mean), _ptr(save_rstd), _ptr(gamma),
+                                     _ptr(beta), _ptr(dy), _ptr(dgamma), _ptr(dbeta), _ptr(residual_grad), _ptr(ws),
+                                     _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+           "numbat_bn_silu_bwd")

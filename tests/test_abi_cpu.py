@@ -1,0 +1,124 @@
+"""The C-ABI library without a GPU: it loads, exports every entry point the header
+declares, and every validation failure returns its own status code and detail text
+before anything reaches the HIP runtime (descriptors are refused before any launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_10632_amd import numbat as nb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "numbat_conv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(numbat_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = nb.load()
+    names = declared_functions()
+    assert len(names) == 10
+    assert set(names) == set(nb.EXPORTED)
+    for name in names:
+        assert getattr(lib, name) is not None
+
+
+def test_version_and_status_strings():
+    assert nb.numbat_abi_version() == nb.NUMBAT_ABI_VERSION
+    for code in range(8):
+        assert nb.numbat_status_string(code).startswith("NUMBAT_")
+    assert nb.numbat_status_string(99) == "NUMBAT_STATUS_UNKNOWN"
+
+
+def test_struct_sizes_match_header_layout():
+    # uint32 + 11 int32 + 2 int64 (8-byte aligned) = 4 + 44 + 16 = 64
+    assert ctypes.sizeof(nb.numbat_conv_problem) == 64
+    # uint32, int32, int64, float, float, 4 x int64 = 4 + 4 + 8 + 4 + 4 + 32 = 56
+    assert ctypes.sizeof(nb.numbat_bn_problem) == 56
+
+
+def test_output_shape():
+    assert nb.numbat_conv_output_shape(nb.conv_problem(16, 640, 640, 3, 48, 3, stride=2)) == (320, 320)
+    assert nb.numbat_conv_output_shape(nb.conv_problem(2, 33, 31, 16, 32, 3, stride=2)) == (17, 16)
+    assert nb.numbat_conv_output_shape(nb.conv_problem(2, 20, 20, 64, 64, 1)) == (20, 20)
+
+
+def status_of(fn, *a, **k):
+    try:
+        fn(*a, **k)
+    except nb.NumbatError as e:
+        assert e.detail  # thread-local detail text is set
+        return e.status
+    return nb.OK
+
+
+def test_descriptor_refusals():
+    good = nb.conv_problem(2, 32, 32, 16, 32, 3)
+    bad_version = nb.conv_problem(2, 32, 32, 16, 32, 3)
+    bad_version.struct_size = 60
+    assert status_of(nb.numbat_conv_output_shape, bad_version) == nb.ERR_VERSION
+    for field, val, code in [("n", 0, nb.ERR_BAD_DESC), ("c_out", 12, nb.ERR_UNSUPPORTED),
+                             ("c_in", 12, nb.ERR_UNSUPPORTED), ("stride_h", 0, nb.ERR_BAD_DESC),
+                             ("pad_w", -1, nb.ERR_BAD_DESC), ("kh", 40, nb.ERR_BAD_DESC),
+                             ("x_pixel_stride", 8, nb.ERR_BAD_DESC), ("y_pixel_stride", 36, nb.ERR_ALIGN),
+                             ("stride_w", 5, nb.ERR_UNSUPPORTED), ("pad_h", 3, nb.ERR_UNSUPPORTED)]:
+        p = nb.conv_problem(2, 32, 32, 16, 32, 3)
+        setattr(p, field, val)
+        assert status_of(nb.numbat_conv_output_shape, p) == code, field
+    assert status_of(nb.numbat_conv_output_shape, good) == nb.OK
+    huge = nb.conv_problem(4096, 1024, 1024, 16, 32, 3)
+    assert status_of(nb.numbat_workspace_size, nb.OP_CONV_FWD, huge) == nb.ERR_UNSUPPORTED
+
+
+def test_bn_descriptor_refusals():
+    for field, val, code in [("c", 12, nb.ERR_UNSUPPORTED), ("m", 1, nb.ERR_BAD_DESC), ("eps", -1.0, nb.ERR_BAD_DESC),
+                             ("momentum", 2.0, nb.ERR_BAD_DESC), ("a_pixel_stride", 36, nb.ERR_ALIGN),
+                             ("dy_pixel_stride", 16, nb.ERR_BAD_DESC), ("c", 4096, nb.ERR_UNSUPPORTED)]:
+        p = nb.bn_problem(1000, 32)
+        setattr(p, field, val)
+        assert status_of(nb.numbat_workspace_size, nb.OP_BN_SILU_FWD, p) == code, field
+    p = nb.bn_problem(1000, 32)
+    p.struct_size = 8
+    assert status_of(nb.numbat_workspace_size, nb.OP_BN_SILU_BWD, p) == nb.ERR_VERSION
+
+
+def test_workspace_sizes_depend_only_on_the_problem():
+    p = nb.conv_problem(16, 160, 160, 48, 48, 3)
+    fwd = nb.numbat_workspace_size(nb.OP_CONV_FWD, p)
+    assert fwd >= (16 * 160 * 160 // 128) * 48 * 8
+    assert nb.numbat_workspace_size(nb.OP_CONV_BWD_DATA, p) >= 48 * 9 * 48 * 2
+    assert nb.numbat_workspace_size(nb.OP_CONV_BWD_WEIGHT, p) % 256 == 0
+    assert nb.numbat_workspace_size(nb.OP_BN_SILU_BWD, nb.bn_problem(409600, 48)) > 0
+    assert status_of(nb.numbat_workspace_size, 17, p) == nb.ERR_BAD_DESC
+
+
+def test_entry_points_refuse_before_launch():
+    """Every one of these fails validation, so no HIP call is made (no GPU here)."""
+    p = nb.conv_problem(2, 32, 32, 16, 32, 3)
+    fake = 1 << 20  # 16-byte aligned, never dereferenced
+    assert status_of(nb.numbat_conv_fwd, p, None, fake, fake) == nb.ERR_NULL
+    assert status_of(nb.numbat_conv_fwd, p, fake + 2, fake, fake) == nb.ERR_ALIGN
+    assert status_of(nb.numbat_conv_fwd, p, fake, fake, fake, batch_stats=fake, ws=None) == nb.ERR_WORKSPACE
+    need = nb.numbat_workspace_size(nb.OP_CONV_FWD, p)
+    assert status_of(nb.numbat_conv_fwd, p, fake, fake, fake, batch_stats=fake, ws=fake, ws_bytes=need - 1) \
+        == nb.ERR_WORKSPACE
+    assert status_of(nb.numbat_conv_bwd_data, p, fake, fake, None) == nb.ERR_NULL
+    assert status_of(nb.numbat_conv_bwd_data, p, fake + 8, fake, fake) == nb.ERR_ALIGN
+    assert status_of(nb.numbat_conv_bwd_data, p, fake, fake, fake, ws=None) == nb.ERR_WORKSPACE
+    assert status_of(nb.numbat_conv_bwd_weight, p, fake, fake, fake + 2) == nb.ERR_ALIGN
+    b = nb.bn_problem(2048, 32)
+    assert status_of(nb.numbat_bn_silu_fwd, b, fake, fake, fake, fake, None, fake, None, fake) == nb.ERR_NULL
+    assert status_of(nb.numbat_bn_silu_fwd, b, fake, fake, fake, fake, None, fake, fake, fake,
+                     running_mean=fake) == nb.ERR_NULL
+    assert status_of(nb.numbat_bn_silu_fwd, b, fake + 4, fake, fake, fake, None, fake, fake, fake) == nb.ERR_ALIGN
+    assert status_of(nb.numbat_bn_silu_fwd, b, fake, None, fake, fake, None, fake, fake, fake, ws=None) \
+        == nb.ERR_WORKSPACE
+    assert status_of(nb.numbat_bn_silu_bwd, b, fake, fake, fake, fake, fake, fake, fake, fake, None) == nb.ERR_NULL
+    assert status_of(nb.numbat_bn_silu_bwd, b, fake, fake, fake, fake, fake, fake, fake, fake, fake,
+                     ws=None) == nb.ERR_WORKSPACE
+    # a failing call leaves its detail text; it names the problem
+    assert "workspace" in nb.numbat_last_error()

@@ -1,0 +1,249 @@
+"""GPU parity of each C-ABI entry point against the fp64 oracle, element by element,
+on seeded inputs at sizes that span several tiles and ragged tails."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import ConvShape
+from parity import Inputs, assert_close, assert_stats, f64
+from paper_2609_10632_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if torch.cuda.is_available():
+    from paper_2609_10632_amd import blocks
+    from paper_2609_10632_amd import numbat as nb
+
+EPS = 1e-3
+
+# n, h, w, ci, co, k, s
+CONV_CASES = [
+    (2, 32, 32, 16, 32, 3, 1),
+    (2, 17, 23, 3, 48, 3, 2),
+    (2, 19, 21, 48, 96, 3, 2),
+    (3, 13, 11, 96, 96, 1, 1),
+    (2, 9, 10, 192, 80, 3, 1),
+    (1, 7, 9, 64, 136, 3, 1),
+    (2, 5, 5, 8, 8, 3, 1),
+    (4, 20, 20, 288, 288, 3, 1),
+    (1, 11, 13, 40, 24, 3, 2),
+    (2, 15, 15, 3, 16, 3, 2),
+    (1, 6, 6, 16, 16, 1, 2),
+    (2, 12, 12, 1152, 64, 1, 1),
+]
+
+
+def ids(c):
+    return "n{}h{}w{}ci{}co{}k{}s{}".format(*c)
+
+
+def shape_of(c):
+    n, h, w, ci, co, k, s = c
+    return ConvShape(n, h, w, ci, co, k, k, s, s, k // 2, k // 2)
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)), ids=[ids(c) for c in CONV_CASES])
+def test_conv_fwd_and_stats(ci):
+    c = CONV_CASES[ci]
+    s = shape_of(c)
+    inp = Inputs(100, ci)
+    xb, wb = inp.normal(s.x_shape, synth.T_X), inp.weight(s.co, s.kh, s.ci)
+    blk = blocks.ConvBlock(s.n, s.h, s.w, s.ci, s.co, s.kh, s.sh)
+    x, w = blocks.dev_bf16(xb), blocks.dev_bf16(wb)
+    y = torch.empty(s.y_shape, dtype=torch.bfloat16, device="cuda")
+    stats = torch.empty(2 * s.co, dtype=torch.float32, device="cuda")
+    nb.numbat_conv_fwd(blk.prob, x, w, y, stats, blocks.workspace(blk.ws_fwd))
+    torch.cuda.synchronize()
+    yref = oracle.conv_fwd(f64(xb), f64(wb), s)
+    assert_close(blocks.host_f64(y), yref, "y")
+    mref, vref = oracle.bn_stats(yref)
+    st = blocks.host_f64(stats)
+    assert_stats(st[:s.co], st[s.co:], mref, vref, EPS, "fused batch stats")
+    # without statistics no workspace is needed and y is identical
+    y2 = torch.empty_like(y)
+    nb.numbat_conv_fwd(blk.prob, x, w, y2)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)), ids=[ids(c) for c in CONV_CASES])
+def test_conv_dgrad(ci):
+    c = CONV_CASES[ci]
+    s = shape_of(c)
+    inp = Inputs(101, ci)
+    dyb, wb = inp.normal(s.y_shape, synth.T_DY), inp.weight(s.co, s.kh, s.ci)
+    blk = blocks.ConvBlock(s.n, s.h, s.w, s.ci, s.co, s.kh, s.sh)
+    dx = torch.full(s.x_shape, float("nan"), dtype=torch.bfloat16, device="cuda")
+    ws = blocks.workspace(blk.ws_dgrad)
+    nb.numbat_conv_bwd_data(blk.prob, blocks.dev_bf16(dyb), blocks.dev_bf16(wb), dx, False, ws)
+    torch.cuda.synchronize()
+    ref = oracle.conv_dgrad(f64(dyb), f64(wb), s)
+    assert_close(blocks.host_f64(dx), ref, "dx")
+    # accumulate into an existing gradient
+    x0 = inp.normal(s.x_shape, synth.T_X)
+    dxa = blocks.dev_bf16(x0)
+    nb.numbat_conv_bwd_data(blk.prob, blocks.dev_bf16(dyb), blocks.dev_bf16(wb), dxa, True, ws)
+    torch.cuda.synchronize()
+    assert_close(blocks.host_f64(dxa), ref + f64(x0), "dx accumulate")
+
+
+@pytest.mark.parametrize("ci", range(len(CONV_CASES)), ids=[ids(c) for c in CONV_CASES])
+def test_conv_wgrad(ci):
+    c = CONV_CASES[ci]
+    s = shape_of(c)
+    inp = Inputs(102, ci)
+    xb, dyb = inp.normal(s.x_shape, synth.T_X), inp.normal(s.y_shape, synth.T_DY)
+    blk = blocks.ConvBlock(s.n, s.h, s.w, s.ci, s.co, s.kh, s.sh)
+    dw = torch.full(s.w_shape, float("nan"), dtype=torch.float32, device="cuda")
+    ws = blocks.workspace(blk.ws_wgrad)
+    nb.numbat_conv_bwd_weight(blk.prob, blocks.dev_bf16(xb), blocks.dev_bf16(dyb), dw, False, ws)
+    torch.cuda.synchronize()
+    ref = oracle.conv_wgrad(f64(xb), f64(dyb), s)
+    assert_close(blocks.host_f64(dw), ref, "dw")
+    w0 = np.random.default_rng(ci).standard_normal(s.w_shape).astype(np.float32)
+    dwa = torch.from_numpy(w0).cuda()
+    nb.numbat_conv_bwd_weight(blk.prob, blocks.dev_bf16(xb), blocks.dev_bf16(dyb), dwa, True, ws)
+    torch.cuda.synchronize()
+    assert_close(blocks.host_f64(dwa), ref + w0.astype(np.float64), "dw accumulate")
+
+
+def test_conv_strided_views():
+    """x and y as channel slices of wider tensors (pixel stride > channels)."""
+    s = ConvShape(2, 14, 14, 48, 48, 3, 3, 1, 1, 1, 1)
+    inp = Inputs(103)
+    big = inp.normal((2, 14, 14, 144), synth.T_X)
+    wb = inp.weight(48, 3, 48)
+    blk = blocks.ConvBlock(2, 14, 14, 48, 48, 3, 1, x_pixel_stride=144, y_pixel_stride=96)
+    xbig = blocks.dev_bf16(big)
+    ybig = torch.zeros((2, 14, 14, 96), dtype=torch.bfloat16, device="cuda")
+    nb.numbat_conv_fwd(blk.prob, xbig[..., 48:96], blocks.dev_bf16(wb), ybig[..., 40:88])
+    torch.cuda.synchronize()
+    yref = oracle.conv_fwd(f64(big[..., 48:96]), f64(wb), s)
+    got = blocks.host_f64(ybig)
+    assert_close(got[..., 40:88], yref, "y view")
+    assert np.all(got[..., :40] == 0) and np.all(got[..., 88:] == 0)
+    # data gradient into a slice, weight gradient from slices
+    dyb = inp.normal((2, 14, 14, 96), synth.T_DY)
+    dxbig = torch.zeros((2, 14, 14, 144), dtype=torch.bfloat16, device="cuda")
+    ws = blocks.workspace(blk.ws_bytes())
+    nb.numbat_conv_bwd_data(blk.prob, blocks.dev_bf16(dyb)[..., 40:88], blocks.dev_bf16(wb), dxbig[..., 48:96], False, ws)
+    dw = torch.empty((48, 3, 3, 48), dtype=torch.float32, device="cuda")
+    nb.numbat_conv_bwd_weight(blk.prob, xbig[..., 48:96], blocks.dev_bf16(dyb)[..., 40:88], dw, False, ws)
+    torch.cuda.synchronize()
+    gx = blocks.host_f64(dxbig)
+    assert_close(gx[..., 48:96], oracle.conv_dgrad(f64(dyb[..., 40:88]), f64(wb), s), "dx view")
+    assert np.all(gx[..., :48] == 0) and np.all(gx[..., 96:] == 0)
+    assert_close(blocks.host_f64(dw), oracle.conv_wgrad(f64(big[..., 48:96]), f64(dyb[..., 40:88]), s), "dw views")
+
+
+BN_CASES = [(1000, 8), (4097, 48), (2048, 96), (777, 576), (300, 64)]
+
+
+@pytest.mark.parametrize("m,c", BN_CASES)
+def test_bn_silu_fwd_given_and_standalone_stats(m, c):
+    inp = Inputs(104, c)
+    yb = inp.normal((m, c), synth.T_Y, 0.3, 2.0)
+    gamma = inp.f32_uniform((c,), synth.T_GAMMA, 0.5, 1.5)
+    beta = inp.f32_normal((c,), synth.T_BETA, 0.0, 0.3)
+    mean_in = inp.f32_normal((c,), synth.T_MEAN, 0.0, 0.5)
+    var_in = inp.f32_uniform((c,), synth.T_VAR, 0.5, 2.0)
+    p = nb.bn_problem(m, c, EPS, 0.1)
+    y = blocks.dev_bf16(yb)
+    out = torch.empty_like(y)
+    sm = torch.empty(c, device="cuda")
+    sr = torch.empty(c, device="cuda")
+    stats = blocks.dev_f32(np.concatenate([mean_in, var_in]))
+    g, b = blocks.dev_f32(gamma), blocks.dev_f32(beta)
+    nb.numbat_bn_silu_fwd(p, y, stats, g, b, None, out, sm, sr)
+    torch.cuda.synchronize()
+    ref = oracle.bn_silu_fwd(f64(yb), mean_in.astype(np.float64), var_in.astype(np.float64), gamma.astype(np.float64),
+                             beta.astype(np.float64), EPS)
+    assert_close(blocks.host_f64(out), ref, "out (given stats)")
+    assert np.allclose(blocks.host_f64(sr), 1 / np.sqrt(var_in.astype(np.float64) + EPS), rtol=1e-6)
+
+    # standalone statistics of the bf16 y, plus the running-statistics update
+    rm = torch.full((c,), 0.25, device="cuda")
+    rv = torch.full((c,), 2.0, device="cuda")
+    ws = blocks.workspace(nb.numbat_workspace_size(nb.OP_BN_SILU_FWD, p))
+    nb.numbat_bn_silu_fwd(p, y, None, g, b, None, out, sm, sr, rm, rv, ws)
+    torch.cuda.synchronize()
+    mref, vref = oracle.bn_stats(f64(yb))
+    rstd = blocks.host_f64(sr)
+    assert_stats(blocks.host_f64(sm), 1 / rstd ** 2 - EPS, mref, vref, EPS, "standalone stats")
+    ref = oracle.bn_silu_fwd(f64(yb), mref, vref, gamma.astype(np.float64), beta.astype(np.float64), EPS)
+    assert_close(blocks.host_f64(out), ref, "out (standalone stats)")
+    rmr, rvr = oracle.running_update(np.full(c, 0.25), np.full(c, 2.0), mref, vref, m, 0.1)
+    assert np.allclose(blocks.host_f64(rm), rmr, rtol=1e-5, atol=1e-6)
+    assert np.allclose(blocks.host_f64(rv), rvr, rtol=1e-5)
+
+
+def test_bn_silu_fwd_residual_and_views():
+    m, c = 2000, 96
+    inp = Inputs(105)
+    ybig = inp.normal((m, 192), synth.T_Y)
+    rb = inp.normal((m, 96), synth.T_RES)
+    gamma = inp.f32_uniform((c,), synth.T_GAMMA, 0.5, 1.5)
+    beta = inp.f32_normal((c,), synth.T_BETA, 0.0, 0.3)
+    p = nb.bn_problem(m, c, EPS, y_pixel_stride=192, a_pixel_stride=288, r_pixel_stride=96)
+    outbig = torch.zeros((m, 288), dtype=torch.bfloat16, device="cuda")
+    sm, sr = torch.empty(c, device="cuda"), torch.empty(c, device="cuda")
+    ws = blocks.workspace(nb.numbat_workspace_size(nb.OP_BN_SILU_FWD, p))
+    nb.numbat_bn_silu_fwd(p, blocks.dev_bf16(ybig)[:, 96:], None, blocks.dev_f32(gamma), blocks.dev_f32(beta),
+                          blocks.dev_bf16(rb), outbig[:, 192:], sm, sr, ws=ws)
+    torch.cuda.synchronize()
+    y = f64(ybig[:, 96:])
+    mref, vref = oracle.bn_stats(y)
+    ref = oracle.bn_silu_fwd(y, mref, vref, gamma.astype(np.float64), beta.astype(np.float64), EPS, f64(rb))
+    got = blocks.host_f64(outbig)
+    assert_close(got[:, 192:], ref, "out with residual into a view")
+    assert np.all(got[:, :192] == 0)
+
+
+@pytest.mark.parametrize("m,c", BN_CASES)
+def test_bn_silu_bwd(m, c):
+    inp = Inputs(106, c)
+    yb = inp.normal((m, c), synth.T_Y, -0.2, 1.5)
+    gb = inp.normal((m, c), synth.T_G)
+    r0 = inp.normal((m, c), synth.T_RES)
+    gamma = inp.f32_uniform((c,), synth.T_GAMMA, 0.5, 1.5)
+    beta = inp.f32_normal((c,), synth.T_BETA, 0.0, 0.3)
+    p = nb.bn_problem(m, c, EPS)
+    y = blocks.dev_bf16(yb)
+    ga, be = blocks.dev_f32(gamma), blocks.dev_f32(beta)
+    out = torch.empty_like(y)
+    sm, sr = torch.empty(c, device="cuda"), torch.empty(c, device="cuda")
+    ws = blocks.workspace(max(nb.numbat_workspace_size(nb.OP_BN_SILU_FWD, p),
+                              nb.numbat_workspace_size(nb.OP_BN_SILU_BWD, p)))
+    nb.numbat_bn_silu_fwd(p, y, None, ga, be, None, out, sm, sr, ws=ws)
+    dy = torch.empty_like(y)
+    dg, db = torch.empty(c, device="cuda"), torch.empty(c, device="cuda")
+    rg = blocks.dev_bf16(r0)
+    nb.numbat_bn_silu_bwd(p, blocks.dev_bf16(gb), y, sm, sr, ga, be, dy, dg, db, rg, ws=ws)
+    torch.cuda.synchronize()
+    mref, vref = oracle.bn_stats(f64(yb))
+    dyr, dgr, dbr = oracle.bn_silu_bwd(f64(gb), f64(yb), mref, vref, gamma.astype(np.float64),
+                                       beta.astype(np.float64), EPS)
+    assert_close(blocks.host_f64(dy), dyr, "dy")
+    assert_close(blocks.host_f64(dg), dgr, "dgamma")
+    assert_close(blocks.host_f64(db), dbr, "dbeta")
+    assert_close(blocks.host_f64(rg), f64(r0) + f64(gb), "residual grad")
+
+
+def test_bitwise_determinism():
+    c = (4, 20, 20, 96, 96, 3, 1)
+    s = shape_of(c)
+    inp = Inputs(107)
+    xb, wb, gb = inp.normal(s.x_shape, synth.T_X), inp.weight(96, 3, 96), inp.normal(s.y_shape, synth.T_G)
+    blk = blocks.ConvBlock(s.n, s.h, s.w, s.ci, s.co, 3, 1)
+    x, w, g = blocks.dev_bf16(xb), blocks.dev_bf16(wb), blocks.dev_bf16(gb)
+    ga = torch.ones(96, device="cuda")
+    be = torch.zeros(96, device="cuda")
+    runs = []
+    for _ in range(2):
+        f = blk.forward(x, w, ga, be)
+        b = blk.backward(g, x, w, ga, be, f)
+        torch.cuda.synchronize()
+        runs.append({**{k: v.clone() for k, v in f.items()}, **{k: v.clone() for k, v in b.items()}})
+    for k in runs[0]:
+        assert torch.equal(runs[0][k], runs[1][k]), k
