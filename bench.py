@@ -1,0 +1,265 @@
+#!/usr/bin/env python3
+"""Benchmark of the Conv2d + BN(train) + SiLU hot path on one MI355X.
+
+Workload (default): the 65 Conv+BN+SiLU layers of the YOLOv8m-class backbone and
+neck at batch 16, 640x640 input (the detector of the paper's case study, Sec. 6.1,
+per-GPU batch 16 of Table 1), in set mode: every layer is an independent problem
+with seeded inputs x ~ N(0,1) (bf16), Kaiming-uniform weights, gamma = 1, beta = 0,
+upstream gradient g ~ N(0,1).  One step = forward over the layers in network order
+(conv_fwd with fused batch statistics, bn_silu_fwd), then backward in reverse order
+(bn_silu_bwd, conv_bwd_weight, conv_bwd_data) -- every row of the hot path.
+
+Prints ONE JSON line.  value = conv FLOPs of the step (fwd + dgrad + wgrad,
+2*M*N*K each) / measured step time, in TFLOP/s.  roofline = the dominant kernel's
+algorithmic FLOPs per launch / its average launch duration (HIP events on the launch
+stream, inside the timed region).  cpu_baseline = the fp64 oracle on a bounded sample
+(all layers at batch 1), on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=4, help="workload configuration (4 or 5)")
+    ap.add_argument("--batch", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-events", action="store_true", help="time without per-call HIP events")
+    ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
+    ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
+    return ap.parse_args()
+
+
+class Layer:
+    """Device buffers and problem descriptors of one layer."""
+
+    def __init__(self, idx, spec, n, cfg_index, eps):
+        import torch
+
+        from paper_2609_10632_amd import blocks, synth
+        from paper_2609_10632_amd import numbat as nb
+
+        self.spec = spec
+        self.name = spec.name
+        sid = lambda t: synth.stream_id(cfg_index, idx, t)
+        b = synth.kaiming_uniform_bound(spec.ci * spec.k * spec.k)
+        self.blk = blocks.ConvBlock(n, spec.h, spec.h, spec.ci, spec.co, spec.k, spec.s, eps=eps)
+        ho = self.blk.ho
+        self.x = blocks.dev_bf16(synth.bf16((n, spec.h, spec.h, spec.ci), sid(synth.T_X)))
+        self.w = blocks.dev_bf16(synth.bf16((spec.co, spec.k, spec.k, spec.ci), sid(synth.T_W), synth.UNIFORM, -b, b))
+        self.g = blocks.dev_bf16(synth.bf16((n, ho, ho, spec.co), sid(synth.T_G)))
+        dev = self.x.device
+        bf = torch.bfloat16
+        self.gamma = torch.ones(spec.co, device=dev)
+        self.beta = torch.zeros(spec.co, device=dev)
+        self.y = torch.empty((n, ho, ho, spec.co), dtype=bf, device=dev)
+        self.a = torch.empty_like(self.y)
+        self.dy = torch.empty_like(self.y)
+        self.dx = torch.empty((n, spec.h, spec.h, spec.ci), dtype=bf, device=dev)
+        self.dw = torch.empty((spec.co, spec.k, spec.k, spec.ci), dtype=torch.float32, device=dev)
+        f32 = lambda k: torch.empty(k, dtype=torch.float32, device=dev)
+        self.stats, self.smean, self.srstd, self.dgamma, self.dbeta = (f32(2 * spec.co), f32(spec.co),
+                                                                       f32(spec.co), f32(spec.co), f32(spec.co))
+        self.bnp = self.blk.bn()
+        self.ws_need = self.blk.ws_bytes()
+        self.nb = nb
+        self.flops = spec.gemm_flops(n)  # one pass
+        self.bn_elems = self.blk.m * spec.co
+
+    def bind_ws(self, ws):
+        self.ws = ws
+        self.ws_len = ws.numel()
+
+    def fwd(self, ev=None):
+        nb = self.nb
+        e = ev.get(self.name) if ev else None
+        if e: e[0].record()
+        nb.numbat_conv_fwd(self.blk.prob, self.x, self.w, self.y, self.stats, self.ws, ws_bytes=self.ws_len)
+        if e: e[1].record()
+        nb.numbat_bn_silu_fwd(self.bnp, self.y, self.stats, self.gamma, self.beta, None, self.a, self.smean,
+                              self.srstd, ws=self.ws, ws_bytes=self.ws_len)
+        if e: e[2].record()
+
+    def bwd(self, ev=None):
+        nb = self.nb
+        e = ev.get(self.name) if ev else None
+        if e: e[3].record()
+        nb.numbat_bn_silu_bwd(self.bnp, self.g, self.y, self.smean, self.srstd, self.gamma, self.beta, self.dy,
+                              self.dgamma, self.dbeta, None, ws=self.ws, ws_bytes=self.ws_len)
+        if e: e[4].record()
+        nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
+        if e: e[5].record()
+        nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
+        if e: e[6].record()
+
+
+PASSES = ("conv_fwd", "bn_silu_fwd", "bn_silu_bwd", "conv_bwd_weight", "conv_bwd_data")
+
+
+def cpu_baseline(wl, threads_hint):
+    """The fp64 oracle on a bounded sample of the same workload: every layer at batch 1,
+    forward + BN/SiLU forward and backward + data and weight gradients."""
+    import numpy as np
+
+    import oracle
+    from oracle import ConvShape
+    from paper_2609_10632_amd import synth
+
+    oracle.build(force=False)
+    flops = 0.0
+    t_total = 0.0
+    for idx, l in enumerate(wl.layers):
+        sid = lambda t: synth.stream_id(90 + wl.index, idx, t)
+        b = synth.kaiming_uniform_bound(l.ci * l.k * l.k)
+        x = synth.bf16_to_f64(synth.bf16((1, l.h, l.h, l.ci), sid(synth.T_X)))
+        w = synth.bf16_to_f64(synth.bf16((l.co, l.k, l.k, l.ci), sid(synth.T_W), synth.UNIFORM, -b, b))
+        g = synth.bf16_to_f64(synth.bf16((1, l.ho, l.ho, l.co), sid(synth.T_G)))
+        s = ConvShape(1, l.h, l.h, l.ci, l.co, l.k, l.k, l.s, l.s, l.p, l.p)
+        ones, zeros = np.ones(l.co), np.zeros(l.co)
+        t0 = time.perf_counter()
+        f = oracle.block_fwd(x, w, s, ones, zeros, wl.eps)
+        oracle.block_bwd(g, x, w, s, f, ones, zeros, wl.eps)
+        t_total += time.perf_counter() - t0
+        flops += 3 * l.gemm_flops(1)
+    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": threads_hint, "kind": "oracle",
+            "sample": f"all {len(wl.layers)} layers at batch 1 (1/{wl.n} of the step): conv fwd + BN/SiLU fwd/bwd + "
+                      f"dgrad + wgrad in fp64; {flops / 1e9:.1f} GFLOP in {t_total:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_10632_amd import numbat as nb
+    from paper_2609_10632_amd.workloads import workload
+
+    nb.load()
+    torch.cuda.set_device(0)
+    wl = workload(args.config, args.batch)
+    specs = wl.layers
+    if args.layers:
+        want = set(args.layers.split(","))
+        specs = [l for l in specs if l.name in want]
+    print(f"# setting up {len(specs)} layers of configuration {wl.index} at batch {wl.n}", file=sys.stderr, flush=True)
+    layers = [Layer(i, l, wl.n, wl.index, wl.eps) for i, l in enumerate(specs)]
+    ws = torch.empty(max(l.ws_need for l in layers), dtype=torch.uint8, device="cuda")
+    for l in layers:
+        l.bind_ws(ws)
+    torch.cuda.synchronize()
+    step_flops = sum(3 * l.flops for l in layers)
+
+    def step(ev=None):
+        for l in layers:
+            l.fwd(ev)
+        for l in reversed(layers):
+            l.bwd(ev)
+
+    print(f"# warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    use_ev = not args.no_events
+    evs = []
+    print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ev = None
+        if use_ev:
+            ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
+            evs.append(ev)
+        step(ev)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+
+    # per-pass device time from the events of the timed steps
+    per_pass = {p: 0.0 for p in PASSES}
+    per_layer = {}
+    if use_ev:
+        for ev in evs:
+            for l in layers:
+                e = ev[l.name]
+                d = [e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[3].elapsed_time(e[4]),
+                     e[4].elapsed_time(e[5]), e[5].elapsed_time(e[6])]
+                for p, v in zip(PASSES, d):
+                    per_pass[p] += v / len(evs)
+                pl = per_layer.setdefault(l.name, [0.0] * 5)
+                for i, v in enumerate(d):
+                    pl[i] += v / len(evs)
+    conv_ms = per_pass["conv_fwd"] + per_pass["conv_bwd_weight"] + per_pass["conv_bwd_data"]
+    bn_ms = per_pass["bn_silu_fwd"] + per_pass["bn_silu_bwd"]
+
+    # dominant entry point by device time; its achieved FLOP rate per launch
+    conv_passes = {"conv_fwd": 0, "conv_bwd_weight": 3, "conv_bwd_data": 4}
+    dom = max(conv_passes, key=lambda p: per_pass[p]) if use_ev else None
+    roofline = None
+    if dom:
+        i = conv_passes[dom]
+        flops = sum(l.flops for l in layers)
+        dur_s = sum(per_layer[l.name][i] for l in layers) / 1e3
+        achieved = flops / dur_s / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                    "kernel": dom, "launches_per_step": len(layers),
+                    "avg_launch_ms": round(dur_s * 1e3 / len(layers), 4)}
+
+    value = step_flops / (ms / 1e3) / 1e12
+    out = {
+        "metric": "conv fwd+bwd TFLOP/s & % bf16 MFMA peak; ms per YOLOv8m-shape step, batch 16",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name + (f" [{len(layers)} layers]" if args.layers else ""),
+                   "config_index": wl.index, "batch": wl.n, "input": "640x640", "layers": len(layers),
+                   "mode": "set", "step_gflop": round(step_flops / 1e9, 2)},
+        "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "conv_kernel_ms": round(conv_ms, 3) if use_ev else None,
+        "conv_kernel_tflops": round(step_flops / (conv_ms / 1e3) / 1e12, 2) if use_ev and conv_ms > 0 else None,
+        "bn_silu_ms": round(bn_ms, 3) if use_ev else None,
+        "per_pass_ms": {k: round(v, 3) for k, v in per_pass.items()} if use_ev else None,
+        "roofline": roofline,
+    }
+    if args.detail and use_ev:
+        with open(args.detail, "w") as f:
+            json.dump({"per_layer_ms": per_layer, "passes": PASSES,
+                       "flops": {l.name: l.flops for l in layers}}, f, indent=1)
+    if not args.no_cpu_baseline:
+        print("# cpu baseline (fp64 oracle, bounded sample)", file=sys.stderr, flush=True)
+        import oracle
+
+        oracle.build(force=False)
+        out["cpu_baseline"] = cpu_baseline(wl, oracle.num_threads())
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

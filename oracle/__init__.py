@@ -67,8 +67,14 @@ def _load():
         for name in ("ref_conv_fwd_sample", "ref_conv_dgrad_sample", "ref_conv_wgrad_sample"):
             getattr(lib, name).argtypes = [P, P, D, P, ctypes.c_int64, P]
         lib.ref_conv_fwd_channel.argtypes = [P, P, D, ctypes.c_int32, P]
+        lib.ref_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the C oracle runs on."""
+    return int(_load().ref_num_threads())
 
 
 @dataclass(frozen=True)

@@ -168,3 +168,7 @@ void ref_conv_fwd_channel(const double* x, const double* wt, const ref_conv_dims
       for (int32_t q = 0; q < wo; ++q)
         col[((int64_t)n * ho + p) * wo + q] = ref_conv_fwd_at(x, wt, d, n, p, q, o);
 }
+
+/* Threads the OpenMP loops above use (reported beside timings). */
+#include <omp.h>
+int ref_num_threads(void) { return omp_get_max_threads(); }
