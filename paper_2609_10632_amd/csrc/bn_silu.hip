@@ -12,7 +12,8 @@ namespace numbat {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxBlocks = 1024;
+constexpr int kMaxBlocks = 4096;
+constexpr int kVpt = 4;  // 16-byte vectors in flight per thread in the apply kernels
 
 // rows handled together by one block: thread t works on channel vector t % cv of row t / cv
 struct RowLayout {
@@ -44,7 +45,23 @@ __global__ __launch_bounds__(kThreads) void bn_stats_kernel(const bf16_t* y, int
 #pragma unroll
   for (int e = 0; e < 8; ++e) s1[e] = s2[e] = 0.f;
   if (t < L.active) {
-    for (int64_t r = r0 + rr; r < r1; r += L.rows_per_iter) {
+    int64_t r = r0 + rr;
+    for (; r + L.rows_per_iter < r1; r += 2 * L.rows_per_iter) {
+      float f[8], h[8];
+      const uint4 u0 = *reinterpret_cast<const uint4*>(y + r * y_pix + cvi * 8);
+      const uint4 u1 = *reinterpret_cast<const uint4*>(y + (r + L.rows_per_iter) * y_pix + cvi * 8);
+      unpack8(u0, f);
+      unpack8(u1, h);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = f[e] - shift[e], d2 = h[e] - shift[e];
+        s1[e] += d;
+        s2[e] += d * d;
+        s1[e] += d2;
+        s2[e] += d2 * d2;
+      }
+    }
+    if (r < r1) {
       float f[8];
       unpack8(*reinterpret_cast<const uint4*>(y + r * y_pix + cvi * 8), f);
 #pragma unroll
@@ -107,23 +124,42 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, FastDiv div_
   __syncthreads();
   const uint32_t cv = (uint32_t)(a.c >> 3);
   const int64_t total = a.m * (int64_t)cv;
-  for (int64_t v = blockIdx.x * (int64_t)kThreads + threadIdx.x; v < total; v += (int64_t)gridDim.x * kThreads) {
-    const uint32_t row = fdiv((uint32_t)v, div_cv);
-    const int cb = (int)((uint32_t)v - row * cv) * 8;
-    float f[8], o[8];
-    unpack8(*reinterpret_cast<const uint4*>(y + (int64_t)row * a.y_pix + cb), f);
+  for (int64_t base = (int64_t)blockIdx.x * kThreads * kVpt; base < total; base += (int64_t)gridDim.x * kThreads * kVpt) {
+    uint4 yv[kVpt], rv[kVpt];
+    int64_t rowoff[kVpt];
+    int cbs[kVpt];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float z = (f[e] - s_mean[cb + e]) * s_scale[cb + e] + s_beta[cb + e];
-      o[e] = z * sigmoidf_fast(z);
+    for (int j = 0; j < kVpt; ++j) {
+      const int64_t v = base + threadIdx.x + j * kThreads;
+      const uint32_t vv = (uint32_t)(v < total ? v : 0);
+      const uint32_t row = fdiv(vv, div_cv);
+      rowoff[j] = row;
+      cbs[j] = (int)(vv - row * cv) * 8;
+      if (v < total) {
+        yv[j] = *reinterpret_cast<const uint4*>(y + (int64_t)row * a.y_pix + cbs[j]);
+        if (res != nullptr) rv[j] = *reinterpret_cast<const uint4*>(res + (int64_t)row * a.r_pix + cbs[j]);
+      }
     }
-    if (res != nullptr) {
-      float r[8];
-      unpack8(*reinterpret_cast<const uint4*>(res + (int64_t)row * a.r_pix + cb), r);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] += r[e];
+    for (int j = 0; j < kVpt; ++j) {
+      const int64_t v = base + threadIdx.x + j * kThreads;
+      if (v >= total) continue;
+      const int cb = cbs[j];
+      float f[8], o[8];
+      unpack8(yv[j], f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float z = (f[e] - s_mean[cb + e]) * s_scale[cb + e] + s_beta[cb + e];
+        o[e] = z * sigmoidf_fast(z);
+      }
+      if (res != nullptr) {
+        float r[8];
+        unpack8(rv[j], r);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] += r[e];
+      }
+      *reinterpret_cast<uint4*>(out + rowoff[j] * a.a_pix + cb) = pack8(o);
     }
-    *reinterpret_cast<uint4*>(out + (int64_t)row * a.a_pix + cb) = pack8(o);
   }
 }
 
@@ -157,10 +193,10 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
 #pragma unroll
   for (int e = 0; e < 8; ++e) sdz[e] = sdx[e] = 0.f;
   if (t < L.active) {
-    for (int64_t r = r0 + rr; r < r1; r += L.rows_per_iter) {
+    auto accum = [&](const uint4& gu, const uint4& yu) {
       float gy[8], yy[8];
-      unpack8(*reinterpret_cast<const uint4*>(g + r * a.a_pix + cb), gy);
-      unpack8(*reinterpret_cast<const uint4*>(y + r * a.y_pix + cb), yy);
+      unpack8(gu, gy);
+      unpack8(yu, yy);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xh = (yy[e] - s_mean[cb + e]) * s_rstd[cb + e];
@@ -170,7 +206,19 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
         sdz[e] += dz;
         sdx[e] += dz * xh;
       }
+    };
+    int64_t r = r0 + rr;
+    for (; r + L.rows_per_iter < r1; r += 2 * L.rows_per_iter) {
+      const int64_t r2 = r + L.rows_per_iter;
+      const uint4 g0 = *reinterpret_cast<const uint4*>(g + r * a.a_pix + cb);
+      const uint4 y0 = *reinterpret_cast<const uint4*>(y + r * a.y_pix + cb);
+      const uint4 g1 = *reinterpret_cast<const uint4*>(g + r2 * a.a_pix + cb);
+      const uint4 y1 = *reinterpret_cast<const uint4*>(y + r2 * a.y_pix + cb);
+      accum(g0, y0);
+      accum(g1, y1);
     }
+    if (r < r1)
+      accum(*reinterpret_cast<const uint4*>(g + r * a.a_pix + cb), *reinterpret_cast<const uint4*>(y + r * a.y_pix + cb));
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       s_red[(rr * c + cb + e) * 2 + 0] = sdz[e];
@@ -240,36 +288,54 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, FastDi
   __syncthreads();
   const uint32_t cv = (uint32_t)(c >> 3);
   const int64_t total = a.m * (int64_t)cv;
-  for (int64_t v = blockIdx.x * (int64_t)kThreads + threadIdx.x; v < total; v += (int64_t)gridDim.x * kThreads) {
-    const uint32_t row = fdiv((uint32_t)v, div_cv);
-    const int cb = (int)((uint32_t)v - row * cv) * 8;
-    float gy[8], yy[8], o[8];
-    const uint4 gv = *reinterpret_cast<const uint4*>(g + (int64_t)row * a.a_pix + cb);
-    unpack8(gv, gy);
-    unpack8(*reinterpret_cast<const uint4*>(y + (int64_t)row * a.y_pix + cb), yy);
+  for (int64_t base = (int64_t)blockIdx.x * kThreads * kVpt; base < total; base += (int64_t)gridDim.x * kThreads * kVpt) {
+    uint4 gv[kVpt], yv[kVpt], rv[kVpt];
+    int64_t rows[kVpt];
+    int cbs[kVpt];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int ch = cb + e;
-      const float xh = (yy[e] - smem[ch]) * smem[c + ch];
-      const float z = smem[2 * c + ch] * xh + smem[3 * c + ch];
-      const float sg = sigmoidf_fast(z);
-      const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
-      o[e] = smem[4 * c + ch] * (dz - smem[5 * c + ch] - xh * smem[6 * c + ch]);
+    for (int j = 0; j < kVpt; ++j) {
+      const int64_t v = base + threadIdx.x + j * kThreads;
+      const uint32_t vv = (uint32_t)(v < total ? v : 0);
+      const uint32_t row = fdiv(vv, div_cv);
+      rows[j] = row;
+      cbs[j] = (int)(vv - row * cv) * 8;
+      if (v < total) {
+        gv[j] = *reinterpret_cast<const uint4*>(g + (int64_t)row * a.a_pix + cbs[j]);
+        yv[j] = *reinterpret_cast<const uint4*>(y + (int64_t)row * a.y_pix + cbs[j]);
+        if (res_grad != nullptr) rv[j] = *reinterpret_cast<const uint4*>(res_grad + (int64_t)row * a.r_pix + cbs[j]);
+      }
     }
-    *reinterpret_cast<uint4*>(dy + (int64_t)row * a.dy_pix + cb) = pack8(o);
-    if (res_grad != nullptr) {
-      float r[8];
-      bf16_t* rp = res_grad + (int64_t)row * a.r_pix + cb;
-      unpack8(*reinterpret_cast<const uint4*>(rp), r);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) r[e] += gy[e];
-      *reinterpret_cast<uint4*>(rp) = pack8(r);
+    for (int j = 0; j < kVpt; ++j) {
+      const int64_t v = base + threadIdx.x + j * kThreads;
+      if (v >= total) continue;
+      const int cb = cbs[j];
+      float gy[8], yy[8], o[8];
+      unpack8(gv[j], gy);
+      unpack8(yv[j], yy);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int ch = cb + e;
+        const float xh = (yy[e] - smem[ch]) * smem[c + ch];
+        const float z = smem[2 * c + ch] * xh + smem[3 * c + ch];
+        const float sg = sigmoidf_fast(z);
+        const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
+        o[e] = smem[4 * c + ch] * (dz - smem[5 * c + ch] - xh * smem[6 * c + ch]);
+      }
+      *reinterpret_cast<uint4*>(dy + rows[j] * a.dy_pix + cb) = pack8(o);
+      if (res_grad != nullptr) {
+        float r[8];
+        unpack8(rv[j], r);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) r[e] += gy[e];
+        *reinterpret_cast<uint4*>(res_grad + rows[j] * a.r_pix + cb) = pack8(r);
+      }
     }
   }
 }
 
 int grid_for_elems(int64_t vecs) {
-  int64_t b = (vecs + kThreads * 4 - 1) / (kThreads * 4);
+  int64_t b = (vecs + kThreads * kVpt - 1) / (kThreads * kVpt);
   if (b > 8192) b = 8192;
   if (b < 1) b = 1;
   return (int)b;
@@ -285,8 +351,8 @@ size_t reduce_smem(int c) {
 }  // namespace
 
 int bn_reduce_blocks(int64_t m, int c) {
-  (void)c;
-  int64_t b = (m + 255) / 256;
+  // about 8 vectors of 8 channels per thread
+  int64_t b = (m * (c / 8) + kThreads * 8 - 1) / (kThreads * 8);
   if (b > kMaxBlocks) b = kMaxBlocks;
   if (b < 1) b = 1;
   return (int)b;

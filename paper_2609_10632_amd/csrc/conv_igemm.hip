@@ -318,48 +318,64 @@ hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
-// Merge of per-tile (mean, M2) partials (Chan et al. pairwise update) in fp64, in
-// a fixed order: thread g of a channel folds tiles g, g+G, g+2G, ... then the G
-// partial results are folded in index order.
+// Merge of per-tile (mean, M2) partials into the batch mean and biased variance, in
+// fp64 and a fixed order.  With K the first tile's mean (a shift shared by every thread
+// of a channel), each thread sums n_t (mean_t - K), n_t (mean_t - K)^2 and M2_t over the
+// tiles g, g+G, g+2G, ...; the G partial sums are added in index order, and
+//   mean = K + S1 / N,   M2 = sum M2_t + S2 - N (S1 / N)^2
+// (the pairwise update of Chan et al. written as sums, with no division per tile).
 
 namespace {
 
 constexpr int kMergeGroups = 16;
 
-__device__ __forceinline__ void chan_merge(double& n, double& mean, double& m2, double nb, double meanb,
-                                           double m2b) {
-  if (nb == 0) return;
-  const double nt = n + nb;
-  const double d = meanb - mean;
-  mean += d * (nb / nt);
-  m2 += m2b + d * d * (n * nb / nt);
-  n = nt;
-}
-
 __global__ __launch_bounds__(64 * kMergeGroups) void stats_merge_kernel(const float2* part, int mtiles,
                                                                         int tile_rows, int64_t m, int c,
                                                                         float* mean_var) {
-  __shared__ double sn[kMergeGroups][64], smu[kMergeGroups][64], sm2[kMergeGroups][64];
+  __shared__ double s1s[kMergeGroups][64], s2s[kMergeGroups][64], m2s[kMergeGroups][64];
   const int cl = threadIdx.x & 63;
   const int g = threadIdx.x >> 6;
   const int ch = blockIdx.x * 64 + cl;
-  double n = 0, mu = 0, m2 = 0;
+  double s1 = 0, s2 = 0, m2 = 0;
+  double K = 0;
   if (ch < c) {
-    for (int t = g; t < mtiles; t += kMergeGroups) {
-      const int64_t left = m - (int64_t)t * tile_rows;
-      const double cnt = (double)(left < tile_rows ? left : tile_rows);
+    K = (double)part[ch].x;
+    // every tile but the last holds tile_rows rows
+    const int full = (int)((m / tile_rows) < mtiles ? (m / tile_rows) : mtiles);
+    const double nt = (double)tile_rows;
+    int t = g;
+#pragma unroll 4
+    for (; t < full; t += kMergeGroups) {
       const float2 p = part[(int64_t)t * c + ch];
-      chan_merge(n, mu, m2, cnt, (double)p.x, (double)p.y);
+      const double d = (double)p.x - K;
+      s1 += nt * d;
+      s2 += nt * d * d;
+      m2 += (double)p.y;
+    }
+    for (; t < mtiles; t += kMergeGroups) {
+      const double cnt = (double)(m - (int64_t)t * tile_rows);
+      const float2 p = part[(int64_t)t * c + ch];
+      const double d = (double)p.x - K;
+      s1 += cnt * d;
+      s2 += cnt * d * d;
+      m2 += (double)p.y;
     }
   }
-  sn[g][cl] = n;
-  smu[g][cl] = mu;
-  sm2[g][cl] = m2;
+  s1s[g][cl] = s1;
+  s2s[g][cl] = s2;
+  m2s[g][cl] = m2;
   __syncthreads();
   if (g == 0 && ch < c) {
-    for (int k = 1; k < kMergeGroups; ++k) chan_merge(n, mu, m2, sn[k][cl], smu[k][cl], sm2[k][cl]);
-    mean_var[ch] = (float)mu;
-    mean_var[c + ch] = (float)(m2 / (double)m);
+    for (int k = 1; k < kMergeGroups; ++k) {
+      s1 += s1s[k][cl];
+      s2 += s2s[k][cl];
+      m2 += m2s[k][cl];
+    }
+    const double n = (double)m;
+    const double dm = s1 / n;
+    mean_var[ch] = (float)(K + dm);
+    const double v = (m2 + s2 - n * dm * dm) / n;
+    mean_var[c + ch] = (float)(v > 0 ? v : 0);
   }
 }
 

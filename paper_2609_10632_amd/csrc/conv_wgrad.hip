@@ -228,12 +228,26 @@ hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-__global__ void splitk_reduce_kernel(const float* part, int splits, int64_t count, float* dw, int accumulate) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) {
-    float s = accumulate ? dw[i] : 0.f;
-    float t = 0.f;
-    for (int k = 0; k < splits; ++k) t += part[(int64_t)k * count + i];
-    dw[i] = s + t;
+// dw = [dw +] sum over splits in split order; four consecutive outputs per thread
+__global__ void splitk_reduce_kernel(const float4* part, int splits, int64_t count4, float* dw, int accumulate) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count4; i += (int64_t)gridDim.x * blockDim.x) {
+    float4 t = part[i];
+    int k = 1;
+    for (; k + 1 < splits; k += 2) {
+      const float4 u = part[(int64_t)k * count4 + i];
+      const float4 v = part[(int64_t)(k + 1) * count4 + i];
+      t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
+      t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+    }
+    if (k < splits) {
+      const float4 u = part[(int64_t)k * count4 + i];
+      t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
+    }
+    float* o = dw + 4 * i;
+    if (accumulate) {
+      t.x = o[0] + t.x; t.y = o[1] + t.y; t.z = o[2] + t.z; t.w = o[3] + t.w;
+    }
+    o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
   }
 }
 
@@ -242,11 +256,11 @@ __global__ void splitk_reduce_kernel(const float* part, int splits, int64_t coun
 int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   const int tiles = (int)(((co + 127) / 128) * ((ktot + 127) / 128));
   const int64_t steps = (m + BR - 1) / BR;
-  int64_t splits = (1024 + tiles - 1) / tiles;
-  // at least 8 steps per split, at most 1024 splits, partials at most 64 MiB
-  const int64_t max_by_steps = steps / 8 > 0 ? steps / 8 : 1;
+  int64_t splits = (512 + tiles - 1) / tiles;
+  // at least 16 steps per split, at most 256 splits, partials at most 64 MiB
+  const int64_t max_by_steps = steps / 16 > 0 ? steps / 16 : 1;
   if (splits > max_by_steps) splits = max_by_steps;
-  if (splits > 1024) splits = 1024;
+  if (splits > 256) splits = 256;
   const int64_t part_bytes = (int64_t)co * ktot * 4;
   while (splits > 1 && splits * part_bytes > (64ll << 20)) --splits;
   if (splits < 1) splits = 1;
@@ -260,11 +274,13 @@ hipError_t wgrad_launch(const WgradArgs& a, hipStream_t s) { return launch_w<4, 
 
 hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
                                 hipStream_t s) {
-  int64_t blocks = (count + 255) / 256;
+  // count = c_out * k_total is a multiple of 8 (c_out is)
+  const int64_t count4 = count / 4;
+  int64_t blocks = (count4 + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, part, splits, count, dw,
-                     accumulate);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                     reinterpret_cast<const float4*>(part), splits, count4, dw, accumulate);
   return hipGetLastError();
 }
 
