@@ -110,3 +110,72 @@ class ConvBlock:
             nb.numbat_conv_bwd_data(self.prob, dy, w, dx, accumulate_dx, ws, stream=stream)
             out["dx"] = dx
         return out
+
+
+class C2fBlock:
+    """A C2f block (CSP backbone unit of the detector, Sec. 6.1) on the C ABI.
+
+    cv1 (1x1, c1 -> c2), split into two c2/2 halves, nb bottlenecks of two 3x3 blocks with
+    a residual add, concatenation of the 2 + nb halves, cv2 (1x1 -> c2).  Split and concat
+    are zero-copy: every half lives at a channel offset of one concat buffer, read and
+    written through pixel strides; the residual add is fused into the BN+SiLU forward, its
+    gradient into the BN+SiLU backward (residual_grad), and the gradient fan-in of a half
+    into the data-gradient accumulate flag.
+    """
+
+    def __init__(self, n, h, c1, c2, nb, eps=1e-3, shortcut=True):
+        self.n, self.h, self.c1, self.c2, self.nb, self.eps, self.shortcut = n, h, c1, c2, nb, eps, shortcut
+        self.half = c2 // 2
+        self.catc = (2 + nb) * self.half
+        hc = self.half
+        self.cv1 = ConvBlock(n, h, h, c1, c2, 1, 1, eps=eps)
+        self.m1 = ConvBlock(n, h, h, hc, hc, 3, 1, eps=eps, x_pixel_stride=self.catc)  # reads a half of cat
+        self.m2 = ConvBlock(n, h, h, hc, hc, 3, 1, eps=eps)
+        self.cv2 = ConvBlock(n, h, h, self.catc, c2, 1, 1, eps=eps)
+        self.ws = workspace(max(b.ws_bytes() for b in (self.cv1, self.m1, self.m2, self.cv2)))
+
+    def _half(self, t, k):
+        return t[..., k * self.half:(k + 1) * self.half]
+
+    def forward(self, x, params):
+        """params: list of (w, gamma, beta) in order cv1, m0.cv1, m0.cv2, ..., cv2."""
+        dev = x.device
+        cat = torch.empty((self.n, self.h, self.h, self.catc), dtype=torch.bfloat16, device=dev)
+        st = {"x": x, "cat": cat}
+        w, g, b = params[0]
+        st["cv1"] = self.cv1.forward(x, w, g, b, a=cat[..., :self.c2], ws=self.ws, a_pixel_stride=self.catc)
+        for i in range(self.nb):
+            inp = self._half(cat, 1 + i)
+            w1, g1, b1 = params[1 + 2 * i]
+            w2, g2, b2 = params[2 + 2 * i]
+            f1 = self.m1.forward(inp, w1, g1, b1, ws=self.ws)
+            f2 = self.m2.forward(f1["a"], w2, g2, b2, a=self._half(cat, 2 + i), ws=self.ws,
+                                 residual=inp if self.shortcut else None, a_pixel_stride=self.catc,
+                                 r_pixel_stride=self.catc)
+            st[f"m{i}.cv1"], st[f"m{i}.cv2"] = f1, f2
+        w, g, b = params[-1]
+        st["cv2"] = self.cv2.forward(cat, w, g, b, ws=self.ws)
+        st["out"] = st["cv2"]["a"]
+        return st
+
+    def backward(self, gout, st, params):
+        """Returns (per-layer gradient dicts in params order, dx)."""
+        grads = [None] * len(params)
+        w, g, b = params[-1]
+        grads[-1] = self.cv2.backward(gout, st["cat"], w, g, b, st["cv2"], ws=self.ws)
+        dcat = grads[-1]["dx"]
+        for i in reversed(range(self.nb)):
+            gi = self._half(dcat, 2 + i)
+            din = self._half(dcat, 1 + i)
+            w1, g1, b1 = params[1 + 2 * i]
+            w2, g2, b2 = params[2 + 2 * i]
+            f1, f2 = st[f"m{i}.cv1"], st[f"m{i}.cv2"]
+            b2g = self.m2.backward(gi, f1["a"], w2, g2, b2, f2, ws=self.ws, g_pixel_stride=self.catc,
+                                   residual_grad=din if self.shortcut else None, r_pixel_stride=self.catc)
+            b1g = self.m1.backward(b2g["dx"], self._half(st["cat"], 1 + i), w1, g1, b1, f1, dx=din,
+                                   accumulate_dx=True, ws=self.ws)
+            grads[1 + 2 * i], grads[2 + 2 * i] = b1g, b2g
+        w, g, b = params[0]
+        grads[0] = self.cv1.backward(dcat[..., :self.c2], st["x"], w, g, b, st["cv1"], ws=self.ws,
+                                     g_pixel_stride=self.catc)
+        return grads, grads[0]["dx"]
