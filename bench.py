@@ -10,10 +10,12 @@ upstream gradient g ~ N(0,1).  One step = forward over the layers in network ord
 (bn_silu_bwd, conv_bwd_weight, conv_bwd_data) -- every row of the hot path.
 
 Prints ONE JSON line.  value = conv FLOPs of the step (fwd + dgrad + wgrad,
-2*M*N*K each) / measured step time, in TFLOP/s.  roofline = the dominant kernel's
-algorithmic FLOPs per launch / its average launch duration (HIP events on the launch
-stream, inside the timed region).  cpu_baseline = the fp64 oracle on a bounded sample
-(all layers at batch 1), on this host's cores.
+2*M*N*K each) / measured step time, in TFLOP/s; the step is captured once into a HIP
+graph (replays are checked bitwise against the eager step) and replayed K times.
+roofline = the dominant conv kernel's algorithmic FLOPs / its summed launch durations,
+from HIP events the library records around every kernel on its launch stream during K
+further (eager) steps.  cpu_baseline = the fp64 oracle on a bounded sample (all layers
+at batch 1), on this host's cores.
 """
 from __future__ import annotations
 
@@ -38,7 +40,8 @@ def parse():
     ap.add_argument("--config", type=int, default=4, help="workload configuration (4 or 5)")
     ap.add_argument("--batch", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-events", action="store_true", help="time without per-call HIP events")
+    ap.add_argument("--no-events", action="store_true", help="skip the instrumented (per-kernel timing) steps")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
     return ap.parse_args()
@@ -140,6 +143,37 @@ def cpu_baseline(wl, threads_hint):
                       f"dgrad + wgrad in fp64; {flops / 1e9:.1f} GFLOP in {t_total:.1f} s"}
 
 
+def capture_graph(step, check_tensors):
+    """Capture one step into a HIP graph; replay it three times, each after an eager fill of
+    the checked outputs with NaN, and require every replay to reproduce the eager result
+    bitwise.  Returns the graph."""
+    import torch
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in check_tensors]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for t in check_tensors:
+            t.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for t, r in zip(check_tensors, ref):
+            if not torch.equal(t, r):
+                raise RuntimeError("graph replay differs from the eager step")
+    return graph
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -178,51 +212,61 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    use_ev = not args.no_events
-    evs = []
-    print(f"# timing {args.steps} steps", file=sys.stderr, flush=True)
+    graph = None
+    if not args.no_graph:
+        print("# capturing the step into a HIP graph (replays checked bitwise against eager)", file=sys.stderr,
+              flush=True)
+        probe = [layers[0].dx, layers[0].a, layers[-1].dw, layers[len(layers) // 2].dx, layers[len(layers) // 2].stats,
+                 layers[-1].dgamma]
+        graph = capture_graph(step, probe)
+
+    # ---- timed region: K steps, nothing else on the stream
+    print(f"# timing {args.steps} steps ({'graph replay' if graph else 'eager launches'})", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        ev = None
-        if use_ev:
-            ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
-            evs.append(ev)
-        step(ev)
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
 
-    # per-pass device time from the events of the timed steps
-    per_pass = {p: 0.0 for p in PASSES}
-    per_layer = {}
-    if use_ev:
-        for ev in evs:
-            for l in layers:
-                e = ev[l.name]
-                d = [e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[3].elapsed_time(e[4]),
-                     e[4].elapsed_time(e[5]), e[5].elapsed_time(e[6])]
-                for p, v in zip(PASSES, d):
-                    per_pass[p] += v / len(evs)
-                pl = per_layer.setdefault(l.name, [0.0] * 5)
-                for i, v in enumerate(d):
-                    pl[i] += v / len(evs)
-    conv_ms = per_pass["conv_fwd"] + per_pass["conv_bwd_weight"] + per_pass["conv_bwd_data"]
-    bn_ms = per_pass["bn_silu_fwd"] + per_pass["bn_silu_bwd"]
+    # ---- instrumented region: the same K steps, eager, every kernel bracketed by HIP events on
+    # its launch stream (library timing), for the per-kernel roofline
+    n_cls = nb.numbat_kernel_class_count()
+    per_cls = {}
+    ms_instr = None
+    if not args.no_events:
+        print(f"# instrumented {args.steps} steps (per-kernel HIP events)", file=sys.stderr, flush=True)
+        torch.cuda.synchronize()
+        nb.numbat_timing_enable(True)
+        ti0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        ms_instr = (time.perf_counter() - ti0) * 1e3 / args.steps
+        for c in range(n_cls):
+            tot, n = nb.numbat_timing_read(c)
+            if n:
+                per_cls[nb.numbat_kernel_class_name(c)] = (tot / args.steps, n // args.steps)
+        nb.numbat_timing_enable(False)
 
-    # dominant entry point by device time; its achieved FLOP rate per launch
-    conv_passes = {"conv_fwd": 0, "conv_bwd_weight": 3, "conv_bwd_data": 4}
-    dom = max(conv_passes, key=lambda p: per_pass[p]) if use_ev else None
+    pass_flops = sum(l.flops for l in layers)  # one pass (fwd, dgrad or wgrad) over all layers
     roofline = None
-    if dom:
-        i = conv_passes[dom]
-        flops = sum(l.flops for l in layers)
-        dur_s = sum(per_layer[l.name][i] for l in layers) / 1e3
-        achieved = flops / dur_s / 1e12
+    conv_cls = ("conv_fwd_igemm", "conv_dgrad_igemm", "wgrad_igemm")
+    if per_cls:
+        dom = max((c for c in conv_cls if c in per_cls), key=lambda c: per_cls[c][0])
+        dom_ms, dom_launches = per_cls[dom]
+        achieved = pass_flops / (dom_ms / 1e3) / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                    "kernel": dom, "launches_per_step": len(layers),
-                    "avg_launch_ms": round(dur_s * 1e3 / len(layers), 4)}
+                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom,
+                    "launches_per_step": dom_launches, "avg_launch_ms": round(dom_ms / max(dom_launches, 1), 4),
+                    "flops_per_step": pass_flops}
+    conv_ms = sum(per_cls[c][0] for c in per_cls if c not in
+                  ("bn_stats", "bn_silu_fwd_apply", "bn_silu_bwd_reduce", "bn_silu_bwd_finalize", "bn_silu_bwd_apply"))
+    bn_ms = sum(per_cls[c][0] for c in per_cls) - conv_ms if per_cls else None
 
     value = step_flops / (ms / 1e3) / 1e12
     out = {
@@ -240,18 +284,29 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name + (f" [{len(layers)} layers]" if args.layers else ""),
                    "config_index": wl.index, "batch": wl.n, "input": "640x640", "layers": len(layers),
-                   "mode": "set", "step_gflop": round(step_flops / 1e9, 2)},
+                   "mode": "set", "step_gflop": round(step_flops / 1e9, 2),
+                   "launch": "hip graph replay" if graph is not None else "eager"},
         "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
-        "conv_kernel_ms": round(conv_ms, 3) if use_ev else None,
-        "conv_kernel_tflops": round(step_flops / (conv_ms / 1e3) / 1e12, 2) if use_ev and conv_ms > 0 else None,
-        "bn_silu_ms": round(bn_ms, 3) if use_ev else None,
-        "per_pass_ms": {k: round(v, 3) for k, v in per_pass.items()} if use_ev else None,
         "roofline": roofline,
     }
-    if args.detail and use_ev:
+    if per_cls:
+        out["kernel_ms_per_step"] = {c: round(v[0], 4) for c, v in per_cls.items()}
+        out["conv_kernel_ms"] = round(conv_ms, 3)
+        out["conv_kernel_tflops"] = round(step_flops / (conv_ms / 1e3) / 1e12, 2)
+        out["bn_silu_kernel_ms"] = round(bn_ms, 3)
+        out["instrumented_ms_per_step"] = round(ms_instr, 3)
+    if args.detail:
+        ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
+        step(ev)
+        torch.cuda.synchronize()
+        per_layer = {}
+        for l in layers:
+            e = ev[l.name]
+            per_layer[l.name] = [e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[3].elapsed_time(e[4]),
+                                 e[4].elapsed_time(e[5]), e[5].elapsed_time(e[6])]
         with open(args.detail, "w") as f:
-            json.dump({"per_layer_ms": per_layer, "passes": PASSES,
-                       "flops": {l.name: l.flops for l in layers}}, f, indent=1)
+            json.dump({"per_layer_ms": per_layer, "passes": PASSES, "flops": {l.name: l.flops for l in layers}}, f,
+                      indent=1)
     if not args.no_cpu_baseline:
         print("# cpu baseline (fp64 oracle, bounded sample)", file=sys.stderr, flush=True)
         import oracle

@@ -171,6 +171,21 @@ numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, cons
                                  const float* beta, void* dy, float* dgamma, float* dbeta, void* residual_grad,
                                  void* ws, size_t ws_bytes, void* stream);
 
+/* Launch timing, for measurement (the paper times its training step phase by phase,
+ * Sec. 8): while enabled, every kernel the library launches is bracketed by two HIP
+ * events recorded on its launch stream, and numbat_timing_read sums their elapsed times
+ * per kernel class.  numbat_timing_enable(1) starts a new record set, (0) stops and
+ * clears it.  Not for use while a stream is being captured into a graph.  Events are
+ * host-side handles created by the library on first use and reused; no device memory is
+ * allocated.  Kernel classes are numbered 0 .. numbat_kernel_class_count() - 1;
+ * numbat_kernel_class_name gives a short name ("" for an unknown class). */
+int numbat_kernel_class_count(void);
+const char* numbat_kernel_class_name(int kernel_class);
+numbat_status numbat_timing_enable(int enable);
+/* Waits for the recorded events of `kernel_class`, then writes their summed duration (ms)
+ * and the number of launches.  NUMBAT_ERR_BAD_DESC for an unknown class. */
+numbat_status numbat_timing_read(int kernel_class, double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,12 +6,69 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/numbat_conv.h"
 #include "kernels.h"
 
 using namespace numbat;
+
+// ---------------------------------------------------------------------------
+// Optional launch timing: HIP events bracket each kernel on its launch stream.
+namespace {
+
+struct TimingRec {
+  int cls;
+  hipEvent_t begin, end;
+};
+
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimingRec> g_recs;
+std::vector<hipEvent_t> g_pool;
+size_t g_pool_used = 0;
+hipEvent_t g_open[KC_COUNT];
+
+hipEvent_t pool_event() {
+  if (g_pool_used == g_pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_pool.push_back(e);
+  }
+  return g_pool[g_pool_used++];
+}
+
+const char* const kClassNames[KC_COUNT] = {
+    "conv_fwd_igemm", "stats_merge", "dgrad_weight_relayout", "conv_dgrad_igemm", "wgrad_igemm",
+    "wgrad_splitk_reduce", "bn_stats", "bn_silu_fwd_apply", "bn_silu_bwd_reduce", "bn_silu_bwd_finalize",
+    "bn_silu_bwd_apply"};
+
+}  // namespace
+
+namespace numbat {
+
+void trace_begin(int cls, hipStream_t s) {
+  if (!g_timing) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  hipEvent_t e = pool_event();
+  g_open[cls] = e;
+  if (e) hipEventRecord(e, s);
+}
+
+void trace_end(int cls, hipStream_t s) {
+  if (!g_timing) return;
+  std::lock_guard<std::mutex> lk(g_tmu);
+  hipEvent_t e = pool_event();
+  if (e && g_open[cls]) {
+    hipEventRecord(e, s);
+    g_recs.push_back(TimingRec{cls, g_open[cls], e});
+  }
+  g_open[cls] = nullptr;
+}
+
+}  // namespace numbat
 
 namespace {
 
@@ -192,6 +249,42 @@ extern "C" {
 
 uint32_t numbat_abi_version(void) { return NUMBAT_ABI_VERSION; }
 
+int numbat_kernel_class_count(void) { return KC_COUNT; }
+
+const char* numbat_kernel_class_name(int kernel_class) {
+  return (kernel_class >= 0 && kernel_class < KC_COUNT) ? kClassNames[kernel_class] : "";
+}
+
+numbat_status numbat_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = enable != 0;
+  g_recs.clear();
+  g_pool_used = 0;
+  for (int i = 0; i < KC_COUNT; ++i) g_open[i] = nullptr;
+  return ok();
+}
+
+numbat_status numbat_timing_read(int kernel_class, double* total_ms, int64_t* launches) {
+  if (total_ms == nullptr || launches == nullptr) return fail(NUMBAT_ERR_NULL, "total_ms / launches is NULL");
+  if (kernel_class < 0 || kernel_class >= KC_COUNT) return fail(NUMBAT_ERR_BAD_DESC, "unknown kernel class %d", kernel_class);
+  std::lock_guard<std::mutex> lk(g_tmu);
+  double t = 0;
+  int64_t n = 0;
+  for (const TimingRec& r : g_recs) {
+    if (r.cls != kernel_class) continue;
+    hipError_t e = hipEventSynchronize(r.end);
+    if (e != hipSuccess) return hip_fail(e, "timing event");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.begin, r.end);
+    if (e != hipSuccess) return hip_fail(e, "timing elapsed");
+    t += ms;
+    ++n;
+  }
+  *total_ms = t;
+  *launches = n;
+  return ok();
+}
+
 const char* numbat_last_error(void) { return g_err.c_str(); }
 
 const char* numbat_status_string(numbat_status s) {
@@ -286,7 +379,7 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
   a.dstep_h = a.dstep_w = 1;
   a.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = igemm_launch(a, t, s);
+  hipError_t e = igemm_launch(a, t, s, KC_CONV_FWD);
   if (e != hipSuccess) return hip_fail(e, "conv forward launch");
   if (batch_stats) {
     const int mt = (int)((d.m + t.bm - 1) / t.bm);
@@ -368,7 +461,7 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
       a.doff_w = pb;
       a.accumulate = accumulate ? 1 : 0;
       const TileCfg t = igemm_pick(a.m, a.nout, a.cs);
-      e = igemm_launch(a, t, s);
+      e = igemm_launch(a, t, s, KC_CONV_DGRAD);
       if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
     }
   return ok();

@@ -365,8 +365,10 @@ hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int n
   const int64_t rpb = rows_per_block(a.m, nblocks);
   const int nb = (int)((a.m + rpb - 1) / rpb);
   float2* part = reinterpret_cast<float2*>(part3);
+  trace_begin(KC_BN_STATS, s);
   hipLaunchKernelGGL(bn_stats_kernel, dim3(nb), dim3(kThreads), reduce_smem(a.c), s, y, a.y_pix, a.m, a.c, rpb,
                      part);
+  trace_end(KC_BN_STATS, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return stats_merge_launch(part, nb, (int)rpb, a.m, a.c, mean_var, s);
@@ -377,8 +379,10 @@ hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var
                          float* run_mean, float* run_var, hipStream_t s) {
   const int64_t vecs = a.m * (a.c / 8);
   const FastDiv d = make_fastdiv((uint32_t)(a.c / 8));
+  trace_begin(KC_BN_FWD, s);
   hipLaunchKernelGGL(bn_fwd_kernel, dim3(grid_for_elems(vecs)), dim3(kThreads), 3 * a.c * sizeof(float), s, a, d, y,
                      mean_var, gamma, beta, res, out, save_mean, save_rstd, run_mean, run_var);
+  trace_end(KC_BN_FWD, s);
   return hipGetLastError();
 }
 
@@ -388,18 +392,24 @@ hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, cons
   const int64_t rpb = rows_per_block(a.m, nblocks);
   const int nb = (int)((a.m + rpb - 1) / rpb);
   float2* part = reinterpret_cast<float2*>(part2);
+  trace_begin(KC_BN_BWD_REDUCE, s);
   hipLaunchKernelGGL(bn_bwd_reduce_kernel, dim3(nb), dim3(kThreads), 4 * a.c * sizeof(float) + reduce_smem(a.c), s,
                      a, g, y, save_mean, save_rstd, gamma, beta, rpb, part);
+  trace_end(KC_BN_BWD_REDUCE, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  trace_begin(KC_BN_BWD_FINALIZE, s);
   hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3((a.c + 63) / 64), dim3(64 * kFinGroups), 0, s, part, nb, a.c, a.m,
                      save_rstd, gamma, dgamma, dbeta, coef);
+  trace_end(KC_BN_BWD_FINALIZE, s);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t vecs = a.m * (a.c / 8);
   const FastDiv d = make_fastdiv((uint32_t)(a.c / 8));
+  trace_begin(KC_BN_BWD_APPLY, s);
   hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(grid_for_elems(vecs)), dim3(kThreads), 7 * a.c * sizeof(float), s, a,
                      d, g, y, save_mean, save_rstd, gamma, beta, coef, dy, res_grad);
+  trace_end(KC_BN_BWD_APPLY, s);
   return hipGetLastError();
 }
 

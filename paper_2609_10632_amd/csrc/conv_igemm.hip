@@ -312,9 +312,12 @@ TileCfg igemm_pick(int64_t m, int nout, int cs) {
   return TileCfg{opts[best].bm, opts[best].bn, opts[best].id};
 }
 
-hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s) {
+hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
   const bool smallc = (a.cs % 8) != 0;
-  return smallc ? launch_any<true>(a, t.id, s) : launch_any<false>(a, t.id, s);
+  trace_begin(cls, s);
+  const hipError_t e = smallc ? launch_any<true>(a, t.id, s) : launch_any<false>(a, t.id, s);
+  trace_end(cls, s);
+  return e;
 }
 
 // ---------------------------------------------------------------------------
@@ -383,8 +386,10 @@ __global__ __launch_bounds__(64 * kMergeGroups) void stats_merge_kernel(const fl
 
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,
                               hipStream_t s) {
+  trace_begin(KC_STATS_MERGE, s);
   hipLaunchKernelGGL(stats_merge_kernel, dim3((c + 63) / 64), dim3(64 * kMergeGroups), 0, s, part, mtiles,
                      tile_rows, m, c, mean_var);
+  trace_end(KC_STATS_MERGE, s);
   return hipGetLastError();
 }
 
@@ -437,7 +442,9 @@ hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int
   int blocks = (int)((total + 255) / 256);
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
+  trace_begin(KC_DGRAD_WEIGHTS, s);
   hipLaunchKernelGGL(dgrad_weights_kernel, dim3(blocks), dim3(256), 0, s, w, wt, co, kh, kw, ci, tab);
+  trace_end(KC_DGRAD_WEIGHTS, s);
   return hipGetLastError();
 }
 

@@ -221,10 +221,12 @@ hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   constexpr int BMO = 2 * TM * 16, BNK = 2 * TN * 16;
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
+  trace_begin(KC_WGRAD, s);
   if (a.ci % 8 == 0)
     hipLaunchKernelGGL((wgrad_kernel<TM, TN, false>), grid, dim3(256), 0, s, a, dwo, dhw);
   else
     hipLaunchKernelGGL((wgrad_kernel<TM, TN, true>), grid, dim3(256), 0, s, a, dwo, dhw);
+  trace_end(KC_WGRAD, s);
   return hipGetLastError();
 }
 
@@ -279,8 +281,10 @@ hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, fl
   int64_t blocks = (count4 + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
+  trace_begin(KC_SPLITK_REDUCE, s);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
                      reinterpret_cast<const float4*>(part), splits, count4, dw, accumulate);
+  trace_end(KC_SPLITK_REDUCE, s);
   return hipGetLastError();
 }
 

@@ -10,6 +10,26 @@ namespace numbat {
 
 constexpr int kMaxTaps = 25;
 
+// Kernel classes for the optional launch timing (numbat_timing_*).  Each launcher
+// brackets its kernel with trace_begin / trace_end, which record HIP events on the
+// launch stream when timing is enabled and do nothing otherwise.
+enum KernelClass {
+  KC_CONV_FWD = 0,      // implicit GEMM, forward
+  KC_STATS_MERGE,       // batch statistics merge
+  KC_DGRAD_WEIGHTS,     // data-gradient weight re-layout
+  KC_CONV_DGRAD,        // implicit GEMM, data-gradient phases
+  KC_WGRAD,             // weight-gradient GEMM
+  KC_SPLITK_REDUCE,     // weight-gradient split reduction
+  KC_BN_STATS,          // standalone BN statistics
+  KC_BN_FWD,            // BN + SiLU forward apply
+  KC_BN_BWD_REDUCE,     // BN + SiLU backward reduce
+  KC_BN_BWD_FINALIZE,   // BN + SiLU backward finalize
+  KC_BN_BWD_APPLY,      // BN + SiLU backward apply
+  KC_COUNT
+};
+void trace_begin(int cls, hipStream_t s);
+void trace_end(int cls, hipStream_t s);
+
 // One implicit GEMM D[M][N] = A[M][K] * B[N][K]^T where
 //   row m   = (img, gi, gj) on a gh x gw grid per image,
 //   col     = output channel of the GEMM (N = nout),
@@ -43,7 +63,7 @@ struct TileCfg {
 
 // choose a tile for an igemm problem (depends on the problem only)
 TileCfg igemm_pick(int64_t m, int nout, int cs);
-hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s);
+hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
 
 // merge per-tile (mean, M2) partials into batch mean / biased variance, fixed order
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,

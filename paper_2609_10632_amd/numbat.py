@@ -23,7 +23,8 @@ OP_CONV_FWD, OP_CONV_BWD_DATA, OP_CONV_BWD_WEIGHT, OP_BN_SILU_FWD, OP_BN_SILU_BW
 EXPORTED = (
     "numbat_abi_version", "numbat_last_error", "numbat_status_string", "numbat_conv_output_shape",
     "numbat_workspace_size", "numbat_conv_fwd", "numbat_conv_bwd_data", "numbat_conv_bwd_weight",
-    "numbat_bn_silu_fwd", "numbat_bn_silu_bwd",
+    "numbat_bn_silu_fwd", "numbat_bn_silu_bwd", "numbat_kernel_class_count", "numbat_kernel_class_name",
+    "numbat_timing_enable", "numbat_timing_read",
 )
 
 
@@ -74,6 +75,11 @@ def load() -> ctypes.CDLL:
             "numbat_conv_bwd_weight": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
             "numbat_bn_silu_fwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
             "numbat_bn_silu_bwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
+            "numbat_kernel_class_count": (ctypes.c_int, []),
+            "numbat_kernel_class_name": (ctypes.c_char_p, [ctypes.c_int]),
+            "numbat_timing_enable": (ctypes.c_int, [ctypes.c_int]),
+            "numbat_timing_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                                   ctypes.POINTER(ctypes.c_int64)]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -187,3 +193,22 @@ def numbat_bn_silu_bwd(p, g, y, save_mean, save_rstd, gamma, beta, dy, dgamma, d
                                      _ptr(beta), _ptr(dy), _ptr(dgamma), _ptr(dbeta), _ptr(residual_grad), _ptr(ws),
                                      _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
            "numbat_bn_silu_bwd")
+
+
+def numbat_kernel_class_count() -> int:
+    return int(load().numbat_kernel_class_count())
+
+
+def numbat_kernel_class_name(kernel_class: int) -> str:
+    return load().numbat_kernel_class_name(kernel_class).decode()
+
+
+def numbat_timing_enable(enable: bool) -> None:
+    _check(load().numbat_timing_enable(int(bool(enable))), "numbat_timing_enable")
+
+
+def numbat_timing_read(kernel_class: int):
+    """(total milliseconds, launches) of one kernel class since timing was enabled."""
+    t, n = ctypes.c_double(), ctypes.c_int64()
+    _check(load().numbat_timing_read(kernel_class, ctypes.byref(t), ctypes.byref(n)), "numbat_timing_read")
+    return t.value, n.value

@@ -21,7 +21,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 14
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -122,3 +122,15 @@ def test_entry_points_refuse_before_launch():
                      ws=None) == nb.ERR_WORKSPACE
     # a failing call leaves its detail text; it names the problem
     assert "workspace" in nb.numbat_last_error()
+
+
+def test_timing_facility_without_launches():
+    n = nb.numbat_kernel_class_count()
+    assert n == 11
+    names = [nb.numbat_kernel_class_name(i) for i in range(n)]
+    assert len(set(names)) == n and all(names)
+    assert nb.numbat_kernel_class_name(n) == ""
+    nb.numbat_timing_enable(True)
+    assert nb.numbat_timing_read(0) == (0.0, 0)
+    nb.numbat_timing_enable(False)
+    assert status_of(nb.numbat_timing_read, n) == nb.ERR_BAD_DESC
