@@ -155,10 +155,16 @@ numbat_status check_conv(const numbat_conv_problem* p, ConvDesc* d) {
     return fail(NUMBAT_ERR_UNSUPPORTED, "more than 2^31-1 pixels (in %lld, out %lld)", (long long)npix_in,
                 (long long)d->m);
   if ((int64_t)d->co * d->kh * d->kw * d->ci > kMaxIndex) return fail(NUMBAT_ERR_UNSUPPORTED, "weight too large");
+  // per-tap element offsets inside a gather are 32-bit
+  if (((int64_t)d->kh * d->w + d->kw) * d->x_pix > kMaxIndex || ((int64_t)d->kh * d->wo + d->kw) * d->y_pix > kMaxIndex)
+    return fail(NUMBAT_ERR_UNSUPPORTED, "row too wide for 32-bit tap offsets");
   return NUMBAT_OK;
 }
 
-TileCfg fwd_tile(const ConvDesc& d) { return igemm_pick(d.m, d.co, d.ci); }
+// 8-channel-aligned inputs take the second-generation kernel, the 3-channel image the scalar-gather one
+bool fwd_vector(const ConvDesc& d) { return d.ci % 8 == 0; }
+
+TileCfg fwd_tile(const ConvDesc& d) { return fwd_vector(d) ? convgemm_pick(d.m, d.co) : igemm_pick(d.m, d.co, d.ci); }
 
 size_t fwd_ws(const ConvDesc& d) {
   const TileCfg t = fwd_tile(d);
@@ -354,32 +360,67 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
   if (st != NUMBAT_OK) return st;
 
   const TileCfg t = fwd_tile(d);
-  IgemmArgs a = base_args();
-  a.src = static_cast<const bf16_t*>(x);
-  a.src_pix = d.x_pix;
-  a.hs = d.h;
-  a.ws = d.w;
-  a.cs = d.ci;
-  a.wt = static_cast<const bf16_t*>(w);
-  a.nout = d.co;
-  a.taps = d.kh * d.kw;
-  a.ktot = a.taps * d.ci;
-  a.gstride_h = d.sh;
-  a.gstride_w = d.sw;
-  for (int r = 0; r < d.kh; ++r)
-    for (int s = 0; s < d.kw; ++s) {
-      const int dh = r - d.ph, dw = s - d.pw;
-      a.off[r * d.kw + s] = (int32_t)((uint32_t)(uint16_t)(int16_t)dh | ((uint32_t)dw << 16));
-    }
-  set_grid(a, d.n, d.ho, d.wo);
-  a.dst = static_cast<bf16_t*>(y);
-  a.dst_pix = d.y_pix;
-  a.hd = d.ho;
-  a.wd = d.wo;
-  a.dstep_h = a.dstep_w = 1;
-  a.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = igemm_launch(a, t, s, KC_CONV_FWD);
+  hipError_t e;
+  if (fwd_vector(d)) {
+    ConvGemmArgs g;
+    std::memset(&g, 0, sizeof g);
+    g.src = static_cast<const bf16_t*>(x);
+    g.src_pix = d.x_pix;
+    g.hs = d.h;
+    g.ws = d.w;
+    g.cs = d.ci;
+    g.nout = d.co;
+    g.nimg = d.n;
+    g.gstride_h = d.sh;
+    g.gstride_w = d.sw;
+    g.dst = static_cast<bf16_t*>(y);
+    g.dst_pix = d.y_pix;
+    g.hd = d.ho;
+    g.wd = d.wo;
+    g.dstep_h = g.dstep_w = 1;
+    g.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
+    g.nphase = 1;
+    GemmPhase& P = g.ph[0];
+    P.wt = static_cast<const bf16_t*>(w);
+    P.taps = d.kh * d.kw;
+    P.ktot = P.taps * d.ci;
+    P.gh = d.ho;
+    P.gw = d.wo;
+    P.m = (int32_t)d.m;
+    P.div_gw = make_fastdiv((uint32_t)d.wo);
+    P.div_ghw = make_fastdiv((uint32_t)(d.ho * d.wo));
+    for (int r = 0; r < d.kh; ++r)
+      for (int q = 0; q < d.kw; ++q)
+        P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
+    e = convgemm_launch(g, t, s, KC_CONV_FWD);
+  } else {
+    IgemmArgs a = base_args();
+    a.src = static_cast<const bf16_t*>(x);
+    a.src_pix = d.x_pix;
+    a.hs = d.h;
+    a.ws = d.w;
+    a.cs = d.ci;
+    a.wt = static_cast<const bf16_t*>(w);
+    a.nout = d.co;
+    a.taps = d.kh * d.kw;
+    a.ktot = a.taps * d.ci;
+    a.gstride_h = d.sh;
+    a.gstride_w = d.sw;
+    for (int r = 0; r < d.kh; ++r)
+      for (int q = 0; q < d.kw; ++q) {
+        const int dh = r - d.ph, dw = q - d.pw;
+        a.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)dh | ((uint32_t)dw << 16));
+      }
+    set_grid(a, d.n, d.ho, d.wo);
+    a.dst = static_cast<bf16_t*>(y);
+    a.dst_pix = d.y_pix;
+    a.hd = d.ho;
+    a.wd = d.wo;
+    a.dstep_h = a.dstep_w = 1;
+    a.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
+    e = igemm_launch(a, t, s, KC_CONV_FWD);
+  }
   if (e != hipSuccess) return hip_fail(e, "conv forward launch");
   if (batch_stats) {
     const int mt = (int)((d.m + t.bm - 1) / t.bm);
@@ -398,6 +439,7 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   if (!aligned16(dy)) return fail(NUMBAT_ERR_ALIGN, "dy must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(w) | reinterpret_cast<uintptr_t>(dx)) & 1u)
     return fail(NUMBAT_ERR_ALIGN, "w and dx must be 2-byte aligned");
+  if (d.ci % 8 == 0 && !aligned16(dx)) return fail(NUMBAT_ERR_ALIGN, "dx must be 16-byte aligned");
   st = check_ws(ws, ws_bytes, bwd_data_ws(d));
   if (st != NUMBAT_OK) return st;
 
@@ -431,39 +473,57 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   bf16_t* wt = static_cast<bf16_t*>(ws);
   hipError_t e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, first, ph, nphase, s);
   if (e != hipSuccess) return hip_fail(e, "data-gradient weight re-layout launch");
+  // all stride phases in launches of up to kMaxPhases phases (blockIdx.z = phase)
+  ConvGemmArgs g;
+  std::memset(&g, 0, sizeof g);
+  g.src = static_cast<const bf16_t*>(dy);
+  g.src_pix = d.y_pix;
+  g.hs = d.ho;
+  g.ws = d.wo;
+  g.cs = d.co;
+  g.nout = d.ci;
+  g.nimg = d.n;
+  g.gstride_h = g.gstride_w = 1;
+  g.dst = static_cast<bf16_t*>(dx);
+  g.dst_pix = d.x_pix;
+  g.hd = d.h;
+  g.wd = d.w;
+  g.dstep_h = d.sh;
+  g.dstep_w = d.sw;
+  g.accumulate = accumulate ? 1 : 0;
   int f = 0;
+  int64_t mmax = 0;
   for (int pa = 0; pa < d.sh; ++pa)
     for (int pb = 0; pb < d.sw; ++pb, ++f) {
       const int gh = pa < d.h ? (d.h - pa + d.sh - 1) / d.sh : 0;
       const int gw = pb < d.w ? (d.w - pb + d.sw - 1) / d.sw : 0;
       if (gh == 0 || gw == 0) continue;
-      IgemmArgs a = base_args();
-      a.src = static_cast<const bf16_t*>(dy);
-      a.src_pix = d.y_pix;
-      a.hs = d.ho;
-      a.ws = d.wo;
-      a.cs = d.co;
-      a.wt = wt + first[f];
-      a.nout = d.ci;
-      a.taps = ph[f].count;
-      a.ktot = a.taps * d.co;
-      a.gstride_h = a.gstride_w = 1;
+      GemmPhase& P = g.ph[g.nphase++];
+      P.wt = wt + first[f];
+      P.taps = ph[f].count;
+      P.ktot = P.taps * d.co;
+      P.gh = gh;
+      P.gw = gw;
+      P.m = d.n * gh * gw;
+      P.div_gw = make_fastdiv((uint32_t)gw);
+      P.div_ghw = make_fastdiv((uint32_t)(gh * gw));
+      P.doff_h = pa;
+      P.doff_w = pb;
       for (int t = 0; t < ph[f].count; ++t)
-        a.off[t] = (int32_t)((uint32_t)(uint16_t)(int16_t)offh[f][t] | ((uint32_t)offw[f][t] << 16));
-      set_grid(a, d.n, gh, gw);
-      a.dst = static_cast<bf16_t*>(dx);
-      a.dst_pix = d.x_pix;
-      a.hd = d.h;
-      a.wd = d.w;
-      a.dstep_h = d.sh;
-      a.dstep_w = d.sw;
-      a.doff_h = pa;
-      a.doff_w = pb;
-      a.accumulate = accumulate ? 1 : 0;
-      const TileCfg t = igemm_pick(a.m, a.nout, a.cs);
-      e = igemm_launch(a, t, s, KC_CONV_DGRAD);
-      if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+        P.off[t] = (int32_t)((uint32_t)(uint16_t)(int16_t)offh[f][t] | ((uint32_t)offw[f][t] << 16));
+      mmax = P.m > mmax ? P.m : mmax;
+      const bool last = (pa == d.sh - 1 && pb == d.sw - 1);
+      if (g.nphase == kMaxPhases || last) {
+        e = convgemm_launch(g, convgemm_pick(mmax, d.ci), s, KC_CONV_DGRAD);
+        if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+        g.nphase = 0;
+        mmax = 0;
+      }
     }
+  if (g.nphase > 0) {
+    e = convgemm_launch(g, convgemm_pick(mmax, d.ci), s, KC_CONV_DGRAD);
+    if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+  }
   return ok();
 }
 

@@ -61,6 +61,38 @@ struct TileCfg {
   int id;  // instantiation id
 };
 
+// Second-generation implicit GEMM (conv_gemm.hip): the same GEMM family as IgemmArgs,
+// for source channel counts that are multiples of 8, with up to four "phases" sharing
+// one launch (blockIdx.z): the stride phases of a data gradient.  Phase p computes rows
+// m < ph[p].m on a ph[p].gh x ph[p].gw grid per image with its own taps, offsets, B
+// matrix and destination offset.
+constexpr int kMaxPhases = 4;
+struct GemmPhase {
+  const bf16_t* wt;     // [nout][ktot], K-major
+  int32_t taps, ktot;   // ktot = taps * cs
+  int32_t gh, gw, m;    // m = nimg * gh * gw
+  FastDiv div_gw, div_ghw;
+  int32_t doff_h, doff_w;
+  int32_t off[kMaxTaps];  // (off_h & 0xffff) | (off_w << 16)
+};
+struct ConvGemmArgs {
+  const bf16_t* src;
+  int64_t src_pix;
+  int32_t hs, ws, cs;
+  int32_t nout, nimg;
+  int32_t gstride_h, gstride_w;
+  bf16_t* dst;
+  int64_t dst_pix;
+  int32_t hd, wd, dstep_h, dstep_w;
+  int32_t accumulate;
+  float2* stats_part;  // phase 0 only: [m tiles][nout] (tile mean, tile M2) or nullptr
+  int32_t nphase;
+  GemmPhase ph[kMaxPhases];
+};
+// tile for a problem with at most m_max rows per phase (depends on the problem only)
+TileCfg convgemm_pick(int64_t m_max, int nout);
+hipError_t convgemm_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
+
 // choose a tile for an igemm problem (depends on the problem only)
 TileCfg igemm_pick(int64_t m, int nout, int cs);
 hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
