@@ -9,6 +9,7 @@ namespace numbat {
 typedef uint16_t bf16_t;  // bf16 bit pattern
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // 16 bytes as a native vector (loads stay loads)
 
 constexpr int kWave = 64;
 
@@ -73,6 +74,11 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const uint4& a, const uint4& b, f3
 }
 
 // sigmoid with the hardware exp2 and reciprocal (about 1 ulp each)
+__device__ __forceinline__ f32x4 mfma16x16x32(const u32x4& a, const u32x4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+
 __device__ __forceinline__ float sigmoidf_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 }  // namespace numbat

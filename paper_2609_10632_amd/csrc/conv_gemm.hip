@@ -13,6 +13,8 @@
 //    other's global-load latency;
 //  * the epilogue stages fp32 results through LDS and writes whole 16-byte vectors of
 //    8 channels (bf16, rounded once, after the optional accumulate).
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace numbat {
@@ -21,6 +23,17 @@ namespace {
 
 constexpr int GK = 32;          // reduction elements per pipeline step
 constexpr int GROW = GK + 8;    // bf16 per LDS row (80 bytes: conflict-free 16-byte fragment reads)
+
+// Sixteen zero bytes in the code object.  Gather lanes that fall on zero padding (or
+// past the end of K or N) load from here instead of being predicated off, so every
+// step issues the same number of loads and the compiler can wait for exactly the ring
+// slot it needs instead of for every outstanding load.
+// (Not const: a const object would live in the constant address space, and a select
+// between it and a global pointer would degrade every gather load to a flat load.)
+__device__ __attribute__((aligned(16))) u32x4 kZero16 = {0u, 0u, 0u, 0u};
+
+template <int V>
+using Ic = std::integral_constant<int, V>;
 
 template <int WM, int TM, int TN>
 struct GemmShape {
@@ -43,7 +56,7 @@ __device__ __forceinline__ void grid_pos(uint32_t m, const GemmPhase& P, uint32_
   gj = rem - gi * (uint32_t)P.gw;
 }
 
-template <int WM, int TM, int TN>
+template <int WM, int TM, int TN, int D>
 __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
   using S = GemmShape<WM, TM, TN>;
   constexpr int BM = S::BM, BN = S::BN, AV = S::AV, BV = S::BV, WTM = S::WTM, WTN = S::WTN;
@@ -124,35 +137,44 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
   const int nk = (P.ktot + GK - 1) / GK;
   __syncthreads();
 
-  uint4 ra[AV], rbv[BV];
-  auto load_tiles = [&](int kt) {
+  static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
+  // D register sets form a ring: the loads of step kt + D are in flight while step kt
+  // computes, so D global round trips overlap instead of one per step.
+  u32x4 ra[D][AV], rbv[D][BV];
+  const bf16_t* zp = reinterpret_cast<const bf16_t*>(&kZero16);
+  auto load_tiles = [&](int kt, u32x4 (&xa)[AV], u32x4 (&xb)[BV]) __attribute__((always_inline)) {
     const bool tok = tapA < P.taps;
-    const int toff = (tok ? s_toff[tapA] : 0) + cA;
+    const int toff = s_toff[tok ? tapA : 0] + cA;
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (tok && ((rmask[i] >> tapA) & 1u)) v = *reinterpret_cast<const uint4*>(rowp[i] + toff);
-      ra[i] = v;
+      const bool ok = tok && ((rmask[i] >> tapA) & 1u);
+      xa[i] = *reinterpret_cast<const u32x4*>(ok ? rowp[i] + toff : zp);
     }
     cA += GK;
-    while (cA >= a.cs) {
-      cA -= a.cs;
-      ++tapA;
+    if (a.cs >= GK) {
+      if (cA >= a.cs) {
+        cA -= a.cs;
+        ++tapA;
+      }
+    } else {
+      while (cA >= a.cs) {
+        cA -= a.cs;
+        ++tapA;
+      }
     }
     const int kb = kt * GK + cv * 8;
 #pragma unroll
     for (int j = 0; j < BV; ++j) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (bok[j] && kb < P.ktot) v = *reinterpret_cast<const uint4*>(bptr[j] + kt * GK);
-      rbv[j] = v;
+      const bool ok = bok[j] && kb < P.ktot;
+      xb[j] = *reinterpret_cast<const u32x4*>(ok ? bptr[j] + kt * GK : zp);
     }
   };
-  auto store_tiles = [&](int buf) {
+  auto store_tiles = [&](int buf, const u32x4 (&xa)[AV], const u32x4 (&xb)[BV]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < AV; ++i) *reinterpret_cast<uint4*>(&As[buf][rb + 64 * i][cv * 8]) = ra[i];
+    for (int i = 0; i < AV; ++i) *reinterpret_cast<u32x4*>(&As[buf][rb + 64 * i][cv * 8]) = xa[i];
 #pragma unroll
     for (int j = 0; j < BV; ++j)
-      if (rb + 64 * j < BN) *reinterpret_cast<uint4*>(&Bs[buf][rb + 64 * j][cv * 8]) = rbv[j];
+      if (rb + 64 * j < BN) *reinterpret_cast<u32x4*>(&Bs[buf][rb + 64 * j][cv * 8]) = xb[j];
   };
 
   f32x4 acc[TM][TN];
@@ -161,27 +183,57 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    load_tiles(0);
-    store_tiles(0);
-    __syncthreads();
-  }
   const int kc = (lane >> 4) * 8;
   const int arow = wm * WTM + (lane & 15), brow = wn * WTN + (lane & 15);
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_tiles(kt + 1);
-    uint4 af[TM], bfr[TN];
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    u32x4 af[TM], bfr[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const uint4*>(&As[buf][arow + i * 16][kc]);
+    for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const u32x4*>(&As[buf][arow + i * 16][kc]);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const uint4*>(&Bs[buf][brow + j * 16][kc]);
+    for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][brow + j * 16][kc]);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
-    if (kt + 1 < nk) store_tiles(buf ^ 1);
+  };
+
+  // One pipeline step with its ring slot fixed at compile time (u = kt mod D), so every
+  // ring access is a register access.
+  auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
+    constexpr int u = decltype(uc)::value;
+    constexpr int nxt = (u + 1) % D;  // slot holding step kt + 1
+    store_tiles((kt + 1) & 1, ra[nxt], rbv[nxt]);
+    load_tiles(kt + 1 + D, ra[nxt], rbv[nxt]);
+    compute(kt & 1);
     __syncthreads();
+  };
+  auto prologue_load = [&](auto dc) __attribute__((always_inline)) {
+    constexpr int d = decltype(dc)::value;
+    load_tiles(d, ra[d], rbv[d]);
+  };
+
+  // prologue: steps 0 .. D-1 in flight, step 0 in LDS, step D in flight in slot 0.
+  // Loads past the end of K read zeros, so they are issued unconditionally.
+  if (nk > 0) {
+    prologue_load(Ic<0>{});
+    if constexpr (D > 1) prologue_load(Ic<1>{});
+    if constexpr (D > 2) prologue_load(Ic<2>{});
+    if constexpr (D > 3) prologue_load(Ic<3>{});
+    store_tiles(0, ra[0], rbv[0]);
+    load_tiles(D, ra[0], rbv[0]);
+    __syncthreads();
+  }
+  for (int kb = 0; kb < nk; kb += D) {
+    step(Ic<0>{}, kb);
+    if constexpr (D > 1) {
+      if (kb + 1 < nk) step(Ic<1 % D>{}, kb + 1);
+    }
+    if constexpr (D > 2) {
+      if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
+    }
+    if constexpr (D > 3) {
+      if (kb + 3 < nk) step(Ic<3 % D>{}, kb + 3);
+    }
   }
 
   // ---- per-channel (mean, M2) of this tile's rows from the fp32 accumulators (phase 0)
@@ -284,18 +336,18 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
 }
 
 struct GInst {
-  int wm, tm, tn;
+  int wm, tm, tn, d;  // waves along M, 16-row tiles per wave, 16-col tiles per wave, prefetch depth
 };
 constexpr GInst kG[] = {
-    {4, 4, 8},  // 0: 256 x 128
-    {4, 4, 6},  // 1: 256 x 96
-    {4, 4, 5},  // 2: 256 x 80
-    {4, 4, 4},  // 3: 256 x 64
-    {4, 4, 3},  // 4: 256 x 48
-    {2, 4, 4},  // 5: 128 x 128
-    {2, 4, 3},  // 6: 128 x 96
-    {2, 4, 2},  // 7: 128 x 64
-    {4, 1, 1},  // 8: 64 x 16
+    {4, 4, 8, 2},  // 0: 256 x 128
+    {4, 4, 6, 3},  // 1: 256 x 96
+    {4, 4, 5, 3},  // 2: 256 x 80
+    {4, 4, 4, 4},  // 3: 256 x 64
+    {4, 4, 3, 4},  // 4: 256 x 48
+    {2, 4, 4, 4},  // 5: 128 x 128
+    {2, 4, 3, 4},  // 6: 128 x 96
+    {2, 4, 2, 4},  // 7: 128 x 64
+    {4, 1, 1, 4},  // 8: 64 x 16
 };
 
 template <int I>
@@ -305,7 +357,7 @@ hipError_t launch_g(const ConvGemmArgs& a, hipStream_t s) {
   int mmax = 0;
   for (int p = 0; p < a.nphase; ++p) mmax = a.ph[p].m > mmax ? a.ph[p].m : mmax;
   dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN), (unsigned)a.nphase);
-  hipLaunchKernelGGL((convgemm_kernel<c.wm, c.tm, c.tn>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((convgemm_kernel<c.wm, c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
