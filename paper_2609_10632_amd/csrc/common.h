@@ -79,6 +79,17 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const u32x4& a, const u32x4& b, f3
                                                  0, 0);
 }
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// 32x32x16 bf16 MFMA, fp32 accumulate (full rate on gfx950; the 16x16x32 form issues at
+// about half the FLOP rate).  Lane l supplies A row (l % 32) and B column (l % 32), each
+// with the 8 reduction elements of group (l / 32); accumulator register r of lane l holds
+// D row 8*(r/4) + 4*(l/32) + (r%4), column (l % 32).
+__device__ __forceinline__ f32x16 mfma32x32x16(const u32x4& a, const u32x4& b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+
 __device__ __forceinline__ float sigmoidf_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 }  // namespace numbat
