@@ -13,7 +13,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxBlocks = 4096;
-constexpr int kVpt = 4;  // 16-byte vectors in flight per thread in the apply kernels
 
 // rows handled together by one block: thread t works on channel vector t % cv of row t / cv
 struct RowLayout {
@@ -95,25 +94,19 @@ __global__ __launch_bounds__(kThreads) void bn_stats_kernel(const bf16_t* y, int
   }
 }
 
-// --- forward apply: out = SiLU((y - mean) * gamma * rstd + beta) [+ residual]
-__global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, FastDiv div_cv, const bf16_t* y,
-                                                          const float* mean_var, const float* gamma,
-                                                          const float* beta, const bf16_t* res, bf16_t* out,
-                                                          float* save_mean, float* save_rstd, float* run_mean,
-                                                          float* run_var) {
-  extern __shared__ float smem[];  // mean[c], scale[c], beta[c]
-  float* s_mean = smem;
-  float* s_scale = smem + a.c;
-  float* s_beta = smem + 2 * a.c;
-  for (int ch = threadIdx.x; ch < a.c; ch += kThreads) {
-    const float mu = mean_var[ch], var = mean_var[a.c + ch];
-    const float rstd = 1.0f / sqrtf(var + a.eps);
-    s_mean[ch] = mu;
-    s_scale[ch] = gamma[ch] * rstd;
-    s_beta[ch] = beta[ch];
-    if (blockIdx.x == 0) {
+// --- forward apply: out = SiLU((y - mean) * gamma * rstd + beta) [+ residual].
+// Thread t always handles channel vector t % cv, so its per-channel constants sit in
+// registers; rows advance by rows_per_iter, four rows in flight.
+__global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t* y, const float* mean_var,
+                                                          const float* gamma, const float* beta, const bf16_t* res,
+                                                          bf16_t* out, float* save_mean, float* save_rstd,
+                                                          float* run_mean, float* run_var, int64_t rows_per_block) {
+  const int t = threadIdx.x;
+  if (blockIdx.x == 0) {
+    for (int ch = t; ch < a.c; ch += kThreads) {
+      const float mu = mean_var[ch], var = mean_var[a.c + ch];
       save_mean[ch] = mu;
-      save_rstd[ch] = rstd;
+      save_rstd[ch] = 1.0f / sqrtf(var + a.eps);
       if (run_mean != nullptr) {
         const float mo = a.momentum;
         run_mean[ch] = (1.0f - mo) * run_mean[ch] + mo * mu;
@@ -121,104 +114,103 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, FastDiv div_
       }
     }
   }
-  __syncthreads();
-  const uint32_t cv = (uint32_t)(a.c >> 3);
-  const int64_t total = a.m * (int64_t)cv;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads * kVpt; base < total; base += (int64_t)gridDim.x * kThreads * kVpt) {
-    uint4 yv[kVpt], rv[kVpt];
-    int64_t rowoff[kVpt];
-    int cbs[kVpt];
+  const RowLayout L = row_layout(a.c);
+  if (t >= L.active) return;
+  const int rr = t / L.cv, cb = (t - rr * L.cv) * 8;
+  float mu[8], sc[8], be[8];
 #pragma unroll
-    for (int j = 0; j < kVpt; ++j) {
-      const int64_t v = base + threadIdx.x + j * kThreads;
-      const uint32_t vv = (uint32_t)(v < total ? v : 0);
-      const uint32_t row = fdiv(vv, div_cv);
-      rowoff[j] = row;
-      cbs[j] = (int)(vv - row * cv) * 8;
-      if (v < total) {
-        yv[j] = *reinterpret_cast<const uint4*>(y + (int64_t)row * a.y_pix + cbs[j]);
-        if (res != nullptr) rv[j] = *reinterpret_cast<const uint4*>(res + (int64_t)row * a.r_pix + cbs[j]);
+  for (int e = 0; e < 8; ++e) {
+    mu[e] = mean_var[cb + e];
+    sc[e] = gamma[cb + e] * (1.0f / sqrtf(mean_var[a.c + cb + e] + a.eps));
+    be[e] = beta[cb + e];
+  }
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
+  const int64_t st = L.rows_per_iter;
+  for (int64_t r = r0 + rr; r < r1; r += 4 * st) {
+    uint4 yv[4], rv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t rj = r + j * st;
+      if (rj < r1) {
+        yv[j] = *reinterpret_cast<const uint4*>(y + rj * a.y_pix + cb);
+        if (res != nullptr) rv[j] = *reinterpret_cast<const uint4*>(res + rj * a.r_pix + cb);
       }
     }
 #pragma unroll
-    for (int j = 0; j < kVpt; ++j) {
-      const int64_t v = base + threadIdx.x + j * kThreads;
-      if (v >= total) continue;
-      const int cb = cbs[j];
+    for (int j = 0; j < 4; ++j) {
+      const int64_t rj = r + j * st;
+      if (rj >= r1) continue;
       float f[8], o[8];
       unpack8(yv[j], f);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float z = (f[e] - s_mean[cb + e]) * s_scale[cb + e] + s_beta[cb + e];
+        const float z = (f[e] - mu[e]) * sc[e] + be[e];
         o[e] = z * sigmoidf_fast(z);
       }
       if (res != nullptr) {
-        float r[8];
-        unpack8(rv[j], r);
+        float q[8];
+        unpack8(rv[j], q);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] += r[e];
+        for (int e = 0; e < 8; ++e) o[e] += q[e];
       }
-      *reinterpret_cast<uint4*>(out + rowoff[j] * a.a_pix + cb) = pack8(o);
+      *reinterpret_cast<uint4*>(out + rj * a.a_pix + cb) = pack8(o);
     }
   }
 }
 
-// --- backward reduce: per-block sums of dz and dz * xhat
+// --- backward reduce: per-block sums of dz and dz * xhat (row layout, constants in registers)
 __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const bf16_t* g, const bf16_t* y,
                                                                  const float* save_mean, const float* save_rstd,
                                                                  const float* gamma, const float* beta,
                                                                  int64_t rows_per_block, float2* part) {
-  extern __shared__ float smem[];  // consts [3][c] then partials [rows_per_iter][c][2]
+  extern __shared__ float s_red[];  // [rows_per_iter][c][2]
   const int c = a.c;
-  float* s_mean = smem;
-  float* s_rstd = smem + c;
-  float* s_gam = smem + 2 * c;
-  float* s_bet = smem + 3 * c;
-  float* s_red = smem + 4 * c;
-  for (int ch = threadIdx.x; ch < c; ch += kThreads) {
-    s_mean[ch] = save_mean[ch];
-    s_rstd[ch] = save_rstd[ch];
-    s_gam[ch] = gamma[ch];
-    s_bet[ch] = beta[ch];
-  }
-  __syncthreads();
   const RowLayout L = row_layout(c);
   const int t = threadIdx.x;
-  const int rr = t / L.cv, cvi = t - rr * L.cv;
-  const int cb = cvi * 8;
+  const int rr = t / L.cv, cb = (t - rr * L.cv) * 8;
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
-  int64_t r1 = r0 + rows_per_block;
-  if (r1 > a.m) r1 = a.m;
+  const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
   float sdz[8], sdx[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) sdz[e] = sdx[e] = 0.f;
   if (t < L.active) {
-    auto accum = [&](const uint4& gu, const uint4& yu) {
-      float gy[8], yy[8];
-      unpack8(gu, gy);
-      unpack8(yu, yy);
+    float mu[8], rs[8], ga[8], be[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float xh = (yy[e] - s_mean[cb + e]) * s_rstd[cb + e];
-        const float z = s_gam[cb + e] * xh + s_bet[cb + e];
-        const float sg = sigmoidf_fast(z);
-        const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
-        sdz[e] += dz;
-        sdx[e] += dz * xh;
-      }
-    };
-    int64_t r = r0 + rr;
-    for (; r + L.rows_per_iter < r1; r += 2 * L.rows_per_iter) {
-      const int64_t r2 = r + L.rows_per_iter;
-      const uint4 g0 = *reinterpret_cast<const uint4*>(g + r * a.a_pix + cb);
-      const uint4 y0 = *reinterpret_cast<const uint4*>(y + r * a.y_pix + cb);
-      const uint4 g1 = *reinterpret_cast<const uint4*>(g + r2 * a.a_pix + cb);
-      const uint4 y1 = *reinterpret_cast<const uint4*>(y + r2 * a.y_pix + cb);
-      accum(g0, y0);
-      accum(g1, y1);
+    for (int e = 0; e < 8; ++e) {
+      mu[e] = save_mean[cb + e];
+      rs[e] = save_rstd[cb + e];
+      ga[e] = gamma[cb + e];
+      be[e] = beta[cb + e];
     }
-    if (r < r1)
-      accum(*reinterpret_cast<const uint4*>(g + r * a.a_pix + cb), *reinterpret_cast<const uint4*>(y + r * a.y_pix + cb));
+    const int64_t st = L.rows_per_iter;
+    for (int64_t r = r0 + rr; r < r1; r += 4 * st) {
+      uint4 gv[4], yv[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t rj = r + j * st;
+        if (rj < r1) {
+          gv[j] = *reinterpret_cast<const uint4*>(g + rj * a.a_pix + cb);
+          yv[j] = *reinterpret_cast<const uint4*>(y + rj * a.y_pix + cb);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (r + j * st >= r1) continue;
+        float gy[8], yy[8];
+        unpack8(gv[j], gy);
+        unpack8(yv[j], yy);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float xh = (yy[e] - mu[e]) * rs[e];
+          const float z = ga[e] * xh + be[e];
+          const float sg = sigmoidf_fast(z);
+          const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
+          sdz[e] += dz;
+          sdx[e] += dz * xh;
+        }
+      }
+    }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       s_red[(rr * c + cb + e) * 2 + 0] = sdz[e];
@@ -236,22 +228,25 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
   }
 }
 
-// --- backward finalize: fixed-order fp64 sums over blocks -> dbeta, dgamma and apply coefficients
-constexpr int kFinGroups = 16;
-__global__ __launch_bounds__(64 * kFinGroups) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c,
-                                                                          int64_t m, const float* save_rstd,
-                                                                          const float* gamma, float* dgamma,
-                                                                          float* dbeta, float* coef) {
-  __shared__ double sa[kFinGroups][64], sb[kFinGroups][64];
-  const int cl = threadIdx.x & 63, gidx = threadIdx.x >> 6;
-  const int ch = blockIdx.x * 64 + cl;
+// --- backward finalize: fixed-order fp64 sums over blocks -> dbeta, dgamma and apply coefficients.
+// 8 channels per block, 32 groups of partial rows per channel (several loads in flight per lane).
+constexpr int kFinCh = 8, kFinGroups = 32;
+__global__ __launch_bounds__(kFinCh * kFinGroups) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c,
+                                                                              int64_t m, const float* save_rstd,
+                                                                              const float* gamma, float* dgamma,
+                                                                              float* dbeta, float* coef) {
+  __shared__ double sa[kFinGroups][kFinCh], sb[kFinGroups][kFinCh];
+  const int cl = threadIdx.x % kFinCh, gidx = threadIdx.x / kFinCh;
+  const int ch = blockIdx.x * kFinCh + cl;
   double p = 0, q = 0;
-  if (ch < c)
+  if (ch < c) {
+#pragma unroll 8
     for (int b = gidx; b < nblocks; b += kFinGroups) {
       const float2 v = part[(int64_t)b * c + ch];
       p += v.x;
       q += v.y;
     }
+  }
   sa[gidx][cl] = p;
   sb[gidx][cl] = q;
   __syncthreads();
@@ -269,76 +264,66 @@ __global__ __launch_bounds__(64 * kFinGroups) void bn_bwd_finalize_kernel(const 
 }
 
 // --- backward apply: dy = gamma * rstd * (dz - dbeta/m - xhat * dgamma/m); residual_grad += g
-__global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, FastDiv div_cv, const bf16_t* g,
-                                                                const bf16_t* y, const float* save_mean,
-                                                                const float* save_rstd, const float* gamma,
-                                                                const float* beta, const float* coef, bf16_t* dy,
-                                                                bf16_t* res_grad) {
-  extern __shared__ float smem[];  // mean, rstd, gamma, beta, k1, k2, k3  [7][c]
+// (row layout, constants in registers, four rows in flight)
+__global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, const bf16_t* g, const bf16_t* y,
+                                                                const float* save_mean, const float* save_rstd,
+                                                                const float* gamma, const float* beta, const float* coef,
+                                                                bf16_t* dy, bf16_t* res_grad, int64_t rows_per_block) {
   const int c = a.c;
-  for (int ch = threadIdx.x; ch < c; ch += kThreads) {
-    smem[ch] = save_mean[ch];
-    smem[c + ch] = save_rstd[ch];
-    smem[2 * c + ch] = gamma[ch];
-    smem[3 * c + ch] = beta[ch];
-    smem[4 * c + ch] = coef[ch];
-    smem[5 * c + ch] = coef[c + ch];
-    smem[6 * c + ch] = coef[2 * c + ch];
-  }
-  __syncthreads();
-  const uint32_t cv = (uint32_t)(c >> 3);
-  const int64_t total = a.m * (int64_t)cv;
-  for (int64_t base = (int64_t)blockIdx.x * kThreads * kVpt; base < total; base += (int64_t)gridDim.x * kThreads * kVpt) {
-    uint4 gv[kVpt], yv[kVpt], rv[kVpt];
-    int64_t rows[kVpt];
-    int cbs[kVpt];
+  const RowLayout L = row_layout(c);
+  const int t = threadIdx.x;
+  if (t >= L.active) return;
+  const int rr = t / L.cv, cb = (t - rr * L.cv) * 8;
+  float mu[8], rs[8], ga[8], be[8], k1[8], k2[8], k3[8];
 #pragma unroll
-    for (int j = 0; j < kVpt; ++j) {
-      const int64_t v = base + threadIdx.x + j * kThreads;
-      const uint32_t vv = (uint32_t)(v < total ? v : 0);
-      const uint32_t row = fdiv(vv, div_cv);
-      rows[j] = row;
-      cbs[j] = (int)(vv - row * cv) * 8;
-      if (v < total) {
-        gv[j] = *reinterpret_cast<const uint4*>(g + (int64_t)row * a.a_pix + cbs[j]);
-        yv[j] = *reinterpret_cast<const uint4*>(y + (int64_t)row * a.y_pix + cbs[j]);
-        if (res_grad != nullptr) rv[j] = *reinterpret_cast<const uint4*>(res_grad + (int64_t)row * a.r_pix + cbs[j]);
+  for (int e = 0; e < 8; ++e) {
+    mu[e] = save_mean[cb + e];
+    rs[e] = save_rstd[cb + e];
+    ga[e] = gamma[cb + e];
+    be[e] = beta[cb + e];
+    k1[e] = coef[cb + e];
+    k2[e] = coef[c + cb + e];
+    k3[e] = coef[2 * c + cb + e];
+  }
+  const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
+  const int64_t st = L.rows_per_iter;
+  for (int64_t r = r0 + rr; r < r1; r += 4 * st) {
+    uint4 gv[4], yv[4], rv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t rj = r + j * st;
+      if (rj < r1) {
+        gv[j] = *reinterpret_cast<const uint4*>(g + rj * a.a_pix + cb);
+        yv[j] = *reinterpret_cast<const uint4*>(y + rj * a.y_pix + cb);
+        if (res_grad != nullptr) rv[j] = *reinterpret_cast<const uint4*>(res_grad + rj * a.r_pix + cb);
       }
     }
 #pragma unroll
-    for (int j = 0; j < kVpt; ++j) {
-      const int64_t v = base + threadIdx.x + j * kThreads;
-      if (v >= total) continue;
-      const int cb = cbs[j];
+    for (int j = 0; j < 4; ++j) {
+      const int64_t rj = r + j * st;
+      if (rj >= r1) continue;
       float gy[8], yy[8], o[8];
       unpack8(gv[j], gy);
       unpack8(yv[j], yy);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int ch = cb + e;
-        const float xh = (yy[e] - smem[ch]) * smem[c + ch];
-        const float z = smem[2 * c + ch] * xh + smem[3 * c + ch];
+        const float xh = (yy[e] - mu[e]) * rs[e];
+        const float z = ga[e] * xh + be[e];
         const float sg = sigmoidf_fast(z);
         const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
-        o[e] = smem[4 * c + ch] * (dz - smem[5 * c + ch] - xh * smem[6 * c + ch]);
+        o[e] = k1[e] * (dz - k2[e] - xh * k3[e]);
       }
-      *reinterpret_cast<uint4*>(dy + rows[j] * a.dy_pix + cb) = pack8(o);
+      *reinterpret_cast<uint4*>(dy + rj * a.dy_pix + cb) = pack8(o);
       if (res_grad != nullptr) {
-        float r[8];
-        unpack8(rv[j], r);
+        float q[8];
+        unpack8(rv[j], q);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) r[e] += gy[e];
-        *reinterpret_cast<uint4*>(res_grad + rows[j] * a.r_pix + cb) = pack8(r);
+        for (int e = 0; e < 8; ++e) q[e] += gy[e];
+        *reinterpret_cast<uint4*>(res_grad + rj * a.r_pix + cb) = pack8(q);
       }
     }
   }
-}
-
-int grid_for_elems(int64_t vecs) {
-  int64_t b = (vecs + kThreads * kVpt - 1) / (kThreads * kVpt);
-  if (b > 8192) b = 8192;
-  if (b < 1) b = 1;
-  return (int)b;
 }
 
 size_t reduce_smem(int c) {
@@ -374,14 +359,26 @@ hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int n
   return stats_merge_launch(part, nb, (int)rpb, a.m, a.c, mean_var, s);
 }
 
+// apply kernels: about 16 rows of 8 channels per thread
+static int apply_blocks(int64_t m, int c, int64_t* rows_per_block) {
+  const int cv = c / 8;
+  int rpi = kThreads / cv;
+  if (rpi < 1) rpi = 1;
+  int64_t b = (m + (int64_t)rpi * 16 - 1) / ((int64_t)rpi * 16);
+  if (b > 16384) b = 16384;
+  if (b < 1) b = 1;
+  *rows_per_block = (m + b - 1) / b;
+  return (int)((m + *rows_per_block - 1) / *rows_per_block);
+}
+
 hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var, const float* gamma,
                          const float* beta, const bf16_t* res, bf16_t* out, float* save_mean, float* save_rstd,
                          float* run_mean, float* run_var, hipStream_t s) {
-  const int64_t vecs = a.m * (a.c / 8);
-  const FastDiv d = make_fastdiv((uint32_t)(a.c / 8));
+  int64_t rpb = 0;
+  const int nb = apply_blocks(a.m, a.c, &rpb);
   trace_begin(KC_BN_FWD, s);
-  hipLaunchKernelGGL(bn_fwd_kernel, dim3(grid_for_elems(vecs)), dim3(kThreads), 3 * a.c * sizeof(float), s, a, d, y,
-                     mean_var, gamma, beta, res, out, save_mean, save_rstd, run_mean, run_var);
+  hipLaunchKernelGGL(bn_fwd_kernel, dim3(nb), dim3(kThreads), 0, s, a, y, mean_var, gamma, beta, res, out, save_mean,
+                     save_rstd, run_mean, run_var, rpb);
   trace_end(KC_BN_FWD, s);
   return hipGetLastError();
 }
@@ -393,22 +390,22 @@ hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, cons
   const int nb = (int)((a.m + rpb - 1) / rpb);
   float2* part = reinterpret_cast<float2*>(part2);
   trace_begin(KC_BN_BWD_REDUCE, s);
-  hipLaunchKernelGGL(bn_bwd_reduce_kernel, dim3(nb), dim3(kThreads), 4 * a.c * sizeof(float) + reduce_smem(a.c), s,
-                     a, g, y, save_mean, save_rstd, gamma, beta, rpb, part);
+  hipLaunchKernelGGL(bn_bwd_reduce_kernel, dim3(nb), dim3(kThreads), reduce_smem(a.c), s, a, g, y, save_mean,
+                     save_rstd, gamma, beta, rpb, part);
   trace_end(KC_BN_BWD_REDUCE, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   trace_begin(KC_BN_BWD_FINALIZE, s);
-  hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3((a.c + 63) / 64), dim3(64 * kFinGroups), 0, s, part, nb, a.c, a.m,
-                     save_rstd, gamma, dgamma, dbeta, coef);
+  hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3((a.c + kFinCh - 1) / kFinCh), dim3(kFinCh * kFinGroups), 0, s, part, nb,
+                     a.c, a.m, save_rstd, gamma, dgamma, dbeta, coef);
   trace_end(KC_BN_BWD_FINALIZE, s);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t vecs = a.m * (a.c / 8);
-  const FastDiv d = make_fastdiv((uint32_t)(a.c / 8));
+  int64_t arpb = 0;
+  const int anb = apply_blocks(a.m, a.c, &arpb);
   trace_begin(KC_BN_BWD_APPLY, s);
-  hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(grid_for_elems(vecs)), dim3(kThreads), 7 * a.c * sizeof(float), s, a,
-                     d, g, y, save_mean, save_rstd, gamma, beta, coef, dy, res_grad);
+  hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(anb), dim3(kThreads), 0, s, a, g, y, save_mean, save_rstd, gamma, beta,
+                     coef, dy, res_grad, arpb);
   trace_end(KC_BN_BWD_APPLY, s);
   return hipGetLastError();
 }

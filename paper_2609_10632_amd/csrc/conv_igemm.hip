@@ -330,15 +330,18 @@ hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s, int
 
 namespace {
 
-constexpr int kMergeGroups = 16;
+// 8 channels per block, 32 groups of tiles per channel: consecutive lanes read the
+// partials of consecutive channels (64-byte segments) and each lane keeps several loads
+// in flight.
+constexpr int kMergeCh = 8, kMergeGroups = 32;
 
-__global__ __launch_bounds__(64 * kMergeGroups) void stats_merge_kernel(const float2* part, int mtiles,
-                                                                        int tile_rows, int64_t m, int c,
-                                                                        float* mean_var) {
-  __shared__ double s1s[kMergeGroups][64], s2s[kMergeGroups][64], m2s[kMergeGroups][64];
-  const int cl = threadIdx.x & 63;
-  const int g = threadIdx.x >> 6;
-  const int ch = blockIdx.x * 64 + cl;
+__global__ __launch_bounds__(kMergeCh * kMergeGroups) void stats_merge_kernel(const float2* part, int mtiles,
+                                                                              int tile_rows, int64_t m, int c,
+                                                                              float* mean_var) {
+  __shared__ double s1s[kMergeGroups][kMergeCh], s2s[kMergeGroups][kMergeCh], m2s[kMergeGroups][kMergeCh];
+  const int cl = threadIdx.x % kMergeCh;
+  const int g = threadIdx.x / kMergeCh;
+  const int ch = blockIdx.x * kMergeCh + cl;
   double s1 = 0, s2 = 0, m2 = 0;
   double K = 0;
   if (ch < c) {
@@ -347,7 +350,7 @@ __global__ __launch_bounds__(64 * kMergeGroups) void stats_merge_kernel(const fl
     const int full = (int)((m / tile_rows) < mtiles ? (m / tile_rows) : mtiles);
     const double nt = (double)tile_rows;
     int t = g;
-#pragma unroll 4
+#pragma unroll 8
     for (; t < full; t += kMergeGroups) {
       const float2 p = part[(int64_t)t * c + ch];
       const double d = (double)p.x - K;
@@ -387,8 +390,8 @@ __global__ __launch_bounds__(64 * kMergeGroups) void stats_merge_kernel(const fl
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,
                               hipStream_t s) {
   trace_begin(KC_STATS_MERGE, s);
-  hipLaunchKernelGGL(stats_merge_kernel, dim3((c + 63) / 64), dim3(64 * kMergeGroups), 0, s, part, mtiles,
-                     tile_rows, m, c, mean_var);
+  hipLaunchKernelGGL(stats_merge_kernel, dim3((c + kMergeCh - 1) / kMergeCh), dim3(kMergeCh * kMergeGroups), 0, s,
+                     part, mtiles, tile_rows, m, c, mean_var);
   trace_end(KC_STATS_MERGE, s);
   return hipGetLastError();
 }
