@@ -125,7 +125,9 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
  * y: bf16 NHWC (pixel stride y_pixel_stride), fp32 accumulation rounded to nearest even.
  * batch_stats: NULL, or fp32 [2*c_out] receiving the batch mean (first c_out entries) and
  * biased batch variance (next c_out) of every output channel over the n*ho*wo rows, taken
- * from the fp32 accumulators before rounding (BN statistics in fp32, Sec. 3.2). */
+ * from the fp32 accumulators before rounding (BN statistics in fp32, Sec. 3.2).
+ * ws: numbat_workspace_size(NUMBAT_OP_CONV_FWD) bytes; it may be NULL only when batch_stats
+ * is NULL and c_in is a multiple of 8 (a narrower input is repacked into the workspace). */
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream);
 

@@ -43,7 +43,7 @@ hipEvent_t pool_event() {
 const char* const kClassNames[KC_COUNT] = {
     "conv_fwd_igemm", "stats_merge", "dgrad_weight_relayout", "conv_dgrad_igemm", "wgrad_igemm",
     "wgrad_splitk_reduce", "bn_stats", "bn_silu_fwd_apply", "bn_silu_bwd_reduce", "bn_silu_bwd_finalize",
-    "bn_silu_bwd_apply"};
+    "bn_silu_bwd_apply", "narrow_input_pack"};
 
 }  // namespace
 
@@ -161,26 +161,36 @@ numbat_status check_conv(const numbat_conv_problem* p, ConvDesc* d) {
   return NUMBAT_OK;
 }
 
-// 8-channel-aligned inputs take the second-generation kernel, the 3-channel image the scalar-gather one
-bool fwd_vector(const ConvDesc& d) { return d.ci % 8 == 0; }
+// Inputs with fewer than 8 channels (the RGB image) are repacked into 8-channel pixels
+// in the workspace (channels ci..7 zero, weights likewise), so every convolution runs on
+// the 16-byte-vector kernels.
+bool narrow(const ConvDesc& d) { return d.ci % 8 != 0; }
+size_t x8_bytes(const ConvDesc& d) { return round_up((size_t)d.n * d.h * d.w * 16, 256); }
+size_t w8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 16, 256); }
 
-TileCfg fwd_tile(const ConvDesc& d) { return fwd_vector(d) ? convgemm_pick(d.m, d.co) : igemm_pick(d.m, d.co, d.ci); }
+TileCfg fwd_tile(const ConvDesc& d) { return convgemm_pick(d.m, d.co); }
 
-size_t fwd_ws(const ConvDesc& d) {
+size_t fwd_stats_bytes(const ConvDesc& d) {
   const TileCfg t = fwd_tile(d);
   const int64_t mt = (d.m + t.bm - 1) / t.bm;
   return round_up((size_t)mt * d.co * sizeof(float2), 256);
 }
 
+size_t fwd_ws(const ConvDesc& d) { return fwd_stats_bytes(d) + (narrow(d) ? x8_bytes(d) + w8_bytes(d) : 0); }
+
 size_t bwd_data_ws(const ConvDesc& d) { return round_up((size_t)d.kh * d.kw * d.ci * d.co * 2, 256); }
 
+size_t dw8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 8 * sizeof(float), 256); }
+
 size_t bwd_weight_ws(const ConvDesc& d, int* splits, int64_t* rps) {
-  const int ktot = d.kh * d.kw * d.ci;
+  const int ci = narrow(d) ? 8 : d.ci;
+  const int ktot = d.kh * d.kw * ci;
   int64_t r = 0;
   const int s = wgrad_pick_splits(d.m, d.co, ktot, &r);
   if (splits) *splits = s;
   if (rps) *rps = r;
-  return s > 1 ? round_up((size_t)s * d.co * ktot * sizeof(float), 256) : 0;
+  const size_t part = s > 1 ? round_up((size_t)s * d.co * ktot * sizeof(float), 256) : 0;
+  return part + (narrow(d) ? x8_bytes(d) + dw8_bytes(d) : 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -232,21 +242,6 @@ numbat_status check_ws(void* ws, size_t have, size_t need) {
   if (have < need) return fail(NUMBAT_ERR_WORKSPACE, "workspace of %zu bytes required, got %zu", need, have);
   if (!aligned16(ws)) return fail(NUMBAT_ERR_ALIGN, "workspace must be 16-byte aligned");
   return NUMBAT_OK;
-}
-
-IgemmArgs base_args() {
-  IgemmArgs a;
-  std::memset(&a, 0, sizeof a);
-  return a;
-}
-
-void set_grid(IgemmArgs& a, int nimg, int gh, int gw) {
-  a.nimg = nimg;
-  a.gh = gh;
-  a.gw = gw;
-  a.m = nimg * gh * gw;
-  a.div_gw = make_fastdiv((uint32_t)gw);
-  a.div_ghw = make_fastdiv((uint32_t)(gh * gw));
 }
 
 }  // namespace
@@ -348,83 +343,73 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
   numbat_status st = check_conv(p, &d);
   if (st != NUMBAT_OK) return st;
   if (x == nullptr || w == nullptr || y == nullptr) return fail(NUMBAT_ERR_NULL, "x, w and y are required");
-  const bool vec_in = d.ci % 8 == 0;
+  const bool vec_in = !narrow(d);
   if ((vec_in && (!aligned16(x) || !aligned16(w))) || !aligned16(y))
     return fail(NUMBAT_ERR_ALIGN, "x, w, y must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w)) & 1u)
     return fail(NUMBAT_ERR_ALIGN, "x and w must be 2-byte aligned");
   if (batch_stats != nullptr && (reinterpret_cast<uintptr_t>(batch_stats) & 3u))
     return fail(NUMBAT_ERR_ALIGN, "batch_stats must be 4-byte aligned");
-  const size_t need = batch_stats ? fwd_ws(d) : 0;
+  const size_t need = (batch_stats ? fwd_stats_bytes(d) : 0) + (vec_in ? 0 : x8_bytes(d) + w8_bytes(d));
   st = check_ws(ws, ws_bytes, need);
   if (st != NUMBAT_OK) return st;
 
   const TileCfg t = fwd_tile(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
-  if (fwd_vector(d)) {
-    ConvGemmArgs g;
-    std::memset(&g, 0, sizeof g);
-    g.src = static_cast<const bf16_t*>(x);
-    g.src_pix = d.x_pix;
-    g.hs = d.h;
-    g.ws = d.w;
-    g.cs = d.ci;
-    g.nout = d.co;
-    g.nimg = d.n;
-    g.gstride_h = d.sh;
-    g.gstride_w = d.sw;
-    g.dst = static_cast<bf16_t*>(y);
-    g.dst_pix = d.y_pix;
-    g.hd = d.ho;
-    g.wd = d.wo;
-    g.dstep_h = g.dstep_w = 1;
-    g.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
-    g.nphase = 1;
-    GemmPhase& P = g.ph[0];
-    P.wt = static_cast<const bf16_t*>(w);
-    P.taps = d.kh * d.kw;
-    P.ktot = P.taps * d.ci;
-    P.gh = d.ho;
-    P.gw = d.wo;
-    P.m = (int32_t)d.m;
-    P.div_gw = make_fastdiv((uint32_t)d.wo);
-    P.div_ghw = make_fastdiv((uint32_t)(d.ho * d.wo));
-    for (int r = 0; r < d.kh; ++r)
-      for (int q = 0; q < d.kw; ++q)
-        P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
-    e = convgemm_launch(g, t, s, KC_CONV_FWD);
-  } else {
-    IgemmArgs a = base_args();
-    a.src = static_cast<const bf16_t*>(x);
-    a.src_pix = d.x_pix;
-    a.hs = d.h;
-    a.ws = d.w;
-    a.cs = d.ci;
-    a.wt = static_cast<const bf16_t*>(w);
-    a.nout = d.co;
-    a.taps = d.kh * d.kw;
-    a.ktot = a.taps * d.ci;
-    a.gstride_h = d.sh;
-    a.gstride_w = d.sw;
-    for (int r = 0; r < d.kh; ++r)
-      for (int q = 0; q < d.kw; ++q) {
-        const int dh = r - d.ph, dw = q - d.pw;
-        a.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)dh | ((uint32_t)dw << 16));
-      }
-    set_grid(a, d.n, d.ho, d.wo);
-    a.dst = static_cast<bf16_t*>(y);
-    a.dst_pix = d.y_pix;
-    a.hd = d.ho;
-    a.wd = d.wo;
-    a.dstep_h = a.dstep_w = 1;
-    a.stats_part = batch_stats ? static_cast<float2*>(ws) : nullptr;
-    e = igemm_launch(a, t, s, KC_CONV_FWD);
+  char* wsp = static_cast<char*>(ws);
+  float2* part = batch_stats ? reinterpret_cast<float2*>(wsp) : nullptr;
+  const bf16_t* src = static_cast<const bf16_t*>(x);
+  const bf16_t* wt = static_cast<const bf16_t*>(w);
+  int64_t src_pix = d.x_pix;
+  int cs = d.ci;
+  if (!vec_in) {
+    bf16_t* x8 = reinterpret_cast<bf16_t*>(wsp + (batch_stats ? fwd_stats_bytes(d) : 0));
+    bf16_t* w8 = reinterpret_cast<bf16_t*>(reinterpret_cast<char*>(x8) + x8_bytes(d));
+    e = pack8_launch(src, d.x_pix, d.ci, (int64_t)d.n * d.h * d.w, x8, s);
+    if (e != hipSuccess) return hip_fail(e, "input repack launch");
+    e = pack8_launch(wt, d.ci, d.ci, (int64_t)d.co * d.kh * d.kw, w8, s);
+    if (e != hipSuccess) return hip_fail(e, "weight repack launch");
+    src = x8;
+    wt = w8;
+    src_pix = 8;
+    cs = 8;
   }
+  ConvGemmArgs g;
+  std::memset(&g, 0, sizeof g);
+  g.src = src;
+  g.src_pix = src_pix;
+  g.hs = d.h;
+  g.ws = d.w;
+  g.cs = cs;
+  g.nout = d.co;
+  g.nimg = d.n;
+  g.gstride_h = d.sh;
+  g.gstride_w = d.sw;
+  g.dst = static_cast<bf16_t*>(y);
+  g.dst_pix = d.y_pix;
+  g.hd = d.ho;
+  g.wd = d.wo;
+  g.dstep_h = g.dstep_w = 1;
+  g.stats_part = part;
+  g.nphase = 1;
+  GemmPhase& P = g.ph[0];
+  P.wt = wt;
+  P.taps = d.kh * d.kw;
+  P.ktot = P.taps * cs;
+  P.gh = d.ho;
+  P.gw = d.wo;
+  P.m = (int32_t)d.m;
+  P.div_gw = make_fastdiv((uint32_t)d.wo);
+  P.div_ghw = make_fastdiv((uint32_t)(d.ho * d.wo));
+  for (int r = 0; r < d.kh; ++r)
+    for (int q = 0; q < d.kw; ++q)
+      P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
+  e = convgemm_launch(g, t, s, KC_CONV_FWD);
   if (e != hipSuccess) return hip_fail(e, "conv forward launch");
   if (batch_stats) {
     const int mt = (int)((d.m + t.bm - 1) / t.bm);
-    e = stats_merge_launch(static_cast<const float2*>(ws), mt, t.bm, d.m, d.co, batch_stats, s);
+    e = stats_merge_launch(part, mt, t.bm, d.m, d.co, batch_stats, s);
     if (e != hipSuccess) return hip_fail(e, "batch statistics merge launch");
   }
   return ok();
@@ -533,7 +518,7 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   numbat_status st = check_conv(p, &d);
   if (st != NUMBAT_OK) return st;
   if (x == nullptr || dy == nullptr || dw == nullptr) return fail(NUMBAT_ERR_NULL, "x, dy and dw are required");
-  if ((d.ci % 8 == 0 && !aligned16(x)) || !aligned16(dy)) return fail(NUMBAT_ERR_ALIGN, "x and dy must be 16-byte aligned");
+  if ((!narrow(d) && !aligned16(x)) || !aligned16(dy)) return fail(NUMBAT_ERR_ALIGN, "x and dy must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(x) & 1u) || (reinterpret_cast<uintptr_t>(dw) & 3u))
     return fail(NUMBAT_ERR_ALIGN, "x must be 2-byte and dw 4-byte aligned");
   int splits = 1;
@@ -541,16 +526,35 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   const size_t need = bwd_weight_ws(d, &splits, &rps);
   st = check_ws(ws, ws_bytes, need);
   if (st != NUMBAT_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  const int ci = narrow(d) ? 8 : d.ci;
+  const int ktot = d.kh * d.kw * ci;
+  char* wsp = static_cast<char*>(ws);
+  const size_t part_bytes = splits > 1 ? round_up((size_t)splits * d.co * ktot * sizeof(float), 256) : 0;
+  const bf16_t* xs = static_cast<const bf16_t*>(x);
+  int64_t x_pix = d.x_pix;
+  float* target = dw;  // where the weight-gradient GEMM (or its split reduction) writes
+  int acc = accumulate ? 1 : 0;
+  if (narrow(d)) {
+    bf16_t* x8 = reinterpret_cast<bf16_t*>(wsp + part_bytes);
+    target = reinterpret_cast<float*>(wsp + part_bytes + x8_bytes(d));
+    e = pack8_launch(xs, d.x_pix, d.ci, (int64_t)d.n * d.h * d.w, x8, s);
+    if (e != hipSuccess) return hip_fail(e, "input repack launch");
+    xs = x8;
+    x_pix = 8;
+    acc = 0;
+  }
   WgradArgs a;
   std::memset(&a, 0, sizeof a);
-  a.x = static_cast<const bf16_t*>(x);
-  a.x_pix = d.x_pix;
+  a.x = xs;
+  a.x_pix = x_pix;
   a.dy = static_cast<const bf16_t*>(dy);
   a.dy_pix = d.y_pix;
   a.n = d.n;
   a.h = d.h;
   a.w = d.w;
-  a.ci = d.ci;
+  a.ci = ci;
   a.co = d.co;
   a.kh = d.kh;
   a.kw = d.kw;
@@ -561,17 +565,20 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   a.ho = d.ho;
   a.wo = d.wo;
   a.m = d.m;
-  a.ktot = d.kh * d.kw * d.ci;
+  a.ktot = ktot;
   a.splits = splits;
   a.rows_per_split = rps;
-  a.out = splits > 1 ? static_cast<float*>(ws) : dw;
-  a.accumulate = accumulate ? 1 : 0;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = wgrad_launch(a, s);
+  a.out = splits > 1 ? reinterpret_cast<float*>(wsp) : target;
+  a.accumulate = acc;
+  e = wgrad_launch(a, s);
   if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
   if (splits > 1) {
-    e = splitk_reduce_launch(static_cast<const float*>(ws), splits, (int64_t)d.co * a.ktot, dw, a.accumulate, s);
+    e = splitk_reduce_launch(reinterpret_cast<const float*>(wsp), splits, (int64_t)d.co * ktot, target, acc, s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient reduction launch");
+  }
+  if (narrow(d)) {
+    e = unpack_dw_launch(target, dw, (int64_t)d.co * d.kh * d.kw, d.ci, accumulate ? 1 : 0, s);
+    if (e != hipSuccess) return hip_fail(e, "weight-gradient channel extraction launch");
   }
   return ok();
 }

@@ -42,7 +42,7 @@ __device__ __forceinline__ void transpose8x8(const uint4 P[8], uint4 Q[8]) {
   }
 }
 
-template <int TM, int TN, bool SMALLC>
+template <int TM, int TN>
 __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo, FastDiv div_howo) {
   constexpr int BMO = 2 * TM * 16;  // output channels per tile
   constexpr int BNK = 2 * TN * 16;  // k columns per tile
@@ -77,7 +77,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
     u_grp[t] = v >> 3;  // channel group (dy) or k group (x)
     u_pb[t] = v & 7;    // pixel block within the step
     u_dh[t] = u_dw[t] = u_c[t] = 0;
-    if (isx && !SMALLC) {
+    if (isx) {
       const int k = k0 + u_grp[t] * 8;
       const int tap = k / a.ci;
       u_c[t] = k - tap * a.ci;
@@ -118,27 +118,11 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
             const uint32_t q = rem - p * (uint32_t)a.wo;
             const int ihb = (int)p * a.sh, iwb = (int)q * a.sw;
             const int64_t ibase = (int64_t)img * a.h;
-            if (!SMALLC) {
+            {
               const int k = k0 + u_grp[t] * 8;
               const int ih = ihb + u_dh[t], iw = iwb + u_dw[t];
               if (k < a.ktot && (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w)
                 P[j] = *reinterpret_cast<const uint4*>(a.x + ((ibase + ih) * a.w + iw) * a.x_pix + u_c[t]);
-            } else {
-              uint32_t hv[8];
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                hv[e] = 0;
-                const int k = k0 + u_grp[t] * 8 + e;
-                if (k < a.ktot) {
-                  const int tap = k / a.ci;
-                  const int c = k - tap * a.ci;
-                  const int ih = ihb + tap / a.kw - a.ph, iw = iwb + tap % a.kw - a.pw;
-                  if ((unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w)
-                    hv[e] = a.x[((ibase + ih) * a.w + iw) * a.x_pix + c];
-                }
-              }
-              P[j] = make_uint4(hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16), hv[4] | (hv[5] << 16),
-                                hv[6] | (hv[7] << 16));
             }
           }
         }
@@ -222,10 +206,7 @@ hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
   trace_begin(KC_WGRAD, s);
-  if (a.ci % 8 == 0)
-    hipLaunchKernelGGL((wgrad_kernel<TM, TN, false>), grid, dim3(256), 0, s, a, dwo, dhw);
-  else
-    hipLaunchKernelGGL((wgrad_kernel<TM, TN, true>), grid, dim3(256), 0, s, a, dwo, dhw);
+  hipLaunchKernelGGL((wgrad_kernel<TM, TN>), grid, dim3(256), 0, s, a, dwo, dhw);
   trace_end(KC_WGRAD, s);
   return hipGetLastError();
 }

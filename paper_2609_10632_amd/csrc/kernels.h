@@ -25,46 +25,26 @@ enum KernelClass {
   KC_BN_BWD_REDUCE,     // BN + SiLU backward reduce
   KC_BN_BWD_FINALIZE,   // BN + SiLU backward finalize
   KC_BN_BWD_APPLY,      // BN + SiLU backward apply
+  KC_PACK,              // 8-channel repacking of a 3-channel image input
   KC_COUNT
 };
 void trace_begin(int cls, hipStream_t s);
 void trace_end(int cls, hipStream_t s);
-
-// One implicit GEMM D[M][N] = A[M][K] * B[N][K]^T where
-//   row m   = (img, gi, gj) on a gh x gw grid per image,
-//   col     = output channel of the GEMM (N = nout),
-//   k       = (tap, c), c < cs, K = taps * cs,
-//   A[m][k] = src[img, gi*gstride_h + off_h[tap], gj*gstride_w + off_w[tap], c]  (0 outside hs x ws),
-//   B[n][k] = wt[n * ktot + k],
-// and D is written (bf16) to dst[img, gi*dstep_h + doff_h, gj*dstep_w + doff_w, col].
-// The forward convolution and every stride phase of the data gradient are such GEMMs.
-struct IgemmArgs {
-  const bf16_t* src;
-  int64_t src_pix;
-  int32_t hs, ws, cs;
-  const bf16_t* wt;
-  int32_t nout, taps, ktot;
-  int32_t gstride_h, gstride_w;
-  int32_t off[kMaxTaps];  // (off_h & 0xffff) | (off_w << 16), both signed 16-bit
-  int32_t nimg, gh, gw, m;
-  FastDiv div_gw, div_ghw;
-  bf16_t* dst;
-  int64_t dst_pix;
-  int32_t hd, wd;
-  int32_t dstep_h, dstep_w, doff_h, doff_w;
-  int32_t accumulate;
-  float2* stats_part;  // [m tiles][nout] (tile mean, tile M2) or nullptr
-};
 
 struct TileCfg {
   int bm, bn;
   int id;  // instantiation id
 };
 
-// Second-generation implicit GEMM (conv_gemm.hip): the same GEMM family as IgemmArgs,
-// for source channel counts that are multiples of 8, with up to four "phases" sharing
-// one launch (blockIdx.z): the stride phases of a data gradient.  Phase p computes rows
-// m < ph[p].m on a ph[p].gh x ph[p].gw grid per image with its own taps, offsets, B
+// Implicit GEMM (conv_gemm.hip) D[M][N] = A[M][K] * B[N][K]^T for source channel
+// counts that are multiples of 8:
+//   row m   = (img, gi, gj) on a gh x gw grid per image,
+//   k       = (tap, c), c < cs, K = taps * cs,
+//   A[m][k] = src[img, gi*gstride_h + off_h[tap], gj*gstride_w + off_w[tap], c]  (0 outside hs x ws),
+//   B[n][k] = wt[n * ktot + k],
+// D written (bf16) to dst[img, gi*dstep_h + doff_h, gj*dstep_w + doff_w, n].  The forward
+// convolution is one such GEMM; the stride phases of a data gradient are up to four
+// "phases" sharing one launch (blockIdx.z), each with its own grid, taps, offsets, B
 // matrix and destination offset.
 constexpr int kMaxPhases = 4;
 struct GemmPhase {
@@ -93,9 +73,10 @@ struct ConvGemmArgs {
 TileCfg convgemm_pick(int64_t m_max, int nout);
 hipError_t convgemm_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
 
-// choose a tile for an igemm problem (depends on the problem only)
-TileCfg igemm_pick(int64_t m, int nout, int cs);
-hipError_t igemm_launch(const IgemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
+// 8-channel repacking of a narrow (ci < 8) NHWC tensor, and extraction of ci channels
+// from a weight gradient computed on the repacked layout
+hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s);
+hipError_t unpack_dw_launch(const float* dw8, float* dw, int64_t rows, int ci, int accumulate, hipStream_t s);
 
 // merge per-tile (mean, M2) partials into batch mean / biased variance, fixed order
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,

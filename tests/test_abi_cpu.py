@@ -126,7 +126,7 @@ def test_entry_points_refuse_before_launch():
 
 def test_timing_facility_without_launches():
     n = nb.numbat_kernel_class_count()
-    assert n == 11
+    assert n == 12
     names = [nb.numbat_kernel_class_name(i) for i in range(n)]
     assert len(set(names)) == n and all(names)
     assert nb.numbat_kernel_class_name(n) == ""
