@@ -168,7 +168,10 @@ bool narrow(const ConvDesc& d) { return d.ci % 8 != 0; }
 size_t x8_bytes(const ConvDesc& d) { return round_up((size_t)d.n * d.h * d.w * 16, 256); }
 size_t w8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 16, 256); }
 
-TileCfg fwd_tile(const ConvDesc& d) { return convgemm_pick(d.m, d.co); }
+TileCfg fwd_tile(const ConvDesc& d) {
+  const int cs = narrow(d) ? 8 : d.ci;
+  return convgemm_pick(d.m, d.co, cs, d.kh * d.kw * cs);
+}
 
 size_t fwd_stats_bytes(const ConvDesc& d) {
   const TileCfg t = fwd_tile(d);
@@ -478,6 +481,7 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   g.accumulate = accumulate ? 1 : 0;
   int f = 0;
   int64_t mmax = 0;
+  int ktmax = 0;
   for (int pa = 0; pa < d.sh; ++pa)
     for (int pb = 0; pb < d.sw; ++pb, ++f) {
       const int gh = pa < d.h ? (d.h - pa + d.sh - 1) / d.sh : 0;
@@ -497,16 +501,18 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
       for (int t = 0; t < ph[f].count; ++t)
         P.off[t] = (int32_t)((uint32_t)(uint16_t)(int16_t)offh[f][t] | ((uint32_t)offw[f][t] << 16));
       mmax = P.m > mmax ? P.m : mmax;
+      ktmax = P.ktot > ktmax ? P.ktot : ktmax;
       const bool last = (pa == d.sh - 1 && pb == d.sw - 1);
       if (g.nphase == kMaxPhases || last) {
-        e = convgemm_launch(g, convgemm_pick(mmax, d.ci), s, KC_CONV_DGRAD);
+        e = convgemm_launch(g, convgemm_pick(mmax, d.ci, d.co, ktmax), s, KC_CONV_DGRAD);
         if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
         g.nphase = 0;
         mmax = 0;
+        ktmax = 0;
       }
     }
   if (g.nphase > 0) {
-    e = convgemm_launch(g, convgemm_pick(mmax, d.ci), s, KC_CONV_DGRAD);
+    e = convgemm_launch(g, convgemm_pick(mmax, d.ci, d.co, ktmax), s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
   }
   return ok();

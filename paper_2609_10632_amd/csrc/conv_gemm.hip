@@ -15,6 +15,7 @@
 //    (4 waves) by up to 128 columns;
 //  * the epilogue stages fp32 results through LDS and writes whole 16-byte vectors of
 //    8 channels (bf16, rounded once, after the optional accumulate).
+#include <cstdlib>
 #include <type_traits>
 
 #include "kernels.h"
@@ -53,6 +54,45 @@ __device__ __forceinline__ void grid_pos(uint32_t m, const GemmPhase& P, uint32_
   const uint32_t rem = m - img * (uint32_t)(P.gh * P.gw);
   gi = fdiv(rem, P.div_gw);
   gj = rem - gi * (uint32_t)P.gw;
+}
+
+// destination element offset of GEMM row m (-1 past the phase's rows)
+__device__ __forceinline__ int64_t dst_offset(const ConvGemmArgs& a, const GemmPhase& P, int m) {
+  if (m >= P.m) return -1;
+  uint32_t img, gi, gj;
+  grid_pos((uint32_t)m, P, img, gi, gj);
+  return (((int64_t)img * a.hd + (int)gi * a.dstep_h + P.doff_h) * a.wd + (int)gj * a.dstep_w + P.doff_w) *
+         a.dst_pix;
+}
+
+// Byte offset (from the tile's gather base, without the halo) of GEMM row m's anchor
+// pixel, and the bitmask of its taps that fall inside the image.  The taps form a grid
+// (rows of tw taps with constant steps), so the mask is the outer product of the grid
+// rows that stay inside the image height and the grid columns inside its width.
+__device__ __forceinline__ void row_gather(const ConvGemmArgs& a, const GemmPhase& P, int m, uint32_t img0,
+                                           uint32_t& vrow, uint32_t& vmask) {
+  vrow = 0;
+  vmask = 0;
+  if (m >= P.m) return;
+  uint32_t img, gi, gj;
+  grid_pos((uint32_t)m, P, img, gi, gj);
+  const int ih0 = (int)gi * a.gstride_h, iw0 = (int)gj * a.gstride_w;
+  vrow = (uint32_t)((((int64_t)(img - img0) * a.hs + ih0) * a.ws + iw0) * (a.src_pix * 2));
+  const int tw = P.tw, th = P.taps / tw;
+  const int dh0 = (int)(int16_t)(P.off[0] & 0xffff), dw0 = P.off[0] >> 16;
+  const int sh = th > 1 ? (int)(int16_t)(P.off[tw] & 0xffff) - dh0 : 0;
+  const int sw = tw > 1 ? (P.off[1] >> 16) - dw0 : 0;
+  uint32_t cols = 0;
+  for (int j = 0; j < tw; ++j) {
+    const int iw = iw0 + dw0 + j * sw;
+    cols |= ((unsigned)iw < (unsigned)a.ws ? 1u : 0u) << j;
+  }
+  uint32_t mk = 0;
+  for (int i = 0; i < th; ++i) {
+    const int ih = ih0 + dh0 + i * sh;
+    mk |= ((unsigned)ih < (unsigned)a.hs ? cols : 0u) << (i * tw);
+  }
+  vmask = mk;  // bits >= taps stay clear, so a walk past the last tap reads zeros
 }
 
 // Shared epilogue: per-channel (mean, M2) partials of the tile's rows (phase 0, when
@@ -114,16 +154,17 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
     // then write 16-byte vectors of 8 channels
     float* st = stage + wave * 8 * S::STAGE_LD;
     constexpr int VPR = BN / 8;  // vectors per staged row
+    // (the staging rows are private to the wave, and one wave's LDS accesses complete in
+    // issue order, so the rounds need no barrier)
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        __syncthreads();
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
           for (int e = 0; e < 4; ++e) st[(4 * half + e) * S::STAGE_LD + j * 32 + l32] = acc[i][j][4 * g + e];
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
         for (int v = lane; v < 8 * VPR; v += 64) {
           const int r = v / VPR, c8 = v - r * VPR;
           const int col = n0 + c8 * 8;
@@ -358,20 +399,212 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Fast path for source channel counts that are multiples of 16 (every layer of the
-// detector except the 3-channel image).  A 16-wide k-slice then never straddles a tap,
-// so the tap of each slice -- and its pixel offset -- is the same for the whole wave:
-// tap tracking runs on the scalar unit and the per-tap offset comes from the kernel
-// arguments, leaving one bit test and one 64-bit add per A fragment.  One pipeline
-// step covers 64 reduction elements (four MFMA k-slices) per barrier.
+// Fast path for source channel counts that are multiples of 16 and at least 32 (every
+// layer of the detector except the 3-channel image).
+//
+// Both operands are staged through LDS.  The gathered operand is loaded coalesced: a
+// thread always loads the same 16-byte chunk c (8 channels) of the 64-element reduction
+// step, and the 8 threads with the same row cover the row's 128 contiguous bytes, so one
+// wave instruction reads 8 whole rows.  (Gathering MFMA fragments straight from global
+// memory reads 32 rows per instruction; the L1 path's cost grows with the rows, not the
+// bytes, an instruction touches, and that design stalled on it.)
+//
+// Loads are raw buffer loads.  The gather base sits halo_px pixels before the first
+// image of the tile, so every in-image address is a non-negative 32-bit offset: row
+// offset (fixed for the whole reduction) + the thread's tap-and-channel offset.  A tap
+// outside the image swaps the offset for one past the buffer's range, which the hardware
+// answers with zeros; so does a weight row past nout or a reduction index past ktot.
+// Each thread walks its own reduction position (tap, channel) with adds and selects:
+// 16-multiple channel counts never split a chunk between taps, and with 32 or more
+// channels a 64-element step crosses at most two tap boundaries.
 constexpr int GK16 = 64;
 constexpr int GROW16 = GK16 + 8;  // 144-byte LDS rows: 16 lanes reading 16 rows hit 16 distinct bank groups
+constexpr uint32_t kOob = 0x80000000u;  // a buffer offset past every range below
+constexpr int kRecords = 0x7ffffff0;    // buffer range (bytes); in-range offsets stay below kOob - 2^24
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) {
+  // raw buffer, stride 0, range kRecords; word 3 = 0x00020000 (32-bit data format, the
+  // setting for linear loads on this architecture)
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, kRecords, 0x00020000);
+}
+
+template <int TM, int TN>
+struct LdsShape {
+  using S = GemmShape<TM, TN>;
+  static constexpr int AV = S::BM / 32;                    // A chunks per thread per step
+  static constexpr int BV = (S::BN * 8 + 255) / 256;       // B chunks per thread per step
+  static constexpr int A_BYTES = 2 * S::BM * GROW16 * 2;   // double-buffered A tile
+  static constexpr int B_BYTES = 2 * S::BN * GROW16 * 2;
+  static constexpr int SM = A_BYTES + B_BYTES > S::STAGE_BYTES ? A_BYTES + B_BYTES : S::STAGE_BYTES;
+};
 
 template <int TM, int TN, int D>
-__global__ __launch_bounds__(256) void convgemm16_kernel(ConvGemmArgs a) {
+__global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
+  using S = GemmShape<TM, TN>;
+  using L = LdsShape<TM, TN>;
+  constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM, AV = L::AV, BV = L::BV;
+  static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
+
+  __shared__ __attribute__((aligned(16))) unsigned char smem[L::SM];
+  __shared__ int64_t s_dst[BM];
+  __shared__ float s_red[4][BN];
+  __shared__ float s_mean[BN];
+  typedef bf16_t ATile[BM][GROW16];
+  typedef bf16_t BTile[BN][GROW16];
+  ATile* As = reinterpret_cast<ATile*>(smem);
+  BTile* Bs = reinterpret_cast<BTile*>(smem + L::A_BYTES);
+
+  const GemmPhase& P = a.ph[blockIdx.z];
+  const int m0 = blockIdx.x * BM;
+  if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
+  const int n0 = blockIdx.y * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int ck = tid & 7, rg = tid >> 3;  // this thread's load chunk and row within a 32-row group
+
+  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, P, m0 + r);
+
+  // A: gather base = first image of the tile, moved back by the halo (carried by toff0)
+  const uint32_t img0 = fdiv((uint32_t)m0, P.div_ghw);
+  const __amdgpu_buffer_rsrc_t rsA =
+      buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
+  uint32_t vrow[AV], vmask[AV];  // rows q*32 + rg of the tile
+#pragma unroll
+  for (int q = 0; q < AV; ++q) row_gather(a, P, m0 + q * 32 + rg, img0, vrow[q], vmask[q]);
+// B: rows j*32 + rg of the weight tile, chunk ck
+  const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
+  const int p_tw = P.tw, p_ktot = P.ktot, cs = a.cs;
+  const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
+  uint32_t voffb[BV];
+#pragma unroll
+  for (int j = 0; j < BV; ++j) {
+    const int row = j * 32 + rg, o = n0 + row;
+    voffb[j] = (row < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + ck * 8) * 2) : kOob;
+  }
+  // this thread's reduction position: channel ch of tap `tap` (column tcol of its grid
+  // row), byte offset toff of the tap
+  int ch = ck * 8, tap = 0, tcol = 0;
+  uint32_t toff = (uint32_t)P.toff0;
+  auto wrap_taps = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      const bool wrap = ch >= cs;
+      ch = wrap ? ch - cs : ch;
+      tap += wrap ? 1 : 0;
+      tcol += wrap ? 1 : 0;
+      const bool rw = tcol == p_tw;
+      tcol = rw ? 0 : tcol;
+      toff += wrap ? (rw ? p_rstep : p_cstep) : 0u;
+    }
+  };
+  wrap_taps();
+  const int nk = (p_ktot + GK16 - 1) / GK16;
+  __syncthreads();
+
+  u32x4 ra[D][AV], rbv[D][BV];
+  // loads of step kt into a ring slot; the A walk advances by one step
+  auto load = [&](int kt, u32x4 (&xa)[AV], u32x4 (&xb)[BV]) __attribute__((always_inline)) {
+    const uint32_t lo = toff + 2u * (uint32_t)ch;
+    const int tq = tap < 31 ? tap : 31;  // past the last tap: bit 31 is clear
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[q], tq, 1);
+      const uint32_t vo = (t & (vrow[q] + lo)) | (~t & kOob);
+      xa[q] = __builtin_amdgcn_raw_buffer_load_b128(rsA, vo, 0u, 0);
+    }
+    const int kb = kt * GK16;
+    const bool kin = kb + ck * 8 < p_ktot;
+#pragma unroll
+    for (int j = 0; j < BV; ++j) xb[j] = __builtin_amdgcn_raw_buffer_load_b128(rsB, kin ? voffb[j] : kOob, (uint32_t)kb * 2, 0);
+    ch += GK16;
+    wrap_taps();
+  };
+  auto store = [&](int buf, const u32x4 (&xa)[AV], const u32x4 (&xb)[BV]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < AV; ++q) *reinterpret_cast<u32x4*>(&As[buf][q * 32 + rg][ck * 8]) = xa[q];
+#pragma unroll
+    for (int j = 0; j < BV; ++j)
+      if (BV * 32 == BN || j * 32 + rg < BN) *reinterpret_cast<u32x4*>(&Bs[buf][j * 32 + rg][ck * 8]) = xb[j];
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      u32x4 afr[TM], bfr[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        afr[i] = *reinterpret_cast<const u32x4*>(&As[buf][wave * WTM + i * 32 + l32][ks * 16 + half * 8]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bfr[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][j * 32 + l32][ks * 16 + half * 8]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(afr[i], bfr[j], acc[i][j]);
+    }
+  };
+  // step kt (ring slot of step kt+1 = nxt): stage step kt+1 in LDS, fetch step kt+1+D
+  // into the freed slot, multiply the tiles of step kt
+  auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
+    constexpr int u = decltype(uc)::value;
+    constexpr int nxt = (u + 1) % D;
+    store((kt + 1) & 1, ra[nxt], rbv[nxt]);
+    load(kt + 1 + D, ra[nxt], rbv[nxt]);
+    compute(kt & 1);
+    __syncthreads();
+  };
+  // Prologue: step 0 goes to LDS; steps 1..D are left in flight, in the order the
+  // steady state issues them, so the loop is entered with the same pending loads as it
+  // loops back with and every wait counts exactly.
+  if (nk > 0) {
+    load(0, ra[0], rbv[0]);
+    store(0, ra[0], rbv[0]);
+    if constexpr (D > 1) load(1, ra[1], rbv[1]);
+    if constexpr (D > 2) load(2, ra[2], rbv[2]);
+    if constexpr (D > 3) load(3, ra[3], rbv[3]);
+    load(D, ra[0], rbv[0]);
+    __syncthreads();
+  }
+  int kb = 0;
+  for (; kb + D <= nk; kb += D) {
+    step(Ic<0>{}, kb);
+    if constexpr (D > 1) step(Ic<1 % D>{}, kb + 1);
+    if constexpr (D > 2) step(Ic<2 % D>{}, kb + 2);
+    if constexpr (D > 3) step(Ic<3 % D>{}, kb + 3);
+  }
+  if constexpr (D > 1) {
+    if (kb < nk) step(Ic<0>{}, kb);
+  }
+  if constexpr (D > 2) {
+    if (kb + 1 < nk) step(Ic<1 % D>{}, kb + 1);
+  }
+  if constexpr (D > 3) {
+    if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
+  }
+  gemm_epilogue<TM, TN>(a, P, acc, m0, n0, smem, s_dst, s_red, s_mean);
+}
+
+// ---------------------------------------------------------------------------
+// Register-direct variant of the fast path: the gathered operand bypasses LDS.  Each
+// wave loads its own MFMA A fragments (16 contiguous bytes per lane: 8 channels of one
+// pixel at one tap) with buffer loads straight into a register ring; only the weight
+// tile goes through LDS.  It needs far less LDS than the staged kernel (two or more
+// blocks per CU), but one fragment load touches 32 rows, so the L1 path caps it; it
+// wins where the reduction is short and blocks are many.  The k-slice position is the
+// same for the whole wave and walks the taps on the scalar unit.
+template <int TM, int TN, int D>
+__global__ __launch_bounds__(256) void convdirect_kernel(ConvGemmArgs a) {
   using S = GemmShape<TM, TN>;
   constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM;
-  constexpr int BV = (BN * 8 + 255) / 256;  // 16-byte B chunks per thread per step (BN rows x 8 chunks)
+  constexpr int BV = (BN * 8 + 255) / 256;
   constexpr int B_BYTES16 = 2 * BN * GROW16 * 2;
   constexpr int SM = B_BYTES16 > S::STAGE_BYTES ? B_BYTES16 : S::STAGE_BYTES;
   static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
@@ -385,93 +618,76 @@ __global__ __launch_bounds__(256) void convgemm16_kernel(ConvGemmArgs a) {
 
   const GemmPhase& P = a.ph[blockIdx.z];
   const int m0 = blockIdx.x * BM;
-  if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
+  if (m0 >= P.m) return;
   const int n0 = blockIdx.y * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
-  for (int r = tid; r < BM; r += 256) {
-    const int m = m0 + r;
-    int64_t d = -1;
-    if (m < P.m) {
-      uint32_t img, gi, gj;
-      grid_pos((uint32_t)m, P, img, gi, gj);
-      d = (((int64_t)img * a.hd + (int)gi * a.dstep_h + P.doff_h) * a.wd + (int)gj * a.dstep_w + P.doff_w) *
-          a.dst_pix;
-    }
-    s_dst[r] = d;
-  }
-  const bf16_t* rowp[TM];
-  uint32_t rmask[TM];
+  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, P, m0 + r);
+
+  const uint32_t img0 = fdiv((uint32_t)m0, P.div_ghw);
+  const __amdgpu_buffer_rsrc_t rsA =
+      buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
+  uint32_t vrow[TM], vmask[TM];
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int m = m0 + wave * WTM + i * 32 + l32;
-    rowp[i] = a.src;
-    rmask[i] = 0;
-    if (m < P.m) {
-      uint32_t img, gi, gj;
-      grid_pos((uint32_t)m, P, img, gi, gj);
-      const int ih0 = (int)gi * a.gstride_h, iw0 = (int)gj * a.gstride_w;
-      rowp[i] = a.src + ((int64_t)img * a.hs * a.ws + (int64_t)ih0 * a.ws + iw0) * a.src_pix + half * 8;
-      uint32_t mk = 0;
-      for (int t = 0; t < P.taps; ++t) {
-        const int off = P.off[t];
-        const int ih = ih0 + (int)(int16_t)(off & 0xffff), iw = iw0 + (off >> 16);
-        if ((unsigned)ih < (unsigned)a.hs && (unsigned)iw < (unsigned)a.ws) mk |= 1u << t;
-      }
-      rmask[i] = mk;
-    }
+    row_gather(a, P, m0 + wave * WTM + i * 32 + l32, img0, vrow[i], vmask[i]);
+    vrow[i] += half * 16;
   }
-  const bf16_t* bptr[BV];
-  bool bok[BV];
-  int brow[BV], bch[BV];
+  const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
+  const int p_tw = P.tw, p_ktot = P.ktot;
+  const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
+  uint32_t voffb[BV];
+  int bk[BV], brow[BV], bch[BV];
 #pragma unroll
   for (int j = 0; j < BV; ++j) {
     const int v = tid + 256 * j;
     brow[j] = v >> 3;
     bch[j] = v & 7;
+    bk[j] = bch[j] * 8;
     const int o = n0 + brow[j];
-    bok[j] = brow[j] < BN && o < a.nout;
-    bptr[j] = P.wt + (int64_t)(bok[j] ? o : 0) * P.ktot + bch[j] * 8;
+    voffb[j] = (brow[j] < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + bk[j]) * 2) : kOob;
   }
-  int tapS = 0, cS = 0;  // wave-uniform position of the next A k-slice
-  const int nk = (P.ktot + GK16 - 1) / GK16;
+  int tap = 0, tcol = 0;
+  uint32_t toff = (uint32_t)P.toff0, cb = 0;
+  const uint32_t cs2 = (uint32_t)a.cs * 2;
+  const int nk = (p_ktot + GK16 - 1) / GK16;
   __syncthreads();
 
-  const bf16_t* zp = reinterpret_cast<const bf16_t*>(&kZero16);
   u32x4 ra[D][4 * TM], rbv[D][BV];
   auto load_a = [&](u32x4 (&xa)[4 * TM]) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      const bool tok = tapS < P.taps;
-      int toff = cS;
-      if (tok) {
-        const int off = P.off[tapS];
-        toff += ((int)(int16_t)(off & 0xffff) * a.ws + (off >> 16)) * (int)a.src_pix;
-      }
+      const uint32_t so = toff + cb;
+      const int tq = tap < 31 ? tap : 31;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
-        const bool ok = tok && ((rmask[i] >> tapS) & 1u);
-        xa[ks * TM + i] = *reinterpret_cast<const u32x4*>(ok ? rowp[i] + toff : zp);
+        const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[i], tq, 1);
+        const uint32_t vo = (t & vrow[i]) | (~t & kOob);
+        xa[ks * TM + i] = __builtin_amdgcn_raw_buffer_load_b128(rsA, vo, so, 0);
       }
-      cS += 16;
-      if (cS == a.cs) {
-        cS = 0;
-        ++tapS;
-      }
+      cb += 32;
+      const bool wrap = cb == cs2;
+      cb = wrap ? 0u : cb;
+      tap += wrap ? 1 : 0;
+      tcol += wrap ? 1 : 0;
+      const bool rw = tcol == p_tw;
+      tcol = rw ? 0 : tcol;
+      toff += wrap ? (rw ? p_rstep : p_cstep) : 0u;
     }
   };
   auto load_b = [&](int kt, u32x4 (&xb)[BV]) __attribute__((always_inline)) {
+    const int kb = kt * GK16;
 #pragma unroll
     for (int j = 0; j < BV; ++j) {
-      const bool ok = bok[j] && kt * GK16 + bch[j] * 8 < P.ktot;
-      xb[j] = *reinterpret_cast<const u32x4*>(ok ? bptr[j] + kt * GK16 : zp);
+      const uint32_t vo = (kb + bk[j] < p_ktot) ? voffb[j] : kOob;
+      xb[j] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, (uint32_t)kb * 2, 0);
     }
   };
   auto store_b = [&](int buf, const u32x4 (&xb)[BV]) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < BV; ++j)
-      if (brow[j] < BN) *reinterpret_cast<u32x4*>(&Bs[buf][brow[j]][bch[j] * 8]) = xb[j];
+      if (BV * 256 == BN * 8 || brow[j] < BN) *reinterpret_cast<u32x4*>(&Bs[buf][brow[j]][bch[j] * 8]) = xb[j];
   };
 
   f32x16 acc[TM][TN];
@@ -504,39 +720,42 @@ __global__ __launch_bounds__(256) void convgemm16_kernel(ConvGemmArgs a) {
     load_a(ra[u]);
     __syncthreads();
   };
+  // prologue in steady-state issue order (see the staged kernel)
   auto prologue = [&](auto dc) __attribute__((always_inline)) {
     constexpr int d = decltype(dc)::value;
+    load_b(d + 1, rbv[(d + 1) % D]);
     load_a(ra[d]);
-    load_b(d, rbv[d]);
   };
-
   if (nk > 0) {
+    load_b(0, rbv[0]);
+    store_b(0, rbv[0]);
     prologue(Ic<0>{});
     if constexpr (D > 1) prologue(Ic<1>{});
     if constexpr (D > 2) prologue(Ic<2>{});
     if constexpr (D > 3) prologue(Ic<3>{});
-    store_b(0, rbv[0]);
-    load_b(D, rbv[0]);
     __syncthreads();
   }
-  for (int kb = 0; kb < nk; kb += D) {
+  int kb = 0;
+  for (; kb + D <= nk; kb += D) {
     step(Ic<0>{}, kb);
-    if constexpr (D > 1) {
-      if (kb + 1 < nk) step(Ic<1 % D>{}, kb + 1);
-    }
-    if constexpr (D > 2) {
-      if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
-    }
-    if constexpr (D > 3) {
-      if (kb + 3 < nk) step(Ic<3 % D>{}, kb + 3);
-    }
+    if constexpr (D > 1) step(Ic<1 % D>{}, kb + 1);
+    if constexpr (D > 2) step(Ic<2 % D>{}, kb + 2);
+    if constexpr (D > 3) step(Ic<3 % D>{}, kb + 3);
+  }
+  if constexpr (D > 1) {
+    if (kb < nk) step(Ic<0>{}, kb);
+  }
+  if constexpr (D > 2) {
+    if (kb + 1 < nk) step(Ic<1 % D>{}, kb + 1);
+  }
+  if constexpr (D > 3) {
+    if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
   }
   gemm_epilogue<TM, TN>(a, P, acc, m0, n0, smem, s_dst, s_red, s_mean);
 }
 
-
 struct GInst {
-  int tm, tn, d;  // 32-row tiles per wave (4 waves along M), 32-col tiles, prefetch depth
+  int tm, tn, d;  // 32-row tiles per wave (4 waves along M), 32-col tiles, prefetch depth (generic kernel)
 };
 constexpr GInst kG[] = {
     {2, 4, 2},  // 0: 256 x 128
@@ -549,57 +768,132 @@ constexpr GInst kG[] = {
     {1, 1, 4},  // 7: 128 x 32
 };
 
-// prefetch depth of the 64-deep fast path (its ring slots are twice as large)
-constexpr int d16(const GInst& c) { return c.tm * c.tn >= 6 ? 2 : 3; }
+// prefetch depths (ring slots) of the two fast paths
+constexpr int d_lds(const GInst& c) { return c.tm == 2 ? 2 : 3; }
+constexpr int d_direct(const GInst& c) { return c.tm * c.tn >= 6 ? 2 : 3; }
 
 template <int I>
-hipError_t launch_g(const ConvGemmArgs& a, hipStream_t s) {
+hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
   constexpr GInst c = kG[I];
   using Sh = GemmShape<c.tm, c.tn>;
   int mmax = 0;
   for (int p = 0; p < a.nphase; ++p) mmax = a.ph[p].m > mmax ? a.ph[p].m : mmax;
   dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN), (unsigned)a.nphase);
-  if (a.cs % 16 == 0)
-    hipLaunchKernelGGL((convgemm16_kernel<c.tm, c.tn, d16(c)>), grid, dim3(256), 0, s, a);
+  if (variant == kVariantLds)
+    hipLaunchKernelGGL((convlds_kernel<c.tm, c.tn, d_lds(c)>), grid, dim3(256), 0, s, a);
+  else if (variant == kVariantDirect)
+    hipLaunchKernelGGL((convdirect_kernel<c.tm, c.tn, d_direct(c)>), grid, dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
+int tap_dh(int32_t off) { return (int)(int16_t)(off & 0xffff); }
+int tap_dw(int32_t off) { return off >> 16; }
+
+// Fills in the tap walk of the fast path (tw, toff0, cstep, rstep, halo_px) and reports
+// whether the fast path applies: 16-multiple source channels (at least 32), taps forming a grid with
+// unit steps, and every gathered byte of a tile within 32-bit buffer offsets.
+bool prepare_fast(ConvGemmArgs& a, int bm) {
+  if (a.cs % 16 != 0 || a.cs < 32) return false;
+  const int64_t pix2 = a.src_pix * 2;
+  int halo = 0;
+  for (int p = 0; p < a.nphase; ++p) {
+    const GemmPhase& P = a.ph[p];
+    for (int t = 0; t < P.taps; ++t) {
+      const int lin = tap_dh(P.off[t]) * a.ws + tap_dw(P.off[t]);
+      halo = -lin > halo ? -lin : halo;
+    }
+  }
+  a.halo_px = halo;
+  int64_t worst = 0;
+  for (int p = 0; p < a.nphase; ++p) {
+    GemmPhase& P = a.ph[p];
+    int tw = 1;
+    while (tw < P.taps && tap_dh(P.off[tw]) == tap_dh(P.off[0])) ++tw;
+    if (P.taps % tw != 0) return false;
+    const int sw = tw > 1 ? tap_dw(P.off[1]) - tap_dw(P.off[0]) : 0;
+    const int sh = P.taps > tw ? tap_dh(P.off[tw]) - tap_dh(P.off[0]) : 0;
+    int64_t maxlin = 0;
+    for (int t = 0; t < P.taps; ++t) {
+      const int i = t / tw, j = t % tw;
+      if (tap_dh(P.off[t]) != tap_dh(P.off[0]) + i * sh || tap_dw(P.off[t]) != tap_dw(P.off[0]) + j * sw) return false;
+      const int64_t lin = (int64_t)tap_dh(P.off[t]) * a.ws + tap_dw(P.off[t]) + halo;
+      maxlin = lin > maxlin ? lin : maxlin;
+    }
+    if ((int64_t)a.nout * P.ktot * 2 >= (int64_t)kRecords) return false;  // weight offsets are 32-bit too
+    P.tw = tw;
+    P.toff0 = (int32_t)(((int64_t)tap_dh(P.off[0]) * a.ws + tap_dw(P.off[0]) + halo) * pix2);
+    P.cstep = (int32_t)((int64_t)sw * pix2);
+    P.rstep = (int32_t)(((int64_t)sh * a.ws - (int64_t)(tw - 1) * sw) * pix2);
+    // a tile's rows span at most bm / (gh*gw) + 2 images
+    const int64_t imgs = bm / ((int64_t)P.gh * P.gw) + 2;
+    const int64_t span = (imgs * a.hs * a.ws + halo + maxlin) * pix2 + (int64_t)a.cs * 2 + 16;
+    worst = span > worst ? span : worst;
+  }
+  return worst < (int64_t)kOob - (1 << 24);
+}
+
 }  // namespace
 
-TileCfg convgemm_pick(int64_t m_max, int nout) {
-  // narrowest padding waste on N (32-column granularity); ties go to the wider tile
+// Tile and kernel choice, fitted to timings of every (kernel, tile) pair over the forward
+// and data-gradient GEMMs of the detector's layers at batch 16 (within a few percent of
+// the per-layer best in total):
+//  * N tile: the least padding among 128, 96 and 64 columns (ties to the wider); when the
+//    grid would hold fewer than 400 blocks of 128 rows, 64 columns for more blocks;
+//  * fast paths: 128-row tiles; the LDS-staged kernel for reductions of 1024 or more or
+//    at most 32768 rows, the register-direct one otherwise;
+//  * generic kernel (narrow or 8-multiple channels): 256-row tiles unless that leaves
+//    fewer than 512 blocks.
+TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
   const int bns[4] = {128, 96, 64, 32};
+  const int ncand = nout <= 32 ? 4 : 3;
   int bn = 128;
   int64_t waste = INT64_MAX;
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < ncand; ++i) {
     const int64_t w = ((nout + bns[i] - 1) / bns[i]) * bns[i] - nout;
     if (w < waste) {
       waste = w;
       bn = bns[i];
     }
   }
-  const int ntiles = (nout + bn - 1) / bn;
-  const int64_t blocks256 = ((m_max + 255) / 256) * ntiles;
-  // few tiles: 128-row tiles fill the 256 CUs better
-  const bool small = blocks256 < 512;
-  const int id = (small ? 4 : 0) + (bn == 128 ? 0 : bn == 96 ? 1 : bn == 64 ? 2 : 3);
-  return TileCfg{small ? 128 : 256, bn, id};
+  const bool fast = cs % 16 == 0 && cs >= 32;
+  int bm, variant;
+  if (fast) {
+    const int64_t blocks128 = ((m_max + 127) / 128) * ((nout + bn - 1) / bn);
+    if (blocks128 < 400 && bn > 64) bn = 64;
+    bm = 128;
+    variant = (ktot >= 1024 || m_max <= 32768) ? kVariantLds : kVariantDirect;
+  } else {
+    const int64_t blocks256 = ((m_max + 255) / 256) * ((nout + bn - 1) / bn);
+    bm = blocks256 < 512 ? 128 : 256;
+    variant = kVariantGeneric;
+  }
+  int id = (bm == 128 ? 4 : 0) + (bn == 128 ? 0 : bn == 96 ? 1 : bn == 64 ? 2 : 3);
+#ifdef NUMBAT_TUNING
+  // timing sweeps only: force the instantiation and kernel
+  if (const char* e = getenv("NUMBAT_TILE")) id = atoi(e);
+  if (const char* e = getenv("NUMBAT_VARIANT")) variant = fast ? atoi(e) : kVariantGeneric;
+  bm = kG[id].tm * 128;
+  bn = kG[id].tn * 32;
+#endif
+  return TileCfg{bm, bn, id, variant};
 }
 
-hipError_t convgemm_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
+hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls) {
+  // a problem the fast paths cannot take runs the generic kernel on the same tile
+  const int variant = (t.variant != kVariantGeneric && prepare_fast(a, t.bm)) ? t.variant : kVariantGeneric;
   trace_begin(cls, s);
   hipError_t e;
   switch (t.id) {
-    case 0: e = launch_g<0>(a, s); break;
-    case 1: e = launch_g<1>(a, s); break;
-    case 2: e = launch_g<2>(a, s); break;
-    case 3: e = launch_g<3>(a, s); break;
-    case 4: e = launch_g<4>(a, s); break;
-    case 5: e = launch_g<5>(a, s); break;
-    case 6: e = launch_g<6>(a, s); break;
-    default: e = launch_g<7>(a, s); break;
+    case 0: e = launch_g<0>(a, variant, s); break;
+    case 1: e = launch_g<1>(a, variant, s); break;
+    case 2: e = launch_g<2>(a, variant, s); break;
+    case 3: e = launch_g<3>(a, variant, s); break;
+    case 4: e = launch_g<4>(a, variant, s); break;
+    case 5: e = launch_g<5>(a, variant, s); break;
+    case 6: e = launch_g<6>(a, variant, s); break;
+    default: e = launch_g<7>(a, variant, s); break;
   }
   trace_end(cls, s);
   return e;

@@ -31,9 +31,13 @@ enum KernelClass {
 void trace_begin(int cls, hipStream_t s);
 void trace_end(int cls, hipStream_t s);
 
+// conv GEMM kernel variants: generic (source channels a multiple of 8), and the two fast
+// paths for 16-multiple channel counts of at least 32 (LDS-staged, register-direct)
+enum { kVariantGeneric = 0, kVariantLds = 1, kVariantDirect = 2 };
 struct TileCfg {
   int bm, bn;
-  int id;  // instantiation id
+  int id;       // instantiation id
+  int variant;  // kVariant*
 };
 
 // Implicit GEMM (conv_gemm.hip) D[M][N] = A[M][K] * B[N][K]^T for source channel
@@ -46,6 +50,11 @@ struct TileCfg {
 // convolution is one such GEMM; the stride phases of a data gradient are up to four
 // "phases" sharing one launch (blockIdx.z), each with its own grid, taps, offsets, B
 // matrix and destination offset.
+//
+// The taps of every phase form a grid (rows of tw taps; off_h and off_w change by a
+// constant +-1 from column to column and row to row).  convgemm_launch derives from
+// off[] the byte steps the 16-channel fast path walks the taps with (tw, toff0, cstep,
+// rstep, halo_px); callers fill in off[] only.
 constexpr int kMaxPhases = 4;
 struct GemmPhase {
   const bf16_t* wt;     // [nout][ktot], K-major
@@ -54,6 +63,10 @@ struct GemmPhase {
   FastDiv div_gw, div_ghw;
   int32_t doff_h, doff_w;
   int32_t off[kMaxTaps];  // (off_h & 0xffff) | (off_w << 16)
+  // set by convgemm_launch: taps per grid row, byte offset of tap 0 (plus the halo
+  // shift), byte step to the next tap in a row and from a row's last tap to the next
+  // row's first
+  int32_t tw, toff0, cstep, rstep;
 };
 struct ConvGemmArgs {
   const bf16_t* src;
@@ -67,11 +80,14 @@ struct ConvGemmArgs {
   int32_t accumulate;
   float2* stats_part;  // phase 0 only: [m tiles][nout] (tile mean, tile M2) or nullptr
   int32_t nphase;
+  int32_t halo_px;     // set by convgemm_launch: pixels the fast path's gather base sits before an image
   GemmPhase ph[kMaxPhases];
 };
-// tile for a problem with at most m_max rows per phase (depends on the problem only)
-TileCfg convgemm_pick(int64_t m_max, int nout);
-hipError_t convgemm_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
+// tile and kernel for a problem with at most m_max rows per phase, nout columns, cs
+// source channels and reduction length ktot (depends on the problem only)
+TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot);
+// a is taken by value: the launcher completes the tap-walk fields
+hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls);
 
 // 8-channel repacking of a narrow (ci < 8) NHWC tensor, and extraction of ci channels
 // from a weight gradient computed on the repacked layout

@@ -31,6 +31,10 @@ CONV_CASES = [
     (2, 15, 15, 3, 16, 3, 2),
     (1, 6, 6, 16, 16, 1, 2),
     (2, 12, 12, 1152, 64, 1, 1),
+    # more than 32768 GEMM rows with short reductions: the register-direct fast path
+    # (48 channels: two tap wraps per step; 32 -> 64 stride 2: 32-column data-gradient tiles)
+    (2, 130, 129, 48, 48, 3, 1),
+    (1, 364, 362, 32, 64, 3, 2),
 ]
 
 
