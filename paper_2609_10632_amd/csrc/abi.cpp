@@ -527,6 +527,14 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   if ((!narrow(d) && !aligned16(x)) || !aligned16(dy)) return fail(NUMBAT_ERR_ALIGN, "x and dy must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(x) & 1u) || (reinterpret_cast<uintptr_t>(dw) & 3u))
     return fail(NUMBAT_ERR_ALIGN, "x must be 2-byte and dw 4-byte aligned");
+  {
+    // the gather of one 64-pixel step addresses its images with 32-bit offsets
+    const int64_t xp = narrow(d) ? 8 : d.x_pix;
+    const int64_t imgs = 64 / ((int64_t)d.ho * d.wo) + 2;
+    if (imgs * d.h * d.w * xp * 2 >= (1ll << 31) - (1ll << 24))
+      return fail(NUMBAT_ERR_UNSUPPORTED, "input images too large for the weight-gradient gather (%lld bytes each)",
+                  (long long)(d.h * (int64_t)d.w * xp * 2));
+  }
   int splits = 1;
   int64_t rps = 0;
   const size_t need = bwd_weight_ws(d, &splits, &rps);

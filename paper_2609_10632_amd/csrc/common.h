@@ -92,4 +92,16 @@ __device__ __forceinline__ f32x16 mfma32x32x16(const u32x4& a, const u32x4& b, f
 
 __device__ __forceinline__ float sigmoidf_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
+// Workgroups are dealt round-robin to the 8 XCDs (linear id L runs on XCD L % 8), and
+// each XCD has its own L2.  Tiles that read the same data should share an XCD, so a
+// kernel whose consecutive logical tiles share data maps its linear id to the logical
+// tile xcd_remap(L, total): XCD x works through the x-th contiguous chunk of logical
+// tiles in order.  A bijection on [0, total).
+constexpr uint32_t kXcds = 8;
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t L, uint32_t total) {
+  const uint32_t q = total / kXcds, r = total % kXcds;
+  const uint32_t x = L % kXcds, i = L / kXcds;
+  return x < r ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+}
+
 }  // namespace numbat

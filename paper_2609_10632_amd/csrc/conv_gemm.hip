@@ -56,6 +56,19 @@ __device__ __forceinline__ void grid_pos(uint32_t m, const GemmPhase& P, uint32_
   gj = rem - gi * (uint32_t)P.gw;
 }
 
+// logical tile of this block.  With the XCD-aware order: n tile fastest, then m tile,
+// then phase, so the blocks sharing rows of the gathered operand (and halo rows of
+// neighbouring tiles) share an XCD; otherwise the launch order (m tile fastest).
+struct TileId {
+  int mt, nt, ph;
+};
+__device__ __forceinline__ TileId tile_id(bool remap) {
+  if (!remap) return TileId{(int)blockIdx.x, (int)blockIdx.y, (int)blockIdx.z};
+  const uint32_t gx = gridDim.x, gy = gridDim.y;  // m tiles, n tiles
+  const uint32_t lg = xcd_remap(blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z), gx * gy * gridDim.z);
+  return TileId{(int)((lg / gy) % gx), (int)(lg % gy), (int)(lg / (gx * gy))};
+}
+
 // destination element offset of GEMM row m (-1 past the phase's rows)
 __device__ __forceinline__ int64_t dst_offset(const ConvGemmArgs& a, const GemmPhase& P, int m) {
   if (m >= P.m) return -1;
@@ -100,9 +113,9 @@ __device__ __forceinline__ void row_gather(const ConvGemmArgs& a, const GemmPhas
 // vectors of 8 channels.  Accumulator register r of a lane sits on wave row
 // 8*(r/4) + 4*(lane/32) + (r%4) of its 32-row block, column lane%32 of its 32-column block.
 template <int TM, int TN>
-__device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmPhase& P, f32x16 (&acc)[TM][TN],
-                                              int m0, int n0, unsigned char* smem, const int64_t* s_dst,
-                                              float (*s_red)[TN * 32], float* s_mean) {
+__device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmPhase& P, const TileId& T,
+                                              f32x16 (&acc)[TM][TN], int m0, int n0, unsigned char* smem,
+                                              const int64_t* s_dst, float (*s_red)[TN * 32], float* s_mean) {
   using S = GemmShape<TM, TN>;
   constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -110,7 +123,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
   float* stage = reinterpret_cast<float*>(smem);
   __syncthreads();  // the main loop's last LDS reads are done before staging reuses LDS
   // ---- per-channel (mean, M2) of this tile's rows from the fp32 accumulators (phase 0)
-  if (a.stats_part != nullptr && blockIdx.z == 0) {
+  if (a.stats_part != nullptr && T.ph == 0) {
     const int left = P.m - m0;
     const int count = left < BM ? left : BM;
 #pragma unroll
@@ -144,7 +157,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
     __syncthreads();
     if (tid < BN && n0 + tid < a.nout) {
       const float q = (s_red[0][tid] + s_red[1][tid]) + (s_red[2][tid] + s_red[3][tid]);
-      a.stats_part[(int64_t)blockIdx.x * a.nout + n0 + tid] = make_float2(s_mean[tid], q);
+      a.stats_part[(int64_t)T.mt * a.nout + n0 + tid] = make_float2(s_mean[tid], q);
     }
   }
 
@@ -226,10 +239,11 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
   typedef bf16_t BTile[BN][GROW];
   BTile* Bs = reinterpret_cast<BTile*>(smem);
 
-  const GemmPhase& P = a.ph[blockIdx.z];
-  const int m0 = blockIdx.x * BM;
+  const TileId T = tile_id(a.remap != 0);
+  const GemmPhase& P = a.ph[T.ph];
+  const int m0 = T.mt * BM;
   if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
-  const int n0 = blockIdx.y * BN;
+  const int n0 = T.nt * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;  // MFMA row / column, k group
 
@@ -395,7 +409,7 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
     }
   }
 
-  gemm_epilogue<TM, TN>(a, P, acc, m0, n0, smem, s_dst, s_red, s_mean);
+  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
 }
 
 // ---------------------------------------------------------------------------
@@ -454,10 +468,11 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
   ATile* As = reinterpret_cast<ATile*>(smem);
   BTile* Bs = reinterpret_cast<BTile*>(smem + L::A_BYTES);
 
-  const GemmPhase& P = a.ph[blockIdx.z];
-  const int m0 = blockIdx.x * BM;
+  const TileId T = tile_id(a.remap != 0);
+  const GemmPhase& P = a.ph[T.ph];
+  const int m0 = T.mt * BM;
   if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
-  const int n0 = blockIdx.y * BN;
+  const int n0 = T.nt * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
   const int ck = tid & 7, rg = tid >> 3;  // this thread's load chunk and row within a 32-row group
@@ -589,7 +604,7 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
   if constexpr (D > 3) {
     if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
   }
-  gemm_epilogue<TM, TN>(a, P, acc, m0, n0, smem, s_dst, s_red, s_mean);
+  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
 }
 
 // ---------------------------------------------------------------------------
@@ -616,10 +631,11 @@ __global__ __launch_bounds__(256) void convdirect_kernel(ConvGemmArgs a) {
   typedef bf16_t BTile[BN][GROW16];
   BTile* Bs = reinterpret_cast<BTile*>(smem);
 
-  const GemmPhase& P = a.ph[blockIdx.z];
-  const int m0 = blockIdx.x * BM;
+  const TileId T = tile_id(a.remap != 0);
+  const GemmPhase& P = a.ph[T.ph];
+  const int m0 = T.mt * BM;
   if (m0 >= P.m) return;
-  const int n0 = blockIdx.y * BN;
+  const int n0 = T.nt * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
@@ -751,7 +767,7 @@ __global__ __launch_bounds__(256) void convdirect_kernel(ConvGemmArgs a) {
   if constexpr (D > 3) {
     if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
   }
-  gemm_epilogue<TM, TN>(a, P, acc, m0, n0, smem, s_dst, s_red, s_mean);
+  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
 }
 
 struct GInst {
@@ -883,6 +899,10 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
 hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls) {
   // a problem the fast paths cannot take runs the generic kernel on the same tile
   const int variant = (t.variant != kVariantGeneric && prepare_fast(a, t.bm)) ? t.variant : kVariantGeneric;
+  a.remap = 0;
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_REMAP_CONV")) a.remap = atoi(e);
+#endif
   trace_begin(cls, s);
   hipError_t e;
   switch (t.id) {

@@ -3,19 +3,36 @@
 //
 // In NHWC both operands are contiguous along o / k and strided along the reduction
 // dimension m, while an MFMA lane needs 8 consecutive reduction elements.  Each thread
-// therefore loads an 8-pixel x 8-channel block (eight 16-byte loads), transposes it in
-// registers with byte permutes, and writes eight 16-byte rows of [channel][pixel] into
-// LDS.  The reduction over m is split into fixed contiguous ranges, one per
-// blockIdx.z, whose fp32 partial sums are added afterwards in split order, so the
-// result does not depend on scheduling.
+// therefore loads an 8-pixel x 8-channel unit (eight 16-byte buffer loads, 8 channels of
+// 8 consecutive pixels), transposes it in registers with byte permutes and writes eight
+// 16-byte rows of [channel][pixel] into LDS; the MFMAs (32x32x16) read both operands
+// from there.  Loads run a register ring several steps ahead of the multiply.  Buffer
+// loads answer padding taps, pixels past the split and channels past the tile with
+// zeros (offsets past the buffer range), so every step issues the same loads.  The
+// reduction over m is split into fixed contiguous ranges, one per blockIdx.z, whose fp32
+// partial sums are added afterwards in split order, so the result does not depend on
+// scheduling.
+#include <cstdlib>
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace numbat {
 
 namespace {
 
+template <int V>
+using Ic = std::integral_constant<int, V>;
+
 constexpr int BR = 64;           // reduction pixels per step
-constexpr int LROW = BR + 8;     // bf16 per LDS row (16 B pad)
+constexpr int LROW = BR + 8;     // bf16 per LDS row (144 bytes: conflict-free fragment reads)
+constexpr int BNK = 128;         // k columns per tile
+constexpr uint32_t kOobW = 0x80000000u;
+constexpr int kRecW = 0x7ffffff0;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t wrsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, kRecW, 0x00020000);
+}
 
 __device__ __forceinline__ uint32_t lo_pair(uint32_t p0, uint32_t p1) {
   return __builtin_amdgcn_perm(p1, p0, 0x05040100u);  // (p0.lo16, p1.lo16)
@@ -23,190 +40,222 @@ __device__ __forceinline__ uint32_t lo_pair(uint32_t p0, uint32_t p1) {
 __device__ __forceinline__ uint32_t hi_pair(uint32_t p0, uint32_t p1) {
   return __builtin_amdgcn_perm(p1, p0, 0x07060302u);  // (p0.hi16, p1.hi16)
 }
-__device__ __forceinline__ uint32_t word(const uint4& v, int i) {
-  return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
-}
 
 // in: P[j] = 8 channels of pixel j.  out: Q[ch] = 8 pixels of channel ch.
-__device__ __forceinline__ void transpose8x8(const uint4 P[8], uint4 Q[8]) {
+__device__ __forceinline__ void transpose8x8(const u32x4 (&P)[8], u32x4 (&Q)[8]) {
 #pragma unroll
   for (int ch = 0; ch < 8; ++ch) {
     const int wi = ch >> 1;
-    uint32_t q[4];
+    u32x4 q;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const uint32_t a = word(P[2 * k], wi), b = word(P[2 * k + 1], wi);
-      q[k] = (ch & 1) ? hi_pair(a, b) : lo_pair(a, b);
+      const uint32_t x0 = P[2 * k][wi], x1 = P[2 * k + 1][wi];
+      q[k] = (ch & 1) ? hi_pair(x0, x1) : lo_pair(x0, x1);
     }
-    Q[ch] = make_uint4(q[0], q[1], q[2], q[3]);
+    Q[ch] = q;
   }
 }
 
-template <int TM, int TN>
+// Tile BMO = 64*TMO output channels x BNK = 128 k columns; 2 x 2 waves of
+// (32*TMO) x 64.  Threads [0, BMO) load dy units, [BMO, BMO + 128) x units.
+template <int TMO, int D>
 __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo, FastDiv div_howo) {
-  constexpr int BMO = 2 * TM * 16;  // output channels per tile
-  constexpr int BNK = 2 * TN * 16;  // k columns per tile
-  constexpr int UDY = (BMO / 8) * (BR / 8);
-  constexpr int UX = (BNK / 8) * (BR / 8);
-  constexpr int UNITS = UDY + UX;
-  constexpr int UPT = (UNITS + 255) / 256;  // units per thread
+  constexpr int BMO = 64 * TMO;
+  constexpr int TM = TMO, TN = 2;
+  constexpr int UDY = BMO, UX = 128;
+  static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
 
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BMO][LROW];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNK][LROW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
-  const int o0 = blockIdx.x * BMO;
-  const int k0 = blockIdx.y * BNK;
-  const int64_t rbeg = (int64_t)blockIdx.z * a.rows_per_split;
+  const int l32 = lane & 31, half = lane >> 5;
+  // logical tile (o tile fastest, then k tile, then split): the blocks of one split read
+  // the same pixels and are kept on one XCD
+  const uint32_t gx = gridDim.x, gy = gridDim.y;
+  const uint32_t lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const uint32_t lg = a.remap ? xcd_remap(lin, gx * gy * gridDim.z) : lin;
+  const int bx = (int)(lg % gx), by = (int)((lg / gx) % gy), bz = (int)(lg / (gx * gy));
+  const int o0 = bx * BMO;
+  const int k0 = by * BNK;
+  const int64_t rbeg = (int64_t)bz * a.rows_per_split;
   int64_t rend = rbeg + a.rows_per_split;
   if (rend > a.m) rend = a.m;
   const int nsteps = rend > rbeg ? (int)((rend - rbeg + BR - 1) / BR) : 0;
 
-  // per-unit static description
-  int u_isx[UPT], u_grp[UPT], u_pb[UPT];
-  int u_dh[UPT], u_dw[UPT], u_c[UPT];
-  bool u_ok[UPT];
-#pragma unroll
-  for (int t = 0; t < UPT; ++t) {
-    const int u = tid + 256 * t;
-    u_ok[t] = u < UNITS;
-    const bool isx = u >= UDY;
-    const int v = isx ? u - UDY : u;
-    u_isx[t] = isx;
-    u_grp[t] = v >> 3;  // channel group (dy) or k group (x)
-    u_pb[t] = v & 7;    // pixel block within the step
-    u_dh[t] = u_dw[t] = u_c[t] = 0;
-    if (isx) {
-      const int k = k0 + u_grp[t] * 8;
-      const int tap = k / a.ci;
-      u_c[t] = k - tap * a.ci;
-      u_dh[t] = tap / a.kw - a.ph;
-      u_dw[t] = tap % a.kw - a.pw;
-    }
+  // this thread's unit: channel group grp (8 output channels, or 8 k columns of one tap)
+  // and pixel block pb (8 consecutive pixels of the step).  8 lanes share a channel
+  // group and cover the step's 8 pixel blocks: a load instruction reads 8 pixels x 128
+  // contiguous bytes, and the transposed LDS rows they write are 128 contiguous bytes
+  // (lanes of the next group land in the other half of the banks).
+  const bool isx = tid >= UDY;  // wave-uniform
+  const bool has = tid < UDY + UX;
+  const int v = isx ? tid - UDY : tid;
+  const int grp = v >> 3;
+  const int pb = v & 7;
+  bool uok;
+  uint32_t ucol;  // byte offset of the unit's 8 channels within a pixel
+  int udh = 0, udw = 0;
+  if (!isx) {
+    const int o = o0 + grp * 8;
+    uok = has && o < a.co;
+    ucol = (uint32_t)o * 2;
+  } else {
+    const int k = k0 + grp * 8;
+    uok = has && k < a.ktot;
+    const int tap = k / a.ci, c = k - tap * a.ci;
+    ucol = (uint32_t)c * 2;
+    udh = tap / a.kw - a.ph;
+    udw = tap % a.kw - a.pw;
   }
+  const int howo = a.ho * a.wo;
+  const uint32_t dpix2 = (uint32_t)a.dy_pix * 2, xpix2 = (uint32_t)a.x_pix * 2;
 
-  uint4 Q[UPT][8];
-
-  auto load_step = [&](int st) {
-    const int64_t pbase = rbeg + (int64_t)st * BR;
+  auto load = [&](int st, u32x4 (&xr)[8]) __attribute__((always_inline)) {
+    const int64_t p0 = rbeg + (int64_t)st * BR;  // first pixel of the step
+    if (!isx) {
+      const __amdgpu_buffer_rsrc_t r = wrsrc(a.dy + p0 * a.dy_pix);
 #pragma unroll
-    for (int t = 0; t < UPT; ++t) {
-      uint4 P[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) P[j] = make_uint4(0, 0, 0, 0);
-      if (u_ok[t]) {
-        const int64_t px0 = pbase + u_pb[t] * 8;
-        if (!u_isx[t]) {
-          const int o = o0 + u_grp[t] * 8;
-          if (o < a.co) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const int64_t px = px0 + j;
-              if (px < rend) P[j] = *reinterpret_cast<const uint4*>(a.dy + px * a.dy_pix + o);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int64_t px = px0 + j;
-            if (px >= rend) continue;
-            const uint32_t pm = (uint32_t)px;
-            const uint32_t img = fdiv(pm, div_howo);
-            const uint32_t rem = pm - img * (uint32_t)(a.ho * a.wo);
-            const uint32_t p = fdiv(rem, div_wo);
-            const uint32_t q = rem - p * (uint32_t)a.wo;
-            const int ihb = (int)p * a.sh, iwb = (int)q * a.sw;
-            const int64_t ibase = (int64_t)img * a.h;
-            {
-              const int k = k0 + u_grp[t] * 8;
-              const int ih = ihb + u_dh[t], iw = iwb + u_dw[t];
-              if (k < a.ktot && (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w)
-                P[j] = *reinterpret_cast<const uint4*>(a.x + ((ibase + ih) * a.w + iw) * a.x_pix + u_c[t]);
-            }
-          }
-        }
+      for (int j = 0; j < 8; ++j) {
+        const int pr = pb * 8 + j;
+        const bool ok = uok && p0 + pr < rend;
+        xr[j] = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (uint32_t)pr * dpix2 + ucol : kOobW, 0u, 0);
       }
-      transpose8x8(P, Q[t]);
-    }
-  };
-
-  auto store_step = [&](int buf) {
+    } else {
+      // gather base: the image of the step's first pixel; the unit's first pixel is
+      // found by division, the next seven by stepping the column
+      const uint32_t img_s = p0 < a.m ? fdiv((uint32_t)p0, div_howo) : 0u;
+      const __amdgpu_buffer_rsrc_t r = wrsrc(a.x + (int64_t)img_s * a.h * a.w * a.x_pix);
+      const int64_t pa = p0 + pb * 8;
+      uint32_t img = 0, p = 0, q = 0;
+      if (pa < a.m) {
+        img = fdiv((uint32_t)pa, div_howo);
+        const uint32_t rem = (uint32_t)pa - img * (uint32_t)howo;
+        p = fdiv(rem, div_wo);
+        q = rem - p * (uint32_t)a.wo;
+      }
+      int rel = (int)(img - img_s);
 #pragma unroll
-    for (int t = 0; t < UPT; ++t) {
-      if (!u_ok[t]) continue;
-      const int row0 = u_grp[t] * 8;
-      const int col = u_pb[t] * 8;
-      if (!u_isx[t]) {
-#pragma unroll
-        for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(&As[buf][row0 + c][col]) = Q[t][c];
-      } else {
-#pragma unroll
-        for (int c = 0; c < 8; ++c) *reinterpret_cast<uint4*>(&Bs[buf][row0 + c][col]) = Q[t][c];
+      for (int j = 0; j < 8; ++j) {
+        const int ih = (int)p * a.sh + udh, iw = (int)q * a.sw + udw;
+        const bool ok = uok && pa + j < rend && (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w;
+        const uint32_t off = (uint32_t)(((rel * a.h + ih) * a.w + iw)) * xpix2 + ucol;
+        xr[j] = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOobW, 0u, 0);
+        ++q;
+        const bool wq = q == (uint32_t)a.wo;
+        q = wq ? 0u : q;
+        p += wq ? 1u : 0u;
+        const bool wp = p == (uint32_t)a.ho;
+        p = wp ? 0u : p;
+        rel += wp ? 1 : 0;
       }
     }
   };
+  auto store = [&](int buf, const u32x4 (&xr)[8]) __attribute__((always_inline)) {
+    if (!has) return;
+    u32x4 Q[8];
+    transpose8x8(xr, Q);
+    const int col = pb * 8;
+    if (!isx) {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) *reinterpret_cast<u32x4*>(&As[buf][grp * 8 + c][col]) = Q[c];
+    } else {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) *reinterpret_cast<u32x4*>(&Bs[buf][grp * 8 + c][col]) = Q[c];
+    }
+  };
 
-  f32x4 acc[TM][TN];
+  f32x16 acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  if (nsteps > 0) {
-    load_step(0);
-    store_step(0);
-    __syncthreads();
-  }
-  for (int st = 0; st < nsteps; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nsteps) load_step(st + 1);
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-    for (int ks = 0; ks < BR / 32; ++ks) {
-      const int kc = ks * 32 + (lane >> 4) * 8;
-      uint4 af[TM], bfr[TN];
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int ks = 0; ks < BR / 16; ++ks) {
+      u32x4 af[TM], bf[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const uint4*>(&As[buf][wm * TM * 16 + i * 16 + (lane & 15)][kc]);
+        af[i] = *reinterpret_cast<const u32x4*>(&As[buf][wm * 32 * TM + i * 32 + l32][ks * 16 + half * 8]);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const uint4*>(&Bs[buf][wn * TN * 16 + j * 16 + (lane & 15)][kc]);
+        bf[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][wn * 64 + j * 32 + l32][ks * 16 + half * 8]);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
     }
-    if (st + 1 < nsteps) store_step(buf ^ 1);
+  };
+
+  // step kt: stage step kt+1 in LDS, issue the loads of step kt+1+D, multiply step kt
+  u32x4 ring[D][8];
+  auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
+    constexpr int u = decltype(uc)::value;
+    constexpr int nxt = (u + 1) % D;
+    store((kt + 1) & 1, ring[nxt]);
+    load(kt + 1 + D, ring[nxt]);
+    compute(kt & 1);
+    __syncthreads();
+  };
+  // prologue in the steady state's issue order (step 0 to LDS, steps 1..D in flight)
+  if (nsteps > 0) {
+    load(0, ring[0]);
+    store(0, ring[0]);
+    if constexpr (D > 1) load(1, ring[1]);
+    if constexpr (D > 2) load(2, ring[2]);
+    if constexpr (D > 3) load(3, ring[3]);
+    load(D, ring[0]);
     __syncthreads();
   }
+  int kb = 0;
+  for (; kb + D <= nsteps; kb += D) {
+    step(Ic<0>{}, kb);
+    if constexpr (D > 1) step(Ic<1 % D>{}, kb + 1);
+    if constexpr (D > 2) step(Ic<2 % D>{}, kb + 2);
+    if constexpr (D > 3) step(Ic<3 % D>{}, kb + 3);
+  }
+  if constexpr (D > 1) {
+    if (kb < nsteps) step(Ic<0>{}, kb);
+  }
+  if constexpr (D > 2) {
+    if (kb + 1 < nsteps) step(Ic<1 % D>{}, kb + 1);
+  }
+  if constexpr (D > 3) {
+    if (kb + 2 < nsteps) step(Ic<2 % D>{}, kb + 2);
+  }
 
-  // epilogue: rows = output channels, cols = k
-  float* out = a.out + (a.splits > 1 ? (int64_t)blockIdx.z * a.co * a.ktot : 0);
+  // epilogue: accumulator register r of a lane is output channel row 8*(r/4) +
+  // 4*(lane/32) + (r%4) of its 32-row block, k column lane%32
+  float* out = a.out + (a.splits > 1 ? (int64_t)bz * a.co * a.ktot : 0);
   const bool acc_in = a.splits == 1 && a.accumulate;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int o = o0 + wm * TM * 16 + i * 16 + 4 * (lane >> 4) + e;
-      if (o >= a.co) continue;
+    for (int j = 0; j < TN; ++j) {
+      const int k = k0 + wn * 64 + j * 32 + l32;
+      if (k >= a.ktot) continue;
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int k = k0 + wn * TN * 16 + j * 16 + (lane & 15);
-        if (k >= a.ktot) continue;
+      for (int r = 0; r < 16; ++r) {
+        const int o = o0 + wm * 32 * TM + i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        if (o >= a.co) continue;
         float* p = out + (int64_t)o * a.ktot + k;
-        const float v = acc[i][j][e];
-        *p = acc_in ? *p + v : v;
+        const float val = acc[i][j][r];
+        *p = acc_in ? *p + val : val;
       }
     }
 }
 
-template <int TM, int TN>
+template <int TMO>
 hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
-  constexpr int BMO = 2 * TM * 16, BNK = 2 * TN * 16;
+  constexpr int BMO = 64 * TMO;
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
   trace_begin(KC_WGRAD, s);
-  hipLaunchKernelGGL((wgrad_kernel<TM, TN>), grid, dim3(256), 0, s, a, dwo, dhw);
+  hipLaunchKernelGGL((wgrad_kernel<TMO, 2>), grid, dim3(256), 0, s, a, dwo, dhw);
   trace_end(KC_WGRAD, s);
   return hipGetLastError();
 }
@@ -236,8 +285,13 @@ __global__ void splitk_reduce_kernel(const float4* part, int splits, int64_t cou
 
 }  // namespace
 
+// output-channel tile: 128 rows (twice the multiply per loaded x tile of 64 rows, which
+// outweighs the padding of channel counts like 192), 64 when one such tile covers c_out
+int wgrad_bmo(int co) { return co <= 64 ? 64 : 128; }
+
 int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
-  const int tiles = (int)(((co + 127) / 128) * ((ktot + 127) / 128));
+  const int bmo = wgrad_bmo(co);
+  const int tiles = (int)(((co + bmo - 1) / bmo) * ((ktot + BNK - 1) / BNK));
   const int64_t steps = (m + BR - 1) / BR;
   int64_t splits = (512 + tiles - 1) / tiles;
   // at least 16 steps per split, at most 256 splits, partials at most 64 MiB
@@ -253,7 +307,14 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   return (int)(splits < 1 ? 1 : splits);
 }
 
-hipError_t wgrad_launch(const WgradArgs& a, hipStream_t s) { return launch_w<4, 4>(a, s); }
+hipError_t wgrad_launch(const WgradArgs& args, hipStream_t s) {
+  WgradArgs a = args;
+  a.remap = 0;
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_REMAP_WG")) a.remap = atoi(e);
+#endif
+  return wgrad_bmo(a.co) == 64 ? launch_w<1>(a, s) : launch_w<2>(a, s);
+}
 
 hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
                                 hipStream_t s) {

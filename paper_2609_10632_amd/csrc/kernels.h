@@ -81,6 +81,7 @@ struct ConvGemmArgs {
   float2* stats_part;  // phase 0 only: [m tiles][nout] (tile mean, tile M2) or nullptr
   int32_t nphase;
   int32_t halo_px;     // set by convgemm_launch: pixels the fast path's gather base sits before an image
+  int32_t remap;       // set by convgemm_launch: XCD-aware tile order (see xcd_remap)
   GemmPhase ph[kMaxPhases];
 };
 // tile and kernel for a problem with at most m_max rows per phase, nout columns, cs
@@ -119,6 +120,7 @@ struct WgradArgs {
   int64_t rows_per_split;  // multiple of the reduction step
   float* out;           // splits == 1: dw (accumulate honoured); else partials [splits][co][ktot]
   int32_t accumulate;
+  int32_t remap;        // set by wgrad_launch: XCD-aware tile order (see xcd_remap)
 };
 int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split);
 hipError_t wgrad_launch(const WgradArgs& a, hipStream_t s);
