@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-events", action="store_true", help="skip the instrumented (per-kernel timing) steps")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
+    ap.add_argument("--serial", action="store_true",
+                    help="run the whole step on one stream (default: weight gradients on a second stream)")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
     return ap.parse_args()
@@ -83,8 +85,8 @@ class Layer:
         self.flops = spec.gemm_flops(n)  # one pass
         self.bn_elems = self.blk.m * spec.co
 
-    def bind_ws(self, ws):
-        self.ws = ws
+    def bind_ws(self, ws, ws_side):
+        self.ws, self.ws_side = ws, ws_side
         self.ws_len = ws.numel()
 
     def fwd(self, ev=None):
@@ -97,14 +99,25 @@ class Layer:
                               self.srstd, ws=self.ws, ws_bytes=self.ws_len)
         if e: e[2].record()
 
-    def bwd(self, ev=None):
+    def bwd(self, ev=None, side=None):
+        """BN/SiLU backward, then the weight and data gradients.  With a side stream the
+        weight gradient (which nothing later in the backward pass reads) runs there, on its
+        own workspace, overlapping the data gradient and the following layers."""
         nb = self.nb
         e = ev.get(self.name) if ev else None
         if e: e[3].record()
         nb.numbat_bn_silu_bwd(self.bnp, self.g, self.y, self.smean, self.srstd, self.gamma, self.beta, self.dy,
                               self.dgamma, self.dbeta, None, ws=self.ws, ws_bytes=self.ws_len)
         if e: e[4].record()
-        nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
+        if side is not None:
+            import torch
+
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws_side,
+                                          ws_bytes=self.ws_len)
+        else:
+            nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
         if e: e[5].record()
         nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
         if e: e[6].record()
@@ -196,16 +209,23 @@ def main():
     print(f"# setting up {len(specs)} layers of configuration {wl.index} at batch {wl.n}", file=sys.stderr, flush=True)
     layers = [Layer(i, l, wl.n, wl.index, wl.eps) for i, l in enumerate(specs)]
     ws = torch.empty(max(l.ws_need for l in layers), dtype=torch.uint8, device="cuda")
+    ws_side = torch.empty_like(ws)
     for l in layers:
-        l.bind_ws(ws)
+        l.bind_ws(ws, ws_side)
+    side = None if args.serial else torch.cuda.Stream()  # default priority
     torch.cuda.synchronize()
     step_flops = sum(3 * l.flops for l in layers)
 
-    def step(ev=None):
+    def step(ev=None, overlap=True):
+        """One training step of the conv set: every layer's forward, then the backward in
+        reverse order.  overlap=False keeps everything on one stream (per-kernel timing)."""
+        sd = side if overlap else None
         for l in layers:
             l.fwd(ev)
         for l in reversed(layers):
-            l.bwd(ev)
+            l.bwd(ev, sd)
+        if sd is not None:
+            torch.cuda.current_stream().wait_stream(sd)
 
     print(f"# warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -244,7 +264,7 @@ def main():
         nb.numbat_timing_enable(True)
         ti0 = time.perf_counter()
         for _ in range(args.steps):
-            step()
+            step(overlap=False)
         torch.cuda.synchronize()
         ms_instr = (time.perf_counter() - ti0) * 1e3 / args.steps
         for c in range(n_cls):
@@ -285,7 +305,8 @@ def main():
         "config": {"workload": wl.name + (f" [{len(layers)} layers]" if args.layers else ""),
                    "config_index": wl.index, "batch": wl.n, "input": "640x640", "layers": len(layers),
                    "mode": "set", "step_gflop": round(step_flops / 1e9, 2),
-                   "launch": "hip graph replay" if graph is not None else "eager"},
+                   "launch": "hip graph replay" if graph is not None else "eager",
+                   "streams": 1 if args.serial else 2},
         "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": roofline,
     }
@@ -297,7 +318,7 @@ def main():
         out["instrumented_ms_per_step"] = round(ms_instr, 3)
     if args.detail:
         ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
-        step(ev)
+        step(ev, overlap=False)
         torch.cuda.synchronize()
         per_layer = {}
         for l in layers:

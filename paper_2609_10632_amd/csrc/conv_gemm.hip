@@ -550,20 +550,26 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // multiply the tiles in LDS buffer buf: fragments of k-slice ks+1 are read while the
+  // MFMAs of slice ks run
+  auto read_frags = [&](int buf, int ks, u32x4 (&af)[TM], u32x4 (&bf)[TN]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      af[i] = *reinterpret_cast<const u32x4*>(&As[buf][wave * WTM + i * 32 + l32][ks * 16 + half * 8]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      bf[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][j * 32 + l32][ks * 16 + half * 8]);
+  };
   auto compute = [&](int buf) __attribute__((always_inline)) {
+    u32x4 af[2][TM], bf[2][TN];
+    read_frags(buf, 0, af[0], bf[0]);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      u32x4 afr[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        afr[i] = *reinterpret_cast<const u32x4*>(&As[buf][wave * WTM + i * 32 + l32][ks * 16 + half * 8]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][j * 32 + l32][ks * 16 + half * 8]);
+      if (ks < 3) read_frags(buf, ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(afr[i], bfr[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
     }
   };
   // step kt (ring slot of step kt+1 = nxt): stage step kt+1 in LDS, fetch step kt+1+D
@@ -571,9 +577,9 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
   auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
     constexpr int u = decltype(uc)::value;
     constexpr int nxt = (u + 1) % D;
+    compute(kt & 1);
     store((kt + 1) & 1, ra[nxt], rbv[nxt]);
     load(kt + 1 + D, ra[nxt], rbv[nxt]);
-    compute(kt & 1);
     __syncthreads();
   };
   // Prologue: step 0 goes to LDS; steps 1..D are left in flight, in the order the
