@@ -181,7 +181,12 @@ size_t fwd_stats_bytes(const ConvDesc& d) {
 
 size_t fwd_ws(const ConvDesc& d) { return fwd_stats_bytes(d) + (narrow(d) ? x8_bytes(d) + w8_bytes(d) : 0); }
 
-size_t bwd_data_ws(const ConvDesc& d) { return round_up((size_t)d.kh * d.kw * d.ci * d.co * 2, 256); }
+// data gradient: re-laid-out weights (channels padded to 8 for a narrow input) and, for a
+// narrow input, the 8-channel gradient the GEMM writes before the ci channels are taken
+size_t dgrad_cpad(const ConvDesc& d) { return narrow(d) ? 8 : d.ci; }
+size_t bwd_data_ws(const ConvDesc& d) {
+  return round_up((size_t)d.kh * d.kw * dgrad_cpad(d) * d.co * 2, 256) + (narrow(d) ? x8_bytes(d) : 0);
+}
 
 size_t dw8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 8 * sizeof(float), 256); }
 
@@ -432,6 +437,7 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   if (st != NUMBAT_OK) return st;
 
   // stride phases (a, b): input rows h = a + sh*i read output rows p = i + (a + ph - r) / sh
+  const int cpad = (int)dgrad_cpad(d);
   PhaseTaps ph[16];
   int first[16];
   int nphase = 0, total = 0;
@@ -453,14 +459,27 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
           ++f.count;
         }
       }
-      first[nphase] = total * d.ci * d.co;
+      first[nphase] = total * cpad * d.co;
       total += f.count;
       ++nphase;
     }
   hipStream_t s = static_cast<hipStream_t>(stream);
   bf16_t* wt = static_cast<bf16_t*>(ws);
-  hipError_t e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, first, ph, nphase, s);
+  hipError_t e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, cpad, first, ph,
+                                      nphase, s);
   if (e != hipSuccess) return hip_fail(e, "data-gradient weight re-layout launch");
+  // a narrow input's gradient is computed as 8 channels (padding channels have zero
+  // weights) into the workspace, so the GEMM writes whole 16-byte vectors; with
+  // accumulate the workspace first receives dx, so the sum is formed in fp32 and rounded
+  // once as on the direct path
+  bf16_t* dx8 = nullptr;
+  if (narrow(d)) {
+    dx8 = reinterpret_cast<bf16_t*>(static_cast<char*>(ws) + round_up((size_t)d.kh * d.kw * cpad * d.co * 2, 256));
+    if (accumulate) {
+      e = pack8_launch(static_cast<const bf16_t*>(dx), d.x_pix, d.ci, (int64_t)d.n * d.h * d.w, dx8, s);
+      if (e != hipSuccess) return hip_fail(e, "gradient repack launch");
+    }
+  }
   // all stride phases in launches of up to kMaxPhases phases (blockIdx.z = phase)
   ConvGemmArgs g;
   std::memset(&g, 0, sizeof g);
@@ -469,11 +488,11 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   g.hs = d.ho;
   g.ws = d.wo;
   g.cs = d.co;
-  g.nout = d.ci;
+  g.nout = cpad;
   g.nimg = d.n;
   g.gstride_h = g.gstride_w = 1;
-  g.dst = static_cast<bf16_t*>(dx);
-  g.dst_pix = d.x_pix;
+  g.dst = dx8 ? dx8 : static_cast<bf16_t*>(dx);
+  g.dst_pix = dx8 ? 8 : d.x_pix;
   g.hd = d.h;
   g.wd = d.w;
   g.dstep_h = d.sh;
@@ -504,7 +523,7 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
       ktmax = P.ktot > ktmax ? P.ktot : ktmax;
       const bool last = (pa == d.sh - 1 && pb == d.sw - 1);
       if (g.nphase == kMaxPhases || last) {
-        e = convgemm_launch(g, convgemm_pick(mmax, d.ci, d.co, ktmax), s, KC_CONV_DGRAD);
+        e = convgemm_launch(g, convgemm_pick(mmax, cpad, d.co, ktmax), s, KC_CONV_DGRAD);
         if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
         g.nphase = 0;
         mmax = 0;
@@ -512,8 +531,12 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
       }
     }
   if (g.nphase > 0) {
-    e = convgemm_launch(g, convgemm_pick(mmax, d.ci, d.co, ktmax), s, KC_CONV_DGRAD);
+    e = convgemm_launch(g, convgemm_pick(mmax, cpad, d.co, ktmax), s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+  }
+  if (dx8) {
+    e = unpack8_launch(dx8, d.ci, (int64_t)d.n * d.h * d.w, static_cast<bf16_t*>(dx), d.x_pix, s);
+    if (e != hipSuccess) return hip_fail(e, "gradient channel extraction launch");
   }
   return ok();
 }

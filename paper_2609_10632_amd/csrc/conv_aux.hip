@@ -90,48 +90,64 @@ namespace {
 
 struct PhaseTable {
   int nphase;
-  int first[16];  // element offset of each phase's matrix inside wt
+  int first[16];     // element offset of each phase's matrix inside wt
+  int row_first[16]; // first destination row of each phase (rows are (c, tap) pairs)
   int count[16];
   int r[16][kMaxTaps], s[16][kMaxTaps];
 };
 
-__global__ void dgrad_weights_kernel(const bf16_t* w, bf16_t* wt, int co, int kh, int kw, int ci, PhaseTable tab) {
-  const int64_t total = (int64_t)co * kh * kw * ci;
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-    // i enumerates the destination: find phase, then (c, t, o)
+// One thread writes 8 consecutive output channels (16 bytes) of one destination row
+// (phase f, channel c, tap t): wt[f][c][t][o..o+7] = w[o..o+7][r][s][c], zero for the
+// padding channels c >= ci.
+__global__ void dgrad_weights_kernel(const bf16_t* w, uint4* wt, int co, int kh, int kw, int ci, int cpad, int nchunks,
+                                     PhaseTable tab) {
+  const int cpr = co / 8;  // chunks per row
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < nchunks; i += gridDim.x * blockDim.x) {
+    const int row = i / cpr, oc = i - row * cpr;
     int f = 0;
-    while (f + 1 < tab.nphase && i >= tab.first[f + 1]) ++f;
-    const int64_t j = i - tab.first[f];
+    while (f + 1 < tab.nphase && row >= tab.row_first[f + 1]) ++f;
     const int T = tab.count[f];
-    const int o = (int)(j % co);
-    const int64_t ct = j / co;
-    const int t = (int)(ct % T);
-    const int c = (int)(ct / T);
-    const int r = tab.r[f][t], s = tab.s[f][t];
-    wt[i] = w[(((int64_t)o * kh + r) * kw + s) * ci + c];
+    const int rl = row - tab.row_first[f];
+    const int c = rl / T, t = rl - (rl / T) * T;
+    uint32_t h[8];
+    if (c < ci) {
+      const bf16_t* src = w + ((int64_t)(oc * 8) * kh * kw + (int64_t)tab.r[f][t] * kw + tab.s[f][t]) * ci + c;
+      const int64_t ostride = (int64_t)kh * kw * ci;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[e] = src[e * ostride];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) h[e] = 0u;
+    }
+    const int64_t dst = (tab.first[f] + ((int64_t)c * T + t) * co) / 8 + oc;
+    wt[dst] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
   }
 }
 
 }  // namespace
 
-hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int kw, int ci, const int* phase_first,
-                                const PhaseTaps* phases, int nphase, hipStream_t s) {
+hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int kw, int ci, int cpad,
+                                const int* phase_first, const PhaseTaps* phases, int nphase, hipStream_t s) {
   PhaseTable tab;
   tab.nphase = nphase;
+  int rows = 0;
   for (int f = 0; f < nphase; ++f) {
     tab.first[f] = phase_first[f];
+    tab.row_first[f] = rows;
     tab.count[f] = phases[f].count;
+    rows += cpad * phases[f].count;
     for (int t = 0; t < phases[f].count; ++t) {
       tab.r[f][t] = phases[f].r[t];
       tab.s[f][t] = phases[f].s[t];
     }
   }
-  const int64_t total = (int64_t)co * kh * kw * ci;
-  int blocks = (int)((total + 255) / 256);
+  const int nchunks = rows * (co / 8);
+  int blocks = (nchunks + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
   trace_begin(KC_DGRAD_WEIGHTS, s);
-  hipLaunchKernelGGL(dgrad_weights_kernel, dim3(blocks), dim3(256), 0, s, w, wt, co, kh, kw, ci, tab);
+  hipLaunchKernelGGL(dgrad_weights_kernel, dim3(blocks), dim3(256), 0, s, w, reinterpret_cast<uint4*>(wt), co, kh, kw,
+                     ci, cpad, nchunks, tab);
   trace_end(KC_DGRAD_WEIGHTS, s);
   return hipGetLastError();
 }
@@ -163,6 +179,18 @@ __global__ void unpack_dw_kernel(const float* dw8, float* dw, int64_t rows, int 
   }
 }
 
+// dst[i*dst_pix + c] (+)= src[i][c] for c < ci: the narrow channels of an 8-channel bf16
+// tensor (the data gradient of a 3-channel input, which the GEMM writes padded to 8)
+__global__ void unpack8_kernel(const uint4* src, int ci, int64_t n, bf16_t* dst, int64_t dst_pix) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint4 v = src[i];
+    const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+      if (c < ci) dst[i * dst_pix + c] = (bf16_t)(wd[c >> 1] >> (16 * (c & 1)));
+  }
+}
+
 int blocks_for(int64_t n) {
   int64_t b = (n + 255) / 256;
   if (b > 16384) b = 16384;
@@ -174,6 +202,14 @@ int blocks_for(int64_t n) {
 hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s) {
   trace_begin(KC_PACK, s);
   hipLaunchKernelGGL(pack8_kernel, dim3(blocks_for(n)), dim3(256), 0, s, src, src_pix, ci, n, reinterpret_cast<uint4*>(dst));
+  trace_end(KC_PACK, s);
+  return hipGetLastError();
+}
+
+hipError_t unpack8_launch(const bf16_t* src8, int ci, int64_t n, bf16_t* dst, int64_t dst_pix, hipStream_t s) {
+  trace_begin(KC_PACK, s);
+  hipLaunchKernelGGL(unpack8_kernel, dim3(blocks_for(n)), dim3(256), 0, s, reinterpret_cast<const uint4*>(src8), ci, n, dst,
+                     dst_pix);
   trace_end(KC_PACK, s);
   return hipGetLastError();
 }

@@ -69,12 +69,45 @@ __device__ __forceinline__ TileId tile_id(bool remap) {
   return TileId{(int)((lg / gy) % gx), (int)(lg % gy), (int)(lg / (gx * gy))};
 }
 
+// The per-phase geometry a block needs, read from the kernel arguments once at entry
+// (the phase is chosen by the block index, so every field access would otherwise be a
+// dependent scalar load)
+struct Geo {
+  int m, gh, gw;
+  FastDiv div_gw, div_ghw;
+  int doff_h, doff_w;
+  int tw, th, dh0, dw0, tsh, tsw;
+};
+__device__ __forceinline__ Geo load_geo(const GemmPhase& P) {
+  Geo g;
+  g.m = P.m;
+  g.gh = P.gh;
+  g.gw = P.gw;
+  g.div_gw = P.div_gw;
+  g.div_ghw = P.div_ghw;
+  g.doff_h = P.doff_h;
+  g.doff_w = P.doff_w;
+  g.tw = P.tw;
+  g.th = P.th;
+  g.dh0 = P.dh0;
+  g.dw0 = P.dw0;
+  g.tsh = P.tsh;
+  g.tsw = P.tsw;
+  return g;
+}
+__device__ __forceinline__ void geo_pos(uint32_t m, const Geo& G, uint32_t& img, uint32_t& gi, uint32_t& gj) {
+  img = fdiv(m, G.div_ghw);
+  const uint32_t rem = m - img * (uint32_t)(G.gh * G.gw);
+  gi = fdiv(rem, G.div_gw);
+  gj = rem - gi * (uint32_t)G.gw;
+}
+
 // destination element offset of GEMM row m (-1 past the phase's rows)
-__device__ __forceinline__ int64_t dst_offset(const ConvGemmArgs& a, const GemmPhase& P, int m) {
-  if (m >= P.m) return -1;
+__device__ __forceinline__ int64_t dst_offset(const ConvGemmArgs& a, const Geo& G, int m) {
+  if (m >= G.m) return -1;
   uint32_t img, gi, gj;
-  grid_pos((uint32_t)m, P, img, gi, gj);
-  return (((int64_t)img * a.hd + (int)gi * a.dstep_h + P.doff_h) * a.wd + (int)gj * a.dstep_w + P.doff_w) *
+  geo_pos((uint32_t)m, G, img, gi, gj);
+  return (((int64_t)img * a.hd + (int)gi * a.dstep_h + G.doff_h) * a.wd + (int)gj * a.dstep_w + G.doff_w) *
          a.dst_pix;
 }
 
@@ -82,28 +115,24 @@ __device__ __forceinline__ int64_t dst_offset(const ConvGemmArgs& a, const GemmP
 // pixel, and the bitmask of its taps that fall inside the image.  The taps form a grid
 // (rows of tw taps with constant steps), so the mask is the outer product of the grid
 // rows that stay inside the image height and the grid columns inside its width.
-__device__ __forceinline__ void row_gather(const ConvGemmArgs& a, const GemmPhase& P, int m, uint32_t img0,
+__device__ __forceinline__ void row_gather(const ConvGemmArgs& a, const Geo& G, int m, uint32_t img0,
                                            uint32_t& vrow, uint32_t& vmask) {
   vrow = 0;
   vmask = 0;
-  if (m >= P.m) return;
+  if (m >= G.m) return;
   uint32_t img, gi, gj;
-  grid_pos((uint32_t)m, P, img, gi, gj);
+  geo_pos((uint32_t)m, G, img, gi, gj);
   const int ih0 = (int)gi * a.gstride_h, iw0 = (int)gj * a.gstride_w;
   vrow = (uint32_t)((((int64_t)(img - img0) * a.hs + ih0) * a.ws + iw0) * (a.src_pix * 2));
-  const int tw = P.tw, th = P.taps / tw;
-  const int dh0 = (int)(int16_t)(P.off[0] & 0xffff), dw0 = P.off[0] >> 16;
-  const int sh = th > 1 ? (int)(int16_t)(P.off[tw] & 0xffff) - dh0 : 0;
-  const int sw = tw > 1 ? (P.off[1] >> 16) - dw0 : 0;
   uint32_t cols = 0;
-  for (int j = 0; j < tw; ++j) {
-    const int iw = iw0 + dw0 + j * sw;
+  for (int j = 0; j < G.tw; ++j) {
+    const int iw = iw0 + G.dw0 + j * G.tsw;
     cols |= ((unsigned)iw < (unsigned)a.ws ? 1u : 0u) << j;
   }
   uint32_t mk = 0;
-  for (int i = 0; i < th; ++i) {
-    const int ih = ih0 + dh0 + i * sh;
-    mk |= ((unsigned)ih < (unsigned)a.hs ? cols : 0u) << (i * tw);
+  for (int i = 0; i < G.th; ++i) {
+    const int ih = ih0 + G.dh0 + i * G.tsh;
+    mk |= ((unsigned)ih < (unsigned)a.hs ? cols : 0u) << (i * G.tw);
   }
   vmask = mk;  // bits >= taps stay clear, so a walk past the last tap reads zeros
 }
@@ -477,16 +506,17 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
   const int l32 = lane & 31, half = lane >> 5;
   const int ck = tid & 7, rg = tid >> 3;  // this thread's load chunk and row within a 32-row group
 
-  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, P, m0 + r);
+  const Geo G = load_geo(P);
+  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, G, m0 + r);
 
   // A: gather base = first image of the tile, moved back by the halo (carried by toff0)
-  const uint32_t img0 = fdiv((uint32_t)m0, P.div_ghw);
+  const uint32_t img0 = fdiv((uint32_t)m0, G.div_ghw);
   const __amdgpu_buffer_rsrc_t rsA =
       buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
   uint32_t vrow[AV], vmask[AV];  // rows q*32 + rg of the tile
 #pragma unroll
-  for (int q = 0; q < AV; ++q) row_gather(a, P, m0 + q * 32 + rg, img0, vrow[q], vmask[q]);
-// B: rows j*32 + rg of the weight tile, chunk ck
+  for (int q = 0; q < AV; ++q) row_gather(a, G, m0 + q * 32 + rg, img0, vrow[q], vmask[q]);
+  // B: rows j*32 + rg of the weight tile, chunk ck
   const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
   const int p_tw = P.tw, p_ktot = P.ktot, cs = a.cs;
   const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
@@ -645,15 +675,16 @@ __global__ __launch_bounds__(256) void convdirect_kernel(ConvGemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
-  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, P, m0 + r);
+  const Geo G = load_geo(P);
+  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, G, m0 + r);
 
-  const uint32_t img0 = fdiv((uint32_t)m0, P.div_ghw);
+  const uint32_t img0 = fdiv((uint32_t)m0, G.div_ghw);
   const __amdgpu_buffer_rsrc_t rsA =
       buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
   uint32_t vrow[TM], vmask[TM];
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    row_gather(a, P, m0 + wave * WTM + i * 32 + l32, img0, vrow[i], vmask[i]);
+    row_gather(a, G, m0 + wave * WTM + i * 32 + l32, img0, vrow[i], vmask[i]);
     vrow[i] += half * 16;
   }
   const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
@@ -845,6 +876,11 @@ bool prepare_fast(ConvGemmArgs& a, int bm) {
     }
     if ((int64_t)a.nout * P.ktot * 2 >= (int64_t)kRecords) return false;  // weight offsets are 32-bit too
     P.tw = tw;
+    P.th = P.taps / tw;
+    P.dh0 = tap_dh(P.off[0]);
+    P.dw0 = tap_dw(P.off[0]);
+    P.tsh = sh;
+    P.tsw = sw;
     P.toff0 = (int32_t)(((int64_t)tap_dh(P.off[0]) * a.ws + tap_dw(P.off[0]) + halo) * pix2);
     P.cstep = (int32_t)((int64_t)sw * pix2);
     P.rstep = (int32_t)(((int64_t)sh * a.ws - (int64_t)(tw - 1) * sw) * pix2);

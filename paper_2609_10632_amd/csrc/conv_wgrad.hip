@@ -260,27 +260,51 @@ hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// dw = [dw +] sum over splits in split order; four consecutive outputs per thread
-__global__ void splitk_reduce_kernel(const float4* part, int splits, int64_t count4, float* dw, int accumulate) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < count4; i += (int64_t)gridDim.x * blockDim.x) {
-    float4 t = part[i];
-    int k = 1;
-    for (; k + 1 < splits; k += 2) {
+// dw = [dw +] sum over splits, four consecutive outputs per thread.  The splits are cut
+// into G contiguous groups summed by G threads in split order; the G group sums are then
+// added in group order.  The order depends only on (splits, G), so the result is bitwise
+// reproducible.  A block holds 256/G outputs (float4) x G groups.
+template <int G>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float4* part, int splits, int64_t count4, float* dw,
+                                                            int accumulate) {
+  constexpr int OPB = 256 / G;  // float4 outputs per block
+  __shared__ float4 s_sum[G][OPB];
+  const int g = threadIdx.x / OPB, lo = threadIdx.x % OPB;
+  const int64_t i = blockIdx.x * (int64_t)OPB + lo;
+  const int s0 = (int)((int64_t)splits * g / G), s1 = (int)((int64_t)splits * (g + 1) / G);
+  float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < count4) {
+    for (int k = s0; k < s1; ++k) {
       const float4 u = part[(int64_t)k * count4 + i];
-      const float4 v = part[(int64_t)(k + 1) * count4 + i];
-      t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
-      t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+      t.x += u.x;
+      t.y += u.y;
+      t.z += u.z;
+      t.w += u.w;
     }
-    if (k < splits) {
-      const float4 u = part[(int64_t)k * count4 + i];
-      t.x += u.x; t.y += u.y; t.z += u.z; t.w += u.w;
-    }
-    float* o = dw + 4 * i;
-    if (accumulate) {
-      t.x = o[0] + t.x; t.y = o[1] + t.y; t.z = o[2] + t.z; t.w = o[3] + t.w;
-    }
-    o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
   }
+  s_sum[g][lo] = t;
+  __syncthreads();
+  if (g != 0 || i >= count4) return;
+  float4 r = s_sum[0][lo];
+#pragma unroll
+  for (int k = 1; k < G; ++k) {
+    const float4 u = s_sum[k][lo];
+    r.x += u.x;
+    r.y += u.y;
+    r.z += u.z;
+    r.w += u.w;
+  }
+  float* o = dw + 4 * i;
+  if (accumulate) {
+    r.x = o[0] + r.x;
+    r.y = o[1] + r.y;
+    r.z = o[2] + r.z;
+    r.w = o[3] + r.w;
+  }
+  o[0] = r.x;
+  o[1] = r.y;
+  o[2] = r.z;
+  o[3] = r.w;
 }
 
 }  // namespace
@@ -318,14 +342,24 @@ hipError_t wgrad_launch(const WgradArgs& args, hipStream_t s) {
 
 hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
                                 hipStream_t s) {
-  // count = c_out * k_total is a multiple of 8 (c_out is)
+  // count = c_out * k_total is a multiple of 8 (c_out is).  Split groups: enough to give
+  // ~1024 blocks (each thread then sums a handful of splits), at most one per split.
   const int64_t count4 = count / 4;
-  int64_t blocks = (count4 + 255) / 256;
-  if (blocks > 8192) blocks = 8192;
-  if (blocks < 1) blocks = 1;
+  int G = 1;
+  while (G < 64 && G < splits && (count4 * G) / 256 < 1024) G *= 2;
+  const float4* p4 = reinterpret_cast<const float4*>(part);
+  const int opb = 256 / G;
+  const unsigned blocks = (unsigned)((count4 + opb - 1) / opb);
   trace_begin(KC_SPLITK_REDUCE, s);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
-                     reinterpret_cast<const float4*>(part), splits, count4, dw, accumulate);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(splitk_reduce_kernel<1>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 2: hipLaunchKernelGGL(splitk_reduce_kernel<2>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 4: hipLaunchKernelGGL(splitk_reduce_kernel<4>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 8: hipLaunchKernelGGL(splitk_reduce_kernel<8>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 16: hipLaunchKernelGGL(splitk_reduce_kernel<16>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 32: hipLaunchKernelGGL(splitk_reduce_kernel<32>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    default: hipLaunchKernelGGL(splitk_reduce_kernel<64>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+  }
   trace_end(KC_SPLITK_REDUCE, s);
   return hipGetLastError();
 }

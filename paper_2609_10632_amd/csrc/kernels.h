@@ -65,8 +65,10 @@ struct GemmPhase {
   int32_t off[kMaxTaps];  // (off_h & 0xffff) | (off_w << 16)
   // set by convgemm_launch: taps per grid row, byte offset of tap 0 (plus the halo
   // shift), byte step to the next tap in a row and from a row's last tap to the next
-  // row's first
+  // row's first; grid rows, offsets of tap 0 and the (+-1 or 0) offset steps between
+  // grid rows and columns
   int32_t tw, toff0, cstep, rstep;
+  int32_t th, dh0, dw0, tsh, tsw;
 };
 struct ConvGemmArgs {
   const bf16_t* src;
@@ -94,18 +96,20 @@ hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int 
 // from a weight gradient computed on the repacked layout
 hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s);
 hipError_t unpack_dw_launch(const float* dw8, float* dw, int64_t rows, int ci, int accumulate, hipStream_t s);
+hipError_t unpack8_launch(const bf16_t* src8, int ci, int64_t n, bf16_t* dst, int64_t dst_pix, hipStream_t s);
 
 // merge per-tile (mean, M2) partials into batch mean / biased variance, fixed order
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,
                               hipStream_t s);
 
-// dgrad weight re-layout: for each stride phase, wt[c][tap][o] = w[o][r][s][c]
+// dgrad weight re-layout: for each stride phase, wt[c][tap][o] = w[o][r][s][c] for
+// c < ci and 0 for ci <= c < cpad (phase_first counts cpad rows of channels)
 struct PhaseTaps {
   int count;
   int r[kMaxTaps], s[kMaxTaps];
 };
-hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int kw, int ci, const int* phase_first,
-                                const PhaseTaps* phases, int nphase, hipStream_t s);
+hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int kw, int ci, int cpad,
+                                const int* phase_first, const PhaseTaps* phases, int nphase, hipStream_t s);
 
 // weight gradient: split-K implicit GEMM and its fixed-order reduction
 struct WgradArgs {
