@@ -126,6 +126,37 @@ class Layer:
 PASSES = ("conv_fwd", "bn_silu_fwd", "bn_silu_bwd", "conv_bwd_weight", "conv_bwd_data")
 
 
+# HBM traffic per launch measured with rocprofv3 counters (FETCH_SIZE, WRITE_SIZE, each
+# scaled by what it reads for a plain device copy) for a kernel class on one workload; the
+# figure is used only while the kernel's sources hash to the value recorded with it.
+TRAFFIC_PROFILES = {
+    ("wgrad_igemm", 4, 16): ("profiles/wgrad_igemm_c4_b16_traffic.md",
+                             ("paper_2609_10632_amd/csrc/conv_wgrad.hip", "paper_2609_10632_amd/csrc/common.h")),
+}
+
+
+def committed_traffic(kernel_class, config_index, batch):
+    import hashlib
+
+    entry = TRAFFIC_PROFILES.get((kernel_class, config_index, batch))
+    if entry is None:
+        return None
+    here = os.path.dirname(os.path.abspath(__file__))
+    prof, sources = entry
+    try:
+        text = open(os.path.join(here, prof)).read()
+        h = hashlib.sha256()
+        for src in sources:
+            with open(os.path.join(here, src), "rb") as f:
+                h.update(f.read())
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines() if line.startswith(("kernel_source_sha256", "traffic")))
+    if fields.get("kernel_source_sha256", "").strip() != h.hexdigest():
+        return None  # the kernel changed since the counters were taken
+    return float(fields["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(wl, threads_hint):
     """The fp64 oracle on a bounded sample of the same workload: every layer at batch 1,
     forward + BN/SiLU forward and backward + data and weight gradients."""
@@ -280,8 +311,9 @@ def main():
         dom = max((c for c in conv_cls if c in per_cls), key=lambda c: per_cls[c][0])
         dom_ms, dom_launches = per_cls[dom]
         achieved = pass_flops / (dom_ms / 1e3) / 1e12
+        traffic = committed_traffic(dom, wl.index, wl.n) if not args.layers else None
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom,
+                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": dom,
                     "launches_per_step": dom_launches, "avg_launch_ms": round(dom_ms / max(dom_launches, 1), 4),
                     "flops_per_step": pass_flops}
     conv_ms = sum(per_cls[c][0] for c in per_cls if c not in

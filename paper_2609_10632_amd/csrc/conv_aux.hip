@@ -90,29 +90,30 @@ namespace {
 
 struct PhaseTable {
   int nphase;
-  int first[16];     // element offset of each phase's matrix inside wt
-  int row_first[16]; // first destination row of each phase (rows are (c, tap) pairs)
+  int first[16];       // element offset of each phase's matrix inside wt
+  int item_first[16];  // first work item of each phase (items are (tap, 8 o's, c) triples)
   int count[16];
   int r[16][kMaxTaps], s[16][kMaxTaps];
 };
 
 // One thread writes 8 consecutive output channels (16 bytes) of one destination row
 // (phase f, channel c, tap t): wt[f][c][t][o..o+7] = w[o..o+7][r][s][c], zero for the
-// padding channels c >= ci.
-__global__ void dgrad_weights_kernel(const bf16_t* w, uint4* wt, int co, int kh, int kw, int ci, int cpad, int nchunks,
+// padding channels c >= ci.  Consecutive threads take consecutive c, so each of the 8
+// source reads is coalesced across the wave.
+__global__ void dgrad_weights_kernel(const bf16_t* w, uint4* wt, int co, int kh, int kw, int ci, int cpad, int nitems,
                                      PhaseTable tab) {
-  const int cpr = co / 8;  // chunks per row
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < nchunks; i += gridDim.x * blockDim.x) {
-    const int row = i / cpr, oc = i - row * cpr;
+  const int cpr = co / 8;  // 8-channel chunks per destination row
+  const int64_t ostride = (int64_t)kh * kw * ci;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < nitems; i += gridDim.x * blockDim.x) {
     int f = 0;
-    while (f + 1 < tab.nphase && row >= tab.row_first[f + 1]) ++f;
+    while (f + 1 < tab.nphase && i >= tab.item_first[f + 1]) ++f;
     const int T = tab.count[f];
-    const int rl = row - tab.row_first[f];
-    const int c = rl / T, t = rl - (rl / T) * T;
+    const int j = i - tab.item_first[f];
+    const int c = j % cpad, q = j / cpad;
+    const int oc = q % cpr, t = q / cpr;
     uint32_t h[8];
     if (c < ci) {
-      const bf16_t* src = w + ((int64_t)(oc * 8) * kh * kw + (int64_t)tab.r[f][t] * kw + tab.s[f][t]) * ci + c;
-      const int64_t ostride = (int64_t)kh * kw * ci;
+      const bf16_t* src = w + (int64_t)(oc * 8) * ostride + ((int64_t)tab.r[f][t] * kw + tab.s[f][t]) * ci + c;
 #pragma unroll
       for (int e = 0; e < 8; ++e) h[e] = src[e * ostride];
     } else {
@@ -130,24 +131,24 @@ hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int
                                 const int* phase_first, const PhaseTaps* phases, int nphase, hipStream_t s) {
   PhaseTable tab;
   tab.nphase = nphase;
-  int rows = 0;
+  int items = 0;
   for (int f = 0; f < nphase; ++f) {
     tab.first[f] = phase_first[f];
-    tab.row_first[f] = rows;
+    tab.item_first[f] = items;
     tab.count[f] = phases[f].count;
-    rows += cpad * phases[f].count;
+    items += cpad * phases[f].count * (co / 8);
     for (int t = 0; t < phases[f].count; ++t) {
       tab.r[f][t] = phases[f].r[t];
       tab.s[f][t] = phases[f].s[t];
     }
   }
-  const int nchunks = rows * (co / 8);
-  int blocks = (nchunks + 255) / 256;
+  const int nitems = items;
+  int blocks = (nitems + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
   trace_begin(KC_DGRAD_WEIGHTS, s);
   hipLaunchKernelGGL(dgrad_weights_kernel, dim3(blocks), dim3(256), 0, s, w, reinterpret_cast<uint4*>(wt), co, kh, kw,
-                     ci, cpad, nchunks, tab);
+                     ci, cpad, nitems, tab);
   trace_end(KC_DGRAD_WEIGHTS, s);
   return hipGetLastError();
 }
