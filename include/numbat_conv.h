@@ -75,7 +75,9 @@ typedef enum {
 } numbat_op;
 
 /* One 2-D convolution (dilation 1, one group).  Output size
- * ho = (h + 2*pad_h - kh) / stride_h + 1, wo likewise. */
+ * ho = (h + 2*pad_h - kh) / stride_h + 1, wo likewise.  Provided: kernel sides kh, kw <= 5,
+ * strides <= 4, padding smaller than the kernel, c_out a multiple of 8, c_in a multiple of
+ * 8 or below 8; anything else returns NUMBAT_ERR_UNSUPPORTED. */
 typedef struct {
   uint32_t struct_size;   /* = sizeof(numbat_conv_problem) */
   int32_t n, h, w;        /* batch and input spatial size */

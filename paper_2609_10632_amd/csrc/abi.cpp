@@ -123,8 +123,8 @@ numbat_status check_conv(const numbat_conv_problem* p, ConvDesc* d) {
                 p->pad_w, p->kh, p->kw);
   const int64_t hp = (int64_t)p->h + 2 * p->pad_h - p->kh, wp = (int64_t)p->w + 2 * p->pad_w - p->kw;
   if (hp < 0 || wp < 0) return fail(NUMBAT_ERR_BAD_DESC, "kernel larger than the padded input");
-  if ((int64_t)p->kh * p->kw > kMaxTaps)
-    return fail(NUMBAT_ERR_UNSUPPORTED, "kh*kw = %d exceeds %d taps", p->kh * p->kw, kMaxTaps);
+  if (p->kh > 5 || p->kw > 5)
+    return fail(NUMBAT_ERR_UNSUPPORTED, "kernel sides above 5 are not provided (%d x %d)", p->kh, p->kw);
   if (p->stride_h > 4 || p->stride_w > 4) return fail(NUMBAT_ERR_UNSUPPORTED, "strides above 4 are not provided");
   if (p->c_out % 8 != 0) return fail(NUMBAT_ERR_UNSUPPORTED, "c_out = %d is not a multiple of 8", p->c_out);
   if (p->c_in % 8 != 0 && p->c_in > 8)

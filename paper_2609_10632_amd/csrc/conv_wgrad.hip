@@ -67,6 +67,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
 
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BMO][LROW];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNK][LROW];
+  __shared__ __attribute__((aligned(16))) uint2 s_pix[2][BR];  // per pixel of a step: (byte offset, tap mask)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
@@ -89,14 +90,19 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
   // group and cover the step's 8 pixel blocks: a load instruction reads 8 pixels x 128
   // contiguous bytes, and the transposed LDS rows they write are 128 contiguous bytes
   // (lanes of the next group land in the other half of the banks).
-  const bool isx = tid >= UDY;  // wave-uniform
+  // the role is the same for the whole wave (UDY is a multiple of 64); deriving it from the
+  // wave index read into a scalar register lets the compiler keep the buffer descriptor
+  // selected by it in scalar registers
+  const bool isx = __builtin_amdgcn_readfirstlane(wave) * 64 >= UDY;
+  const uint32_t xsel = 0u - (uint32_t)isx;  // all ones for the x role
   const bool has = tid < UDY + UX;
   const int v = isx ? tid - UDY : tid;
   const int grp = v >> 3;
   const int pb = v & 7;
   bool uok;
-  uint32_t ucol;  // byte offset of the unit's 8 channels within a pixel
-  int udh = 0, udw = 0;
+  uint32_t ucol;  // dy: byte offset of the 8 channels; x: tap offset + channel offset (bytes)
+  int utap = 31;  // x: tap of the unit's k group (31: none; bit 31 of a tap mask is clear)
+  const uint32_t dpix2 = (uint32_t)a.dy_pix * 2, xpix2 = (uint32_t)a.x_pix * 2;
   if (!isx) {
     const int o = o0 + grp * 8;
     uok = has && o < a.co;
@@ -105,50 +111,73 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
     const int k = k0 + grp * 8;
     uok = has && k < a.ktot;
     const int tap = k / a.ci, c = k - tap * a.ci;
-    ucol = (uint32_t)c * 2;
-    udh = tap / a.kw - a.ph;
-    udw = tap % a.kw - a.pw;
+    const int r = tap / a.kw, q = tap - r * a.kw;
+    ucol = (uint32_t)(r * a.w + q) * xpix2 + (uint32_t)c * 2;
+    utap = uok ? tap : 31;
   }
   const int howo = a.ho * a.wo;
-  const uint32_t dpix2 = (uint32_t)a.dy_pix * 2, xpix2 = (uint32_t)a.x_pix * 2;
+  const int halo_px = a.ph * a.w + a.pw;  // the x gather base sits this many pixels before an image
 
+  // x gather base of step st: the image of its first pixel, moved back by the halo
+  auto step_img = [&](int st) __attribute__((always_inline)) -> uint32_t {
+    const int64_t p0 = rbeg + (int64_t)st * BR;
+    return p0 < a.m ? fdiv((uint32_t)p0, div_howo) : 0u;
+  };
+  // The 64 pixels of a step are decoded once, by threads 0..63, into table slot st & 1:
+  // the byte offset of the pixel's top-left tap from the step's gather base and the mask
+  // of its taps inside the image (0 past the split)
+  auto decode = [&](int st) __attribute__((always_inline)) {
+    if (tid >= BR) return;
+    const int64_t px = rbeg + (int64_t)st * BR + tid;
+    uint2 e = make_uint2(0u, 0u);
+    if (px < rend) {
+      const uint32_t img_s = step_img(st);
+      const uint32_t img = fdiv((uint32_t)px, div_howo);
+      const uint32_t rem = (uint32_t)px - img * (uint32_t)howo;
+      const uint32_t p = fdiv(rem, div_wo), q = rem - p * (uint32_t)a.wo;
+      const int ih0 = (int)p * a.sh - a.ph, iw0 = (int)q * a.sw - a.pw;
+      e.x = (uint32_t)((((int)(img - img_s) * a.h + ih0) * a.w + iw0 + halo_px)) * xpix2;
+      // kernel sides are at most 5 (25 taps): fixed-trip loops, so no loop sits inside
+      // the main loop (a loop there would make the load counters wait for everything)
+      uint32_t cols = 0;
+#pragma unroll
+      for (int j = 0; j < 5; ++j)
+        cols |= (j < a.kw && (unsigned)(iw0 + j) < (unsigned)a.w ? 1u : 0u) << j;
+      uint32_t mk = 0;
+#pragma unroll
+      for (int i = 0; i < 5; ++i)
+        mk |= (i < a.kh && (unsigned)(ih0 + i) < (unsigned)a.h ? cols : 0u) << (i * a.kw);
+      e.y = mk;
+    }
+    s_pix[st & 1][tid] = e;
+  };
+
+  // Every thread runs the same load code -- the dy and the x offset are both formed and
+  // the role selects one -- so the loads are never under divergent control flow and the
+  // compiler's load counters wait for exactly the ring slot being staged.
   auto load = [&](int st, u32x4 (&xr)[8]) __attribute__((always_inline)) {
     const int64_t p0 = rbeg + (int64_t)st * BR;  // first pixel of the step
-    if (!isx) {
-      const __amdgpu_buffer_rsrc_t r = wrsrc(a.dy + p0 * a.dy_pix);
+    const __amdgpu_buffer_rsrc_t r =
+        isx ? wrsrc(a.x + ((int64_t)step_img(st) * a.h * a.w - halo_px) * a.x_pix) : wrsrc(a.dy + p0 * a.dy_pix);
+    const uint4* tab = reinterpret_cast<const uint4*>(&s_pix[st & 1][pb * 8]);
+    // pixels of the step inside the split (a 32-bit scalar: a 64-bit per-lane compare
+    // here was turned into a branch around one load)
+    const int64_t left64 = rend - p0;
+    const int left = left64 <= 0 ? 0 : (left64 >= BR ? BR : (int)left64);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int pr = pb * 8 + j;
-        const bool ok = uok && p0 + pr < rend;
-        xr[j] = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (uint32_t)pr * dpix2 + ucol : kOobW, 0u, 0);
-      }
-    } else {
-      // gather base: the image of the step's first pixel; the unit's first pixel is
-      // found by division, the next seven by stepping the column
-      const uint32_t img_s = p0 < a.m ? fdiv((uint32_t)p0, div_howo) : 0u;
-      const __amdgpu_buffer_rsrc_t r = wrsrc(a.x + (int64_t)img_s * a.h * a.w * a.x_pix);
-      const int64_t pa = p0 + pb * 8;
-      uint32_t img = 0, p = 0, q = 0;
-      if (pa < a.m) {
-        img = fdiv((uint32_t)pa, div_howo);
-        const uint32_t rem = (uint32_t)pa - img * (uint32_t)howo;
-        p = fdiv(rem, div_wo);
-        q = rem - p * (uint32_t)a.wo;
-      }
-      int rel = (int)(img - img_s);
+    for (int j2 = 0; j2 < 4; ++j2) {
+      const uint4 e = tab[j2];  // two pixels
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int ih = (int)p * a.sh + udh, iw = (int)q * a.sw + udw;
-        const bool ok = uok && pa + j < rend && (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w;
-        const uint32_t off = (uint32_t)(((rel * a.h + ih) * a.w + iw)) * xpix2 + ucol;
-        xr[j] = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOobW, 0u, 0);
-        ++q;
-        const bool wq = q == (uint32_t)a.wo;
-        q = wq ? 0u : q;
-        p += wq ? 1u : 0u;
-        const bool wp = p == (uint32_t)a.ho;
-        p = wp ? 0u : p;
-        rel += wp ? 1 : 0;
+      for (int h = 0; h < 2; ++h) {
+        const int j = 2 * j2 + h;
+        const uint32_t base = h ? e.z : e.x, mask = h ? e.w : e.y;
+        // branch-free selects (bit masks): the compiler otherwise turns one of them into
+        // control flow around a load
+        const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)mask, utap, 1);
+        const uint32_t xo = (t & (base + ucol)) | (~t & kOobW);
+        const uint32_t d = 0u - (uint32_t)(uok && pb * 8 + j < left);
+        const uint32_t dofs = (d & ((uint32_t)(pb * 8 + j) * dpix2 + ucol)) | (~d & kOobW);
+        xr[j] = __builtin_amdgcn_raw_buffer_load_b128(r, (xsel & xo) | (~xsel & dofs), 0u, 0);
       }
     }
   };
@@ -191,24 +220,33 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
     }
   };
 
-  // step kt: stage step kt+1 in LDS, issue the loads of step kt+1+D, multiply step kt
+  // Step kt: stage step kt+1 in LDS, issue the loads of step kt+1+D (their pixels were
+  // decoded during step kt-1), decode the pixels of step kt+2+D, multiply step kt.  The
+  // barrier ending the step publishes both the staged tiles and the decoded pixels.
   u32x4 ring[D][8];
   auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
     constexpr int u = decltype(uc)::value;
     constexpr int nxt = (u + 1) % D;
+    compute(kt & 1);
     store((kt + 1) & 1, ring[nxt]);
     load(kt + 1 + D, ring[nxt]);
-    compute(kt & 1);
+    decode(kt + 2 + D);
     __syncthreads();
   };
   // prologue in the steady state's issue order (step 0 to LDS, steps 1..D in flight)
   if (nsteps > 0) {
+    decode(0);
+    __syncthreads();
     load(0, ring[0]);
     store(0, ring[0]);
-    if constexpr (D > 1) load(1, ring[1]);
-    if constexpr (D > 2) load(2, ring[2]);
-    if constexpr (D > 3) load(3, ring[3]);
-    load(D, ring[0]);
+    __syncthreads();  // step 0's table slot is reused by step 2
+#pragma unroll
+    for (int st = 1; st <= D; ++st) {
+      decode(st);
+      __syncthreads();
+      load(st, ring[st % D]);
+    }
+    decode(D + 1);
     __syncthreads();
   }
   int kb = 0;
@@ -255,7 +293,7 @@ hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
   trace_begin(KC_WGRAD, s);
-  hipLaunchKernelGGL((wgrad_kernel<TMO, 2>), grid, dim3(256), 0, s, a, dwo, dhw);
+  hipLaunchKernelGGL((wgrad_kernel<TMO, 3>), grid, dim3(256), 0, s, a, dwo, dhw);
   trace_end(KC_WGRAD, s);
   return hipGetLastError();
 }
@@ -317,8 +355,10 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   const int bmo = wgrad_bmo(co);
   const int tiles = (int)(((co + bmo - 1) / bmo) * ((ktot + BNK - 1) / BNK));
   const int64_t steps = (m + BR - 1) / BR;
-  int64_t splits = (512 + tiles - 1) / tiles;
-  // at least 16 steps per split, at most 256 splits, partials at most 64 MiB
+  // Two blocks fit per CU (LDS), 512 on the chip: as many splits as keep the grid within
+  // one such round (a few blocks past it would cost a whole second round); at least 16
+  // steps per split, at most 256 splits, partials at most 64 MiB
+  int64_t splits = tiles < 512 ? 512 / tiles : 1;
   const int64_t max_by_steps = steps / 16 > 0 ? steps / 16 : 1;
   if (splits > max_by_steps) splits = max_by_steps;
   if (splits > 256) splits = 256;
