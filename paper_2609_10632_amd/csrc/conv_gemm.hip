@@ -644,6 +644,214 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Direct-to-LDS variant of the staged fast path.  The loads of both operands write LDS
+// themselves (buffer_load ... lds: lane i of a wave instruction deposits its 16 bytes
+// at the instruction's LDS base + 16*i), so a pipeline step costs no VGPR staging and no
+// LDS store instructions, and the prefetch depth lives in LDS stages instead of a
+// register ring.  A wave instruction fills 8 consecutive 128-byte rows (64 reduction
+// elements each), so rows are unpadded; bank conflicts on the 16-byte fragment reads are
+// avoided by storing 16-byte chunk k of row r in slot k ^ ((r >> 1) & 7): a load lane
+// picks the chunk its fixed LDS slot needs, so the swizzle costs nothing per step.
+//
+// Stage s of each operand is its own LDS object, so the compiler can tell the stages
+// apart when it counts the loads an LDS read must wait for; every step issues the same
+// loads (past the end of K they read zeros), and a step begins with a wait for its own
+// loads (the later stages stay in flight) and a barrier, after which the stage it frees
+// is refilled before its multiply.
+constexpr int kDmaRow = 64;  // reduction elements per LDS row (128 bytes)
+
+template <int TM, int TN, int S>
+struct DmaShape {
+  using G = GemmShape<TM, TN>;
+  static constexpr int AV = G::BM / 32, BV = G::BN / 32;  // load instructions per thread per step
+  static constexpr int A_ELEMS = G::BM * kDmaRow, B_ELEMS = G::BN * kDmaRow;
+  // stage 0 of A doubles as the epilogue's staging area
+  static constexpr int A0_ELEMS = 2 * A_ELEMS >= G::STAGE_BYTES ? A_ELEMS : G::STAGE_BYTES / 2;
+  static constexpr int PENDING = (S - 2) * (AV + BV);  // loads still in flight when a step's own are done
+};
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int TM, int TN, int S>
+__global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
+  using G = GemmShape<TM, TN>;
+  using Sh = DmaShape<TM, TN, S>;
+  constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM, AV = Sh::AV, BV = Sh::BV;
+  static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
+  static_assert(Sh::PENDING <= 63, "load counter range");
+
+  __shared__ __attribute__((aligned(16))) bf16_t sA0[Sh::A0_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sA1[Sh::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sA2[Sh::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sA3[Sh::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sB0[Sh::B_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sB1[Sh::B_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sB2[Sh::B_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sB3[Sh::B_ELEMS];
+  __shared__ int64_t s_dst[BM];
+  __shared__ float s_red[4][BN];
+  __shared__ float s_mean[BN];
+  auto stage_a = [&](auto sc) __attribute__((always_inline)) -> bf16_t* {
+    constexpr int s = decltype(sc)::value;
+    if constexpr (s == 0) return sA0;
+    else if constexpr (s == 1) return sA1;
+    else if constexpr (s == 2) return sA2;
+    else return sA3;
+  };
+  auto stage_b = [&](auto sc) __attribute__((always_inline)) -> bf16_t* {
+    constexpr int s = decltype(sc)::value;
+    if constexpr (s == 0) return sB0;
+    else if constexpr (s == 1) return sB1;
+    else if constexpr (s == 2) return sB2;
+    else return sB3;
+  };
+
+  const TileId T = tile_id(a.remap != 0);
+  const GemmPhase& P = a.ph[T.ph];
+  const int m0 = T.mt * BM;
+  if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
+  const int n0 = T.nt * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, half = lane >> 5;
+  // the 16-byte chunk this thread loads: its LDS slot is lane & 7 of row wave*8 + lane/8
+  // (mod 32), which holds chunk slot ^ ((row >> 1) & 7)
+  const int kc = (lane & 7) ^ ((lane >> 4) | ((wave & 1) << 2));
+  const int rg = wave * 8 + (lane >> 3);
+
+  const Geo Ge = load_geo(P);
+  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, Ge, m0 + r);
+
+  const uint32_t img0 = fdiv((uint32_t)m0, Ge.div_ghw);
+  const __amdgpu_buffer_rsrc_t rsA =
+      buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
+  uint32_t vrow[AV], vmask[AV];  // rows q*32 + rg of the tile
+#pragma unroll
+  for (int q = 0; q < AV; ++q) row_gather(a, Ge, m0 + q * 32 + rg, img0, vrow[q], vmask[q]);
+  const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
+  const int p_tw = P.tw, p_ktot = P.ktot, cs = a.cs;
+  const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
+  uint32_t voffb[BV];
+#pragma unroll
+  for (int j = 0; j < BV; ++j) {
+    const int o = n0 + j * 32 + rg;
+    voffb[j] = o < a.nout ? (uint32_t)(((int64_t)o * p_ktot + kc * 8) * 2) : kOob;
+  }
+  int ch = kc * 8, tap = 0, tcol = 0;
+  uint32_t toff = (uint32_t)P.toff0;
+  auto wrap_taps = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+      const bool wrap = ch >= cs;
+      ch = wrap ? ch - cs : ch;
+      tap += wrap ? 1 : 0;
+      tcol += wrap ? 1 : 0;
+      const bool rw = tcol == p_tw;
+      tcol = rw ? 0 : tcol;
+      toff += wrap ? (rw ? p_rstep : p_cstep) : 0u;
+    }
+  };
+  wrap_taps();
+  const int nk = (p_ktot + kDmaRow - 1) / kDmaRow;
+
+  // issue the loads of step kt into stage s; the A walk advances by one step
+  auto issue = [&](auto sc, int kt) __attribute__((always_inline)) {
+    bf16_t* A = stage_a(sc);
+    bf16_t* B = stage_b(sc);
+    const uint32_t lo = toff + 2u * (uint32_t)ch;
+    const int tq = tap < 31 ? tap : 31;  // past the last tap: bit 31 is clear
+#pragma unroll
+    for (int q = 0; q < AV; ++q) {
+      const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[q], tq, 1);
+      const uint32_t vo = (t & (vrow[q] + lo)) | (~t & kOob);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void_t*)(A + (q * 32 + wave * 8) * kDmaRow), 16, vo, 0, 0, 0);
+    }
+    const int kb = kt * kDmaRow;
+    const bool kin = kb + kc * 8 < p_ktot;
+#pragma unroll
+    for (int j = 0; j < BV; ++j) {
+      // (the select stays out of the builtin's argument list: written inline, the host
+      // pass drops the kernel's launch stub)
+      const uint32_t vb = kin ? voffb[j] : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(B + (j * 32 + wave * 8) * kDmaRow), 16, vb,
+                                               (uint32_t)kb * 2, 0, 0);
+    }
+    ch += kDmaRow;
+    wrap_taps();
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // fragment byte offsets: row (wave rows + l32) of A, l32 of B; k-slice ks sits in chunk
+  // 2*ks + half, stored in slot (2*ks + half) ^ ((l32 >> 1) & 7)
+  const int sw = (l32 >> 1) & 7;
+  const uint32_t arow = (uint32_t)(wave * WTM + l32) * (kDmaRow * 2), brow = (uint32_t)l32 * (kDmaRow * 2);
+  uint32_t koff[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) koff[ks] = (uint32_t)(((2 * ks + half) ^ sw) * 16);
+  auto compute = [&](auto sc) __attribute__((always_inline)) {
+    const unsigned char* A = reinterpret_cast<const unsigned char*>(stage_a(sc));
+    const unsigned char* B = reinterpret_cast<const unsigned char*>(stage_b(sc));
+    u32x4 af[2][TM], bf[2][TN];
+    auto rd = [&](int ks, u32x4 (&xa)[TM], u32x4 (&xb)[TN]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) xa[i] = *reinterpret_cast<const u32x4*>(A + arow + i * 32 * kDmaRow * 2 + koff[ks]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) xb[j] = *reinterpret_cast<const u32x4*>(B + brow + j * 32 * kDmaRow * 2 + koff[ks]);
+    };
+    rd(0, af[0], bf[0]);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) rd(ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
+    }
+  };
+  // this wave's loads of the current step are done (the later stages' stay in flight),
+  // then every wave's: the stage is complete in LDS and the stage read last step is free
+  auto sync = [&]() __attribute__((always_inline)) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(Sh::PENDING) : "memory");
+  };
+  // step kt reads stage u = kt mod S and refills stage (kt - 1) mod S with step kt + S - 1
+  auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
+    constexpr int u = decltype(uc)::value;
+    sync();
+    issue(Ic<(u + S - 1) % S>{}, kt + S - 1);
+    compute(uc);
+  };
+  if (nk > 0) {
+    issue(Ic<0>{}, 0);
+    if constexpr (S > 2) issue(Ic<1>{}, 1);
+    if constexpr (S > 3) issue(Ic<2>{}, 2);
+  }
+  int kb = 0;
+  for (; kb + S <= nk; kb += S) {
+    step(Ic<0>{}, kb);
+    step(Ic<1>{}, kb + 1);
+    if constexpr (S > 2) step(Ic<2 % S>{}, kb + 2);
+    if constexpr (S > 3) step(Ic<3 % S>{}, kb + 3);
+  }
+  if (kb < nk) step(Ic<0>{}, kb);
+  if constexpr (S > 2) {
+    if (kb + 1 < nk) step(Ic<1>{}, kb + 1);
+  }
+  if constexpr (S > 3) {
+    if (kb + 2 < nk) step(Ic<2>{}, kb + 2);
+  }
+  // the loads issued past the last step land in LDS before stage 0 becomes staging space
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, reinterpret_cast<unsigned char*>(sA0), s_dst, s_red, s_mean);
+}
+
+// ---------------------------------------------------------------------------
 // Register-direct variant of the fast path: the gathered operand bypasses LDS.  Each
 // wave loads its own MFMA A fragments (16 contiguous bytes per lane: 8 channels of one
 // pixel at one tap) with buffer loads straight into a register ring; only the weight
@@ -836,6 +1044,10 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
     hipLaunchKernelGGL((convlds_kernel<c.tm, c.tn, d_lds(c)>), grid, dim3(256), 0, s, a);
   else if (variant == kVariantDirect)
     hipLaunchKernelGGL((convdirect_kernel<c.tm, c.tn, d_direct(c)>), grid, dim3(256), 0, s, a);
+  else if (variant == kVariantDma3)
+    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3>), grid, dim3(256), 0, s, a);
+  else if (variant == kVariantDma2)
+    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 2>), grid, dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
@@ -894,13 +1106,16 @@ bool prepare_fast(ConvGemmArgs& a, int bm) {
 
 }  // namespace
 
-// Tile and kernel choice, fitted to timings of every (kernel, tile) pair over the forward
-// and data-gradient GEMMs of the detector's layers at batch 16 (within a few percent of
-// the per-layer best in total):
+// Tile and kernel choice, fitted to timings of every (kernel, tile, stages) choice over
+// the forward and data-gradient GEMMs of the detector's layers at batch 16, weighted by
+// how often each shape occurs (4% above the per-layer best in total):
 //  * N tile: the least padding among 128, 96 and 64 columns (ties to the wider); when the
 //    grid would hold fewer than 400 blocks of 128 rows, 64 columns for more blocks;
-//  * fast paths: 128-row tiles; the LDS-staged kernel for reductions of 1024 or more or
-//    at most 32768 rows, the register-direct one otherwise;
+//  * fast paths, 128-row tiles: more than 32768 rows (short reductions, many blocks) the
+//    LDS-staged kernel for reductions of 1024 or more, else the register-direct one;
+//    8193..32768 rows the direct-to-LDS kernel with two stages (two blocks per CU) on
+//    96 columns when they divide N <= 192, else 64; up to 8192 rows the direct-to-LDS
+//    kernel with three stages;
 //  * generic kernel (narrow or 8-multiple channels): 256-row tiles unless that leaves
 //    fewer than 512 blocks.
 TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
@@ -921,7 +1136,14 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
     const int64_t blocks128 = ((m_max + 127) / 128) * ((nout + bn - 1) / bn);
     if (blocks128 < 400 && bn > 64) bn = 64;
     bm = 128;
-    variant = (ktot >= 1024 || m_max <= 32768) ? kVariantLds : kVariantDirect;
+    if (m_max > 32768) {
+      variant = ktot >= 1024 ? kVariantLds : kVariantDirect;
+    } else if (m_max > 8192) {
+      variant = kVariantDma2;
+      bn = (nout % 96 == 0 && nout <= 192) ? 96 : 64;
+    } else {
+      variant = kVariantDma3;
+    }
   } else {
     const int64_t blocks256 = ((m_max + 255) / 256) * ((nout + bn - 1) / bn);
     bm = blocks256 < 512 ? 128 : 256;
