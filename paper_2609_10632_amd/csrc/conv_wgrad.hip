@@ -2,16 +2,14 @@
 // the n*ho*wo output pixels and X[m][(tap, c)] is the input pixel that tap reads.
 //
 // In NHWC both operands are contiguous along o / k and strided along the reduction
-// dimension m, while an MFMA lane needs 8 consecutive reduction elements.  Each thread
-// therefore loads an 8-pixel x 8-channel unit (eight 16-byte buffer loads, 8 channels of
-// 8 consecutive pixels), transposes it in registers with byte permutes and writes eight
-// 16-byte rows of [channel][pixel] into LDS; the MFMAs (32x32x16) read both operands
-// from there.  Loads run a register ring several steps ahead of the multiply.  Buffer
-// loads answer padding taps, pixels past the split and channels past the tile with
-// zeros (offsets past the buffer range), so every step issues the same loads.  The
-// reduction over m is split into fixed contiguous ranges, one per blockIdx.z, whose fp32
-// partial sums are added afterwards in split order, so the result does not depend on
-// scheduling.
+// dimension m, while an MFMA lane needs 8 consecutive reduction elements.  The loads
+// write LDS directly in the tensors' own [pixel][channel] layout and the MFMA operands
+// are read out of LDS with transposing reads, so no transpose runs in registers (the
+// kernel below).  Buffer loads answer padding taps, pixels past the split and channels
+// past the tile with zeros (offsets past the buffer range), so every step issues the
+// same loads.  The reduction over m is split into fixed contiguous ranges, one per
+// blockIdx.z, whose fp32 partial sums are added afterwards in split order, so the result
+// does not depend on scheduling.
 #include <cstdlib>
 #include <type_traits>
 
@@ -25,7 +23,6 @@ template <int V>
 using Ic = std::integral_constant<int, V>;
 
 constexpr int BR = 64;           // reduction pixels per step
-constexpr int LROW = BR + 8;     // bf16 per LDS row (144 bytes: conflict-free fragment reads)
 constexpr int BNK = 128;         // k columns per tile
 constexpr uint32_t kOobW = 0x80000000u;
 constexpr int kRecW = 0x7ffffff0;
@@ -34,46 +31,78 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t wrsrc(const void* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, kRecW, 0x00020000);
 }
 
-__device__ __forceinline__ uint32_t lo_pair(uint32_t p0, uint32_t p1) {
-  return __builtin_amdgcn_perm(p1, p0, 0x05040100u);  // (p0.lo16, p1.lo16)
+// The loads write LDS themselves (buffer_load ... lds: lane i of a wave instruction
+// deposits its 16 bytes at the instruction's LDS base + 16*i) in the tensors' own
+// layout, [pixel][64 channels] sub-tiles of 128-byte rows, and the MFMA operands -- 8 consecutive pixels of one channel per lane -- come out of LDS
+// through transposing reads (ds_read_b64_tr_b16): within each 16-lane group, lane j
+// reads 4 channels of one pixel and lane i receives 4 pixels of channel i; two reads make
+// a fragment.  So a step costs no register transposes and no LDS store instructions.
+// The 16-byte chunk c of pixel row r sits in slot c ^ (4 * ((r >> 1) & 1)), which makes
+// the transposing reads of 32 lanes cover all 64 banks once; a load lane picks the chunk
+// its fixed slot needs.  Each stage is its own LDS object (exact load waits, as in the
+// convolution's direct-to-LDS kernel); a step begins with a wait for its own loads and a
+// barrier, refills the stage read last step, decodes the pixels of a later step and
+// multiplies.
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef unsigned v2u_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void wlds_void_t;
+typedef __attribute__((address_space(3))) v4s_t wlds_v4s_t;
+
+// An LDS read of one pixel-table entry that completes before it returns.  Written as
+// plain code, the compiler cannot tell the table from the stages the direct-to-LDS loads
+// are filling and waits for every load in flight before it; this read waits for LDS
+// only.
+__device__ __forceinline__ v2u_t table_read(const uint2* p) {
+  const uint32_t addr = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+  v2u_t r;
+  asm volatile("ds_read_b64 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(addr) : "memory");
+  return r;
 }
-__device__ __forceinline__ uint32_t hi_pair(uint32_t p0, uint32_t p1) {
-  return __builtin_amdgcn_perm(p1, p0, 0x07060302u);  // (p0.hi16, p1.hi16)
-}
 
-// in: P[j] = 8 channels of pixel j.  out: Q[ch] = 8 pixels of channel ch.
-__device__ __forceinline__ void transpose8x8(const u32x4 (&P)[8], u32x4 (&Q)[8]) {
-#pragma unroll
-  for (int ch = 0; ch < 8; ++ch) {
-    const int wi = ch >> 1;
-    u32x4 q;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t x0 = P[2 * k][wi], x1 = P[2 * k + 1][wi];
-      q[k] = (ch & 1) ? hi_pair(x0, x1) : lo_pair(x0, x1);
-    }
-    Q[ch] = q;
-  }
-}
+template <int TMO, int S>
+struct WgDmaShape {
+  static constexpr int BMO = 64 * TMO;
+  static constexpr int D_ELEMS = TMO * BR * 64;  // dy: TMO sub-tiles of [64 px][64 ch]
+  static constexpr int X_ELEMS = 2 * BR * 64;    // x: 2 sub-tiles of [64 px][64 k]
+  static constexpr int LOADS = 2 * TMO + 4;      // load instructions per thread per step
+  static constexpr int PENDING = (S - 2) * LOADS;
+};
 
-// Tile BMO = 64*TMO output channels x BNK = 128 k columns; 2 x 2 waves of
-// (32*TMO) x 64.  Threads [0, BMO) load dy units, [BMO, BMO + 128) x units.
-template <int TMO, int D>
-__global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo, FastDiv div_howo) {
-  constexpr int BMO = 64 * TMO;
-  constexpr int TM = TMO, TN = 2;
-  constexpr int UDY = BMO, UX = 128;
-  static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
+template <int TMO, int S>
+__global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div_wo, FastDiv div_howo) {
+  using Sh = WgDmaShape<TMO, S>;
+  constexpr int BMO = Sh::BMO, TM = TMO, TN = 2, LOADS = Sh::LOADS;
+  static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
+  static_assert(Sh::PENDING <= 63, "load counter range");
 
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BMO][LROW];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNK][LROW];
-  __shared__ __attribute__((aligned(16))) uint2 s_pix[2][BR];  // per pixel of a step: (byte offset, tap mask)
+  __shared__ __attribute__((aligned(16))) bf16_t sD0[Sh::D_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sD1[Sh::D_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sD2[Sh::D_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sD3[Sh::D_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sX0[Sh::X_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sX1[Sh::X_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sX2[Sh::X_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sX3[Sh::X_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint2 s_pix[2][BR];  // per pixel of a step: (x byte offset, tap mask)
+  auto stage_d = [&](auto sc) __attribute__((always_inline)) -> bf16_t* {
+    constexpr int s = decltype(sc)::value;
+    if constexpr (s == 0) return sD0;
+    else if constexpr (s == 1) return sD1;
+    else if constexpr (s == 2) return sD2;
+    else return sD3;
+  };
+  auto stage_x = [&](auto sc) __attribute__((always_inline)) -> bf16_t* {
+    constexpr int s = decltype(sc)::value;
+    if constexpr (s == 0) return sX0;
+    else if constexpr (s == 1) return sX1;
+    else if constexpr (s == 2) return sX2;
+    else return sX3;
+  };
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
-  const int l32 = lane & 31, half = lane >> 5;
-  // logical tile (o tile fastest, then k tile, then split): the blocks of one split read
-  // the same pixels and are kept on one XCD
+  const int half = lane >> 5;
   const uint32_t gx = gridDim.x, gy = gridDim.y;
   const uint32_t lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
   const uint32_t lg = a.remap ? xcd_remap(lin, gx * gy * gridDim.z) : lin;
@@ -85,47 +114,35 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
   if (rend > a.m) rend = a.m;
   const int nsteps = rend > rbeg ? (int)((rend - rbeg + BR - 1) / BR) : 0;
 
-  // this thread's unit: channel group grp (8 output channels, or 8 k columns of one tap)
-  // and pixel block pb (8 consecutive pixels of the step).  8 lanes share a channel
-  // group and cover the step's 8 pixel blocks: a load instruction reads 8 pixels x 128
-  // contiguous bytes, and the transposed LDS rows they write are 128 contiguous bytes
-  // (lanes of the next group land in the other half of the banks).
-  // the role is the same for the whole wave (UDY is a multiple of 64); deriving it from the
-  // wave index read into a scalar register lets the compiler keep the buffer descriptor
-  // selected by it in scalar registers
-  const bool isx = __builtin_amdgcn_readfirstlane(wave) * 64 >= UDY;
-  const uint32_t xsel = 0u - (uint32_t)isx;  // all ones for the x role
-  const bool has = tid < UDY + UX;
-  const int v = isx ? tid - UDY : tid;
-  const int grp = v >> 3;
-  const int pb = v & 7;
-  bool uok;
-  uint32_t ucol;  // dy: byte offset of the 8 channels; x: tap offset + channel offset (bytes)
-  int utap = 31;  // x: tap of the unit's k group (31: none; bit 31 of a tap mask is clear)
+  // Load instruction t of this wave fills rows 8*(wave + 4*(t & 1)) .. +8 of sub-tile t/2
+  // (dy sub-tiles first, then x): lane loads chunk ck of pixel row 8*rowblock + lane/8.
+  const int ck = (lane & 7) ^ (4 * ((lane >> 4) & 1));
+  const int prow = lane >> 3;  // pixel row within the 8-row block
   const uint32_t dpix2 = (uint32_t)a.dy_pix * 2, xpix2 = (uint32_t)a.x_pix * 2;
-  if (!isx) {
-    const int o = o0 + grp * 8;
-    uok = has && o < a.co;
-    ucol = (uint32_t)o * 2;
-  } else {
-    const int k = k0 + grp * 8;
-    uok = has && k < a.ktot;
+  uint32_t dcol[TMO];  // dy: byte offset of this lane's 8 channels in sub-tile h (kOobW past c_out)
+#pragma unroll
+  for (int h = 0; h < TMO; ++h) {
+    const int o = o0 + 64 * h + 8 * ck;
+    dcol[h] = o < a.co ? (uint32_t)o * 2 : kOobW;
+  }
+  uint32_t xcol[2];  // x: tap offset + channel offset (bytes) of this lane's 8 k columns
+  int xtap[2];       // their tap (31: past k_total; bit 31 of a tap mask is clear)
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int k = k0 + 64 * h + 8 * ck;
     const int tap = k / a.ci, c = k - tap * a.ci;
     const int r = tap / a.kw, q = tap - r * a.kw;
-    ucol = (uint32_t)(r * a.w + q) * xpix2 + (uint32_t)c * 2;
-    utap = uok ? tap : 31;
+    xcol[h] = (uint32_t)(r * a.w + q) * xpix2 + (uint32_t)c * 2;
+    xtap[h] = k < a.ktot ? tap : 31;
   }
   const int howo = a.ho * a.wo;
-  const int halo_px = a.ph * a.w + a.pw;  // the x gather base sits this many pixels before an image
+  const int halo_px = a.ph * a.w + a.pw;
 
-  // x gather base of step st: the image of its first pixel, moved back by the halo
   auto step_img = [&](int st) __attribute__((always_inline)) -> uint32_t {
     const int64_t p0 = rbeg + (int64_t)st * BR;
     return p0 < a.m ? fdiv((uint32_t)p0, div_howo) : 0u;
   };
-  // The 64 pixels of a step are decoded once, by threads 0..63, into table slot st & 1:
-  // the byte offset of the pixel's top-left tap from the step's gather base and the mask
-  // of its taps inside the image (0 past the split)
+  // the 64 pixels of a step, decoded once by threads 0..63 into table slot st & 1
   auto decode = [&](int st) __attribute__((always_inline)) {
     if (tid >= BR) return;
     const int64_t px = rbeg + (int64_t)st * BR + tid;
@@ -137,8 +154,6 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
       const uint32_t p = fdiv(rem, div_wo), q = rem - p * (uint32_t)a.wo;
       const int ih0 = (int)p * a.sh - a.ph, iw0 = (int)q * a.sw - a.pw;
       e.x = (uint32_t)((((int)(img - img_s) * a.h + ih0) * a.w + iw0 + halo_px)) * xpix2;
-      // kernel sides are at most 5 (25 taps): fixed-trip loops, so no loop sits inside
-      // the main loop (a loop there would make the load counters wait for everything)
       uint32_t cols = 0;
 #pragma unroll
       for (int j = 0; j < 5; ++j)
@@ -152,46 +167,33 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
     s_pix[st & 1][tid] = e;
   };
 
-  // Every thread runs the same load code -- the dy and the x offset are both formed and
-  // the role selects one -- so the loads are never under divergent control flow and the
-  // compiler's load counters wait for exactly the ring slot being staged.
-  auto load = [&](int st, u32x4 (&xr)[8]) __attribute__((always_inline)) {
-    const int64_t p0 = rbeg + (int64_t)st * BR;  // first pixel of the step
-    const __amdgpu_buffer_rsrc_t r =
-        isx ? wrsrc(a.x + ((int64_t)step_img(st) * a.h * a.w - halo_px) * a.x_pix) : wrsrc(a.dy + p0 * a.dy_pix);
-    const uint4* tab = reinterpret_cast<const uint4*>(&s_pix[st & 1][pb * 8]);
-    // pixels of the step inside the split (a 32-bit scalar: a 64-bit per-lane compare
-    // here was turned into a branch around one load)
+  // issue the loads of step st into stage s
+  auto issue = [&](auto sc, int st) __attribute__((always_inline)) {
+    bf16_t* D = stage_d(sc);
+    bf16_t* X = stage_x(sc);
+    const int64_t p0 = rbeg + (int64_t)st * BR;
+    const __amdgpu_buffer_rsrc_t rx = wrsrc(a.x + ((int64_t)step_img(st) * a.h * a.w - halo_px) * a.x_pix);
+    const __amdgpu_buffer_rsrc_t rd = wrsrc(a.dy + p0 * a.dy_pix);
     const int64_t left64 = rend - p0;
     const int left = left64 <= 0 ? 0 : (left64 >= BR ? BR : (int)left64);
+    const v2u_t e0 = table_read(&s_pix[st & 1][wave * 8 + prow]);
+    const v2u_t e1 = table_read(&s_pix[st & 1][(wave + 4) * 8 + prow]);
 #pragma unroll
-    for (int j2 = 0; j2 < 4; ++j2) {
-      const uint4 e = tab[j2];  // two pixels
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int j = 2 * j2 + h;
-        const uint32_t base = h ? e.z : e.x, mask = h ? e.w : e.y;
-        // branch-free selects (bit masks): the compiler otherwise turns one of them into
-        // control flow around a load
-        const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)mask, utap, 1);
-        const uint32_t xo = (t & (base + ucol)) | (~t & kOobW);
-        const uint32_t d = 0u - (uint32_t)(uok && pb * 8 + j < left);
-        const uint32_t dofs = (d & ((uint32_t)(pb * 8 + j) * dpix2 + ucol)) | (~d & kOobW);
-        xr[j] = __builtin_amdgcn_raw_buffer_load_b128(r, (xsel & xo) | (~xsel & dofs), 0u, 0);
+    for (int t = 0; t < LOADS; ++t) {
+      const int rb = wave + 4 * (t & 1);  // row block
+      const int px = rb * 8 + prow;       // pixel of the step
+      if (t < 2 * TMO) {
+        const int h = t >> 1;
+        const uint32_t ok = 0u - (uint32_t)(px < left);
+        const uint32_t vo = (ok & ((uint32_t)px * dpix2 + dcol[h])) | (~ok & kOobW);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (wlds_void_t*)(D + h * BR * 64 + rb * 8 * 64), 16, vo, 0, 0, 0);
+      } else {
+        const int h = (t - 2 * TMO) >> 1;
+        const v2u_t e = (t & 1) ? e1 : e0;
+        const uint32_t tb = (uint32_t)__builtin_amdgcn_sbfe((int)e.y, xtap[h], 1);
+        const uint32_t vo = (tb & (e.x + xcol[h])) | (~tb & kOobW);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (wlds_void_t*)(X + h * BR * 64 + rb * 8 * 64), 16, vo, 0, 0, 0);
       }
-    }
-  };
-  auto store = [&](int buf, const u32x4 (&xr)[8]) __attribute__((always_inline)) {
-    if (!has) return;
-    u32x4 Q[8];
-    transpose8x8(xr, Q);
-    const int col = pb * 8;
-    if (!isx) {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) *reinterpret_cast<u32x4*>(&As[buf][grp * 8 + c][col]) = Q[c];
-    } else {
-#pragma unroll
-      for (int c = 0; c < 8; ++c) *reinterpret_cast<u32x4*>(&Bs[buf][grp * 8 + c][col]) = Q[c];
     }
   };
 
@@ -203,73 +205,96 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  auto compute = [&](int buf) __attribute__((always_inline)) {
+  // transposing-read addresses: lane j of a 16-lane group reads 4 channels (8 bytes) of
+  // pixel row 4*rd + (j / 4) of the slice's half; its 32-channel block jb sits in chunks
+  // 4*jb + 2*((lane >> 4) & 1) + ((lane >> 1) & 1), swizzled by the row
+  const uint32_t rbase = (uint32_t)((8 * half + ((lane & 15) >> 2)) * 128 + (lane & 1) * 8);
+  const uint32_t slot0 = (uint32_t)((2 * ((lane >> 4) & 1) + ((lane >> 1) & 1)) ^ (4 * ((lane >> 3) & 1)));
+  const uint32_t aoff[2] = {rbase + slot0 * 16, rbase + (slot0 ^ 4u) * 16};
+  auto frag = [&](const unsigned char* T, int sub, int jb, int ks) __attribute__((always_inline)) -> u32x4 {
+    const unsigned char* p = T + sub * BR * 128 + aoff[jb] + ks * 16 * 128;
+    const v4s_t r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wlds_v4s_t*)p);
+    const v4s_t r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wlds_v4s_t*)(p + 4 * 128));
+    const v2u_t lo = __builtin_bit_cast(v2u_t, r0), hi = __builtin_bit_cast(v2u_t, r1);
+    u32x4 f;
+    f[0] = lo.x;
+    f[1] = lo.y;
+    f[2] = hi.x;
+    f[3] = hi.y;
+    return f;
+  };
+  auto compute = [&](auto sc) __attribute__((always_inline)) {
+    const unsigned char* D = reinterpret_cast<const unsigned char*>(stage_d(sc));
+    const unsigned char* X = reinterpret_cast<const unsigned char*>(stage_x(sc));
 #pragma unroll
     for (int ks = 0; ks < BR / 16; ++ks) {
       u32x4 af[TM], bf[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const u32x4*>(&As[buf][wm * 32 * TM + i * 32 + l32][ks * 16 + half * 8]);
+      for (int i = 0; i < TM; ++i) {
+        const int ol = wm * 32 * TM + i * 32;  // first output channel of the fragment
+        af[i] = frag(D, ol >> 6, (ol >> 5) & 1, ks);
+      }
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bf[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][wn * 64 + j * 32 + l32][ks * 16 + half * 8]);
+      for (int j = 0; j < TN; ++j) bf[j] = frag(X, wn, j, ks);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
     }
   };
-
-  // Step kt: stage step kt+1 in LDS, issue the loads of step kt+1+D (their pixels were
-  // decoded during step kt-1), decode the pixels of step kt+2+D, multiply step kt.  The
-  // barrier ending the step publishes both the staged tiles and the decoded pixels.
-  u32x4 ring[D][8];
+  auto sync = [&]() __attribute__((always_inline)) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(Sh::PENDING) : "memory");
+  };
+  // step kt reads stage u = kt mod S, refills stage (kt - 1) mod S with step kt + S - 1
+  // (pixels decoded last step) and decodes step kt + S
   auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
     constexpr int u = decltype(uc)::value;
-    constexpr int nxt = (u + 1) % D;
-    compute(kt & 1);
-    store((kt + 1) & 1, ring[nxt]);
-    load(kt + 1 + D, ring[nxt]);
-    decode(kt + 2 + D);
-    __syncthreads();
+    sync();
+    issue(Ic<(u + S - 1) % S>{}, kt + S - 1);
+    decode(kt + S);
+    compute(uc);
   };
-  // prologue in the steady state's issue order (step 0 to LDS, steps 1..D in flight)
+  // prologue: steps 0..S-2 in flight (a plain barrier: the decoded table is LDS data, and
+  // the loads already issued need not land yet)
+  auto table_barrier = [&]() __attribute__((always_inline)) {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
   if (nsteps > 0) {
     decode(0);
-    __syncthreads();
-    load(0, ring[0]);
-    store(0, ring[0]);
-    __syncthreads();  // step 0's table slot is reused by step 2
-#pragma unroll
-    for (int st = 1; st <= D; ++st) {
-      decode(st);
-      __syncthreads();
-      load(st, ring[st % D]);
+    table_barrier();
+    issue(Ic<0>{}, 0);
+    decode(1);
+    if constexpr (S > 2) {
+      table_barrier();
+      issue(Ic<1>{}, 1);
+      decode(2);
     }
-    decode(D + 1);
-    __syncthreads();
+    if constexpr (S > 3) {
+      table_barrier();
+      issue(Ic<2>{}, 2);
+      decode(3);
+    }
   }
   int kb = 0;
-  for (; kb + D <= nsteps; kb += D) {
+  for (; kb + S <= nsteps; kb += S) {
     step(Ic<0>{}, kb);
-    if constexpr (D > 1) step(Ic<1 % D>{}, kb + 1);
-    if constexpr (D > 2) step(Ic<2 % D>{}, kb + 2);
-    if constexpr (D > 3) step(Ic<3 % D>{}, kb + 3);
+    step(Ic<1>{}, kb + 1);
+    if constexpr (S > 2) step(Ic<2 % S>{}, kb + 2);
+    if constexpr (S > 3) step(Ic<3 % S>{}, kb + 3);
   }
-  if constexpr (D > 1) {
-    if (kb < nsteps) step(Ic<0>{}, kb);
+  if (kb < nsteps) step(Ic<0>{}, kb);
+  if constexpr (S > 2) {
+    if (kb + 1 < nsteps) step(Ic<1>{}, kb + 1);
   }
-  if constexpr (D > 2) {
-    if (kb + 1 < nsteps) step(Ic<1 % D>{}, kb + 1);
+  if constexpr (S > 3) {
+    if (kb + 2 < nsteps) step(Ic<2>{}, kb + 2);
   }
-  if constexpr (D > 3) {
-    if (kb + 2 < nsteps) step(Ic<2 % D>{}, kb + 2);
-  }
+  // loads issued past the last step must land before the block ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-  // epilogue: accumulator register r of a lane is output channel row 8*(r/4) +
-  // 4*(lane/32) + (r%4) of its 32-row block, k column lane%32
   float* out = a.out + (a.splits > 1 ? (int64_t)bz * a.co * a.ktot : 0);
   const bool acc_in = a.splits == 1 && a.accumulate;
+  const int l32 = lane & 31;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -285,17 +310,6 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, FastDiv div_wo,
         *p = acc_in ? *p + val : val;
       }
     }
-}
-
-template <int TMO>
-hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
-  constexpr int BMO = 64 * TMO;
-  dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
-  const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
-  trace_begin(KC_WGRAD, s);
-  hipLaunchKernelGGL((wgrad_kernel<TMO, 3>), grid, dim3(256), 0, s, a, dwo, dhw);
-  trace_end(KC_WGRAD, s);
-  return hipGetLastError();
 }
 
 // dw = [dw +] sum over splits, four consecutive outputs per thread.  The splits are cut
@@ -371,13 +385,36 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   return (int)(splits < 1 ? 1 : splits);
 }
 
+namespace {
+// two LDS stages: two blocks per CU for 128-channel tiles, which measured faster on every
+// layer of the detector than one block with three stages
+template <int TMO>
+hipError_t launch_w(const WgradArgs& a, int stages, hipStream_t s) {
+  constexpr int BMO = 64 * TMO;
+  dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
+  const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
+  trace_begin(KC_WGRAD, s);
+#ifdef NUMBAT_TUNING
+  if (stages == 3)
+    hipLaunchKernelGGL((wgrad_dma_kernel<TMO, 3>), grid, dim3(256), 0, s, a, dwo, dhw);
+  else
+#endif
+    hipLaunchKernelGGL((wgrad_dma_kernel<TMO, 2>), grid, dim3(256), 0, s, a, dwo, dhw);
+  (void)stages;
+  trace_end(KC_WGRAD, s);
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t wgrad_launch(const WgradArgs& args, hipStream_t s) {
   WgradArgs a = args;
   a.remap = 0;
+  int stages = 2;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_REMAP_WG")) a.remap = atoi(e);
+  if (const char* e = getenv("NUMBAT_WG_STAGES")) stages = atoi(e);
 #endif
-  return wgrad_bmo(a.co) == 64 ? launch_w<1>(a, s) : launch_w<2>(a, s);
+  return wgrad_bmo(a.co) == 64 ? launch_w<1>(a, stages, s) : launch_w<2>(a, stages, s);
 }
 
 hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
