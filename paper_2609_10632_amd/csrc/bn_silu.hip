@@ -102,7 +102,10 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
                                                           bf16_t* out, float* save_mean, float* save_rstd,
                                                           float* run_mean, float* run_var, int64_t rows_per_block) {
   const int t = threadIdx.x;
-  if (blockIdx.x == 0) {
+  // the last block only publishes the saved statistics and updates the running ones, in
+  // parallel with the row blocks (done by a row block, it would lengthen that block by a
+  // round trip to memory)
+  if (blockIdx.x == gridDim.x - 1) {
     for (int ch = t; ch < a.c; ch += kThreads) {
       const float mu = mean_var[ch], var = mean_var[a.c + ch];
       save_mean[ch] = mu;
@@ -113,6 +116,7 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
         run_var[ch] = (1.0f - mo) * run_var[ch] + mo * (float)((double)var * (double)a.m / (double)(a.m - 1));
       }
     }
+    return;
   }
   const RowLayout L = row_layout(a.c);
   if (t >= L.active) return;
@@ -184,10 +188,11 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
       be[e] = beta[cb + e];
     }
     const int64_t st = L.rows_per_iter;
-    for (int64_t r = r0 + rr; r < r1; r += 4 * st) {
-      uint4 gv[4], yv[4];
+    // eight rows in flight: with the block count bn_reduce_blocks picks, one round
+    for (int64_t r = r0 + rr; r < r1; r += 8 * st) {
+      uint4 gv[8], yv[8];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 8; ++j) {
         const int64_t rj = r + j * st;
         if (rj < r1) {
           gv[j] = *reinterpret_cast<const uint4*>(g + rj * a.a_pix + cb);
@@ -195,7 +200,7 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
         }
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 8; ++j) {
         if (r + j * st >= r1) continue;
         float gy[8], yy[8];
         unpack8(gv[j], gy);
@@ -388,7 +393,7 @@ hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var
   int64_t rpb = 0;
   const int nb = apply_blocks(a.m, a.c, &rpb);
   trace_begin(KC_BN_FWD, s);
-  hipLaunchKernelGGL(bn_fwd_kernel, dim3(nb), dim3(kThreads), 0, s, a, y, mean_var, gamma, beta, res, out, save_mean,
+  hipLaunchKernelGGL(bn_fwd_kernel, dim3(nb + 1), dim3(kThreads), 0, s, a, y, mean_var, gamma, beta, res, out, save_mean,
                      save_rstd, run_mean, run_var, rpb);
   trace_end(KC_BN_FWD, s);
   return hipGetLastError();

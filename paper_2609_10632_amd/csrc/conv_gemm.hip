@@ -648,36 +648,49 @@ __global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
 // themselves (buffer_load ... lds: lane i of a wave instruction deposits its 16 bytes
 // at the instruction's LDS base + 16*i), so a pipeline step costs no VGPR staging and no
 // LDS store instructions, and the prefetch depth lives in LDS stages instead of a
-// register ring.  A wave instruction fills 8 consecutive 128-byte rows (64 reduction
-// elements each), so rows are unpadded; bank conflicts on the 16-byte fragment reads are
-// avoided by storing 16-byte chunk k of row r in slot k ^ ((r >> 1) & 7): a load lane
-// picks the chunk its fixed LDS slot needs, so the swizzle costs nothing per step.
+// register ring.  A stage holds BK reduction elements (64 or 32) of every row, in
+// unpadded rows of 2*BK bytes; a wave instruction fills 1 KiB of consecutive rows.
+// Bank conflicts on the 16-byte fragment reads (16 lanes, 16 rows, one 256-byte bank
+// window) are avoided by storing 16-byte chunk k of row r in slot k ^ ((r / W) % C),
+// with W rows per bank window and C chunks per row: rows sharing a window differ in
+// their byte offset, rows of different windows in their slot.  A load lane picks the
+// chunk its fixed LDS slot needs, so the swizzle costs nothing per step.
 //
 // Stage s of each operand is its own LDS object, so the compiler can tell the stages
 // apart when it counts the loads an LDS read must wait for; every step issues the same
 // loads (past the end of K they read zeros), and a step begins with a wait for its own
 // loads (the later stages stay in flight) and a barrier, after which the stage it frees
 // is refilled before its multiply.
-constexpr int kDmaRow = 64;  // reduction elements per LDS row (128 bytes)
-
-template <int TM, int TN, int S>
+template <int TM, int TN, int S, int BK>
 struct DmaShape {
   using G = GemmShape<TM, TN>;
-  static constexpr int AV = G::BM / 32, BV = G::BN / 32;  // load instructions per thread per step
-  static constexpr int A_ELEMS = G::BM * kDmaRow, B_ELEMS = G::BN * kDmaRow;
+  static constexpr int ROWB = 2 * BK;               // bytes per LDS row
+  static constexpr int CPR = BK / 8;                // 16-byte chunks per row
+  static constexpr int RPI = 1024 / ROWB;           // rows per wave load instruction
+  static constexpr int WIN = 256 / ROWB;            // rows per 256-byte bank window
+  static constexpr int AI = G::BM / RPI / 4;        // A load instructions per wave per step
+  static constexpr int BI = (G::BN + RPI - 1) / RPI;     // B load instructions per step (all waves)
+  static constexpr int BI_MIN = BI / 4;                  // ... issued by every wave
+  static constexpr int BI_MAX = (BI + 3) / 4;            // ... issued by the first waves
+  static constexpr int A_ELEMS = G::BM * BK, B_ELEMS = BI * RPI * BK;
   // stage 0 of A doubles as the epilogue's staging area
   static constexpr int A0_ELEMS = 2 * A_ELEMS >= G::STAGE_BYTES ? A_ELEMS : G::STAGE_BYTES / 2;
-  static constexpr int PENDING = (S - 2) * (AV + BV);  // loads still in flight when a step's own are done
+  // loads still in flight when a step's own are done (every wave issues at least
+  // AI + BI_MIN loads per step; a wave that issues more waits a little longer)
+  static constexpr int PENDING = (S - 2) * (AI + BI_MIN);
+  static_assert(G::BM % (4 * RPI) == 0, "A rows per step split evenly over the waves");
 };
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-template <int TM, int TN, int S>
+template <int TM, int TN, int S, int BK>
 __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   using G = GemmShape<TM, TN>;
-  using Sh = DmaShape<TM, TN, S>;
-  constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM, AV = Sh::AV, BV = Sh::BV;
+  using Sh = DmaShape<TM, TN, S, BK>;
+  constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM;
+  constexpr int AI = Sh::AI, BI = Sh::BI, BI_MAX = Sh::BI_MAX, RPI = Sh::RPI, CPR = Sh::CPR, WIN = Sh::WIN;
   static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
+  static_assert(BK == 32 || BK == 64, "stage depth");
   static_assert(Sh::PENDING <= 63, "load counter range");
 
   __shared__ __attribute__((aligned(16))) bf16_t sA0[Sh::A0_ELEMS];
@@ -714,10 +727,11 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
-  // the 16-byte chunk this thread loads: its LDS slot is lane & 7 of row wave*8 + lane/8
-  // (mod 32), which holds chunk slot ^ ((row >> 1) & 7)
-  const int kc = (lane & 7) ^ ((lane >> 4) | ((wave & 1) << 2));
-  const int rg = wave * 8 + (lane >> 3);
+  // Load instruction q of this wave fills rows (4*q + wave)*RPI .. +RPI; the lane's LDS
+  // slot is lane % CPR of row lane / CPR in it, which holds chunk slot ^ ((row / WIN) % CPR)
+  // (the same for every q)
+  const int lrow = lane / CPR;
+  const int kc = (lane % CPR) ^ (((wave * RPI + lrow) / WIN) % CPR);
 
   const Geo Ge = load_geo(P);
   for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, Ge, m0 + r);
@@ -725,17 +739,17 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   const uint32_t img0 = fdiv((uint32_t)m0, Ge.div_ghw);
   const __amdgpu_buffer_rsrc_t rsA =
       buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
-  uint32_t vrow[AV], vmask[AV];  // rows q*32 + rg of the tile
+  uint32_t vrow[AI], vmask[AI];  // the rows this thread loads
 #pragma unroll
-  for (int q = 0; q < AV; ++q) row_gather(a, Ge, m0 + q * 32 + rg, img0, vrow[q], vmask[q]);
+  for (int q = 0; q < AI; ++q) row_gather(a, Ge, m0 + (4 * q + wave) * RPI + lrow, img0, vrow[q], vmask[q]);
   const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
   const int p_tw = P.tw, p_ktot = P.ktot, cs = a.cs;
   const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
-  uint32_t voffb[BV];
+  uint32_t voffb[BI_MAX];
 #pragma unroll
-  for (int j = 0; j < BV; ++j) {
-    const int o = n0 + j * 32 + rg;
-    voffb[j] = o < a.nout ? (uint32_t)(((int64_t)o * p_ktot + kc * 8) * 2) : kOob;
+  for (int j = 0; j < BI_MAX; ++j) {
+    const int row = (4 * j + wave) * RPI + lrow, o = n0 + row;
+    voffb[j] = (row < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + kc * 8) * 2) : kOob;
   }
   int ch = kc * 8, tap = 0, tcol = 0;
   uint32_t toff = (uint32_t)P.toff0;
@@ -752,7 +766,7 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
     }
   };
   wrap_taps();
-  const int nk = (p_ktot + kDmaRow - 1) / kDmaRow;
+  const int nk = (p_ktot + BK - 1) / BK;
 
   // issue the loads of step kt into stage s; the A walk advances by one step
   auto issue = [&](auto sc, int kt) __attribute__((always_inline)) {
@@ -761,22 +775,24 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
     const uint32_t lo = toff + 2u * (uint32_t)ch;
     const int tq = tap < 31 ? tap : 31;  // past the last tap: bit 31 is clear
 #pragma unroll
-    for (int q = 0; q < AV; ++q) {
+    for (int q = 0; q < AI; ++q) {
       const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[q], tq, 1);
       const uint32_t vo = (t & (vrow[q] + lo)) | (~t & kOob);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void_t*)(A + (q * 32 + wave * 8) * kDmaRow), 16, vo, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void_t*)(A + (4 * q + wave) * RPI * BK), 16, vo, 0, 0, 0);
     }
-    const int kb = kt * kDmaRow;
+    const int kb = kt * BK;
     const bool kin = kb + kc * 8 < p_ktot;
 #pragma unroll
-    for (int j = 0; j < BV; ++j) {
-      // (the select stays out of the builtin's argument list: written inline, the host
-      // pass drops the kernel's launch stub)
-      const uint32_t vb = kin ? voffb[j] : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(B + (j * 32 + wave * 8) * kDmaRow), 16, vb,
-                                               (uint32_t)kb * 2, 0, 0);
+    for (int j = 0; j < BI_MAX; ++j) {
+      if (4 * j + wave < BI) {  // wave-uniform
+        // (the select stays out of the builtin's argument list: written inline, the host
+        // pass drops the kernel's launch stub)
+        const uint32_t vb = kin ? voffb[j] : kOob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(B + (4 * j + wave) * RPI * BK), 16, vb,
+                                                 (uint32_t)kb * 2, 0, 0);
+      }
     }
-    ch += kDmaRow;
+    ch += BK;
     wrap_taps();
   };
 
@@ -789,26 +805,26 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // fragment byte offsets: row (wave rows + l32) of A, l32 of B; k-slice ks sits in chunk
-  // 2*ks + half, stored in slot (2*ks + half) ^ ((l32 >> 1) & 7)
-  const int sw = (l32 >> 1) & 7;
-  const uint32_t arow = (uint32_t)(wave * WTM + l32) * (kDmaRow * 2), brow = (uint32_t)l32 * (kDmaRow * 2);
-  uint32_t koff[4];
+  // 2*ks + half, stored in slot (2*ks + half) ^ ((l32 / WIN) % CPR)
+  const int sw = (l32 / WIN) % CPR;
+  const uint32_t arow = (uint32_t)(wave * WTM + l32) * (BK * 2), brow = (uint32_t)l32 * (BK * 2);
+  uint32_t koff[BK / 16];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) koff[ks] = (uint32_t)(((2 * ks + half) ^ sw) * 16);
+  for (int ks = 0; ks < BK / 16; ++ks) koff[ks] = (uint32_t)(((2 * ks + half) ^ sw) * 16);
   auto compute = [&](auto sc) __attribute__((always_inline)) {
     const unsigned char* A = reinterpret_cast<const unsigned char*>(stage_a(sc));
     const unsigned char* B = reinterpret_cast<const unsigned char*>(stage_b(sc));
     u32x4 af[2][TM], bf[2][TN];
     auto rd = [&](int ks, u32x4 (&xa)[TM], u32x4 (&xb)[TN]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i) xa[i] = *reinterpret_cast<const u32x4*>(A + arow + i * 32 * kDmaRow * 2 + koff[ks]);
+      for (int i = 0; i < TM; ++i) xa[i] = *reinterpret_cast<const u32x4*>(A + arow + i * 32 * BK * 2 + koff[ks]);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) xb[j] = *reinterpret_cast<const u32x4*>(B + brow + j * 32 * kDmaRow * 2 + koff[ks]);
+      for (int j = 0; j < TN; ++j) xb[j] = *reinterpret_cast<const u32x4*>(B + brow + j * 32 * BK * 2 + koff[ks]);
     };
     rd(0, af[0], bf[0]);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      if (ks < 3) rd(ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      if (ks + 1 < BK / 16) rd(ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -1045,9 +1061,15 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
   else if (variant == kVariantDirect)
     hipLaunchKernelGGL((convdirect_kernel<c.tm, c.tn, d_direct(c)>), grid, dim3(256), 0, s, a);
   else if (variant == kVariantDma3)
-    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3, 64>), grid, dim3(256), 0, s, a);
   else if (variant == kVariantDma2)
-    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 2>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 2, 64>), grid, dim3(256), 0, s, a);
+  else if (variant == kVariantDma32)
+    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3, 32>), grid, dim3(256), 0, s, a);
+#ifdef NUMBAT_TUNING
+  else if (variant == 6)
+    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 4, 32>), grid, dim3(256), 0, s, a);
+#endif
   else
     hipLaunchKernelGGL((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
@@ -1111,11 +1133,11 @@ bool prepare_fast(ConvGemmArgs& a, int bm) {
 // how often each shape occurs (4% above the per-layer best in total):
 //  * N tile: the least padding among 128, 96 and 64 columns (ties to the wider); when the
 //    grid would hold fewer than 400 blocks of 128 rows, 64 columns for more blocks;
-//  * fast paths, 128-row tiles: more than 32768 rows (short reductions, many blocks) the
-//    LDS-staged kernel for reductions of 1024 or more, else the register-direct one;
-//    8193..32768 rows the direct-to-LDS kernel with two stages (two blocks per CU) on
-//    96 columns when they divide N <= 192, else 64; up to 8192 rows the direct-to-LDS
-//    kernel with three stages;
+//  * fast paths, all on the direct-to-LDS kernel: more than 32768 rows, three stages of
+//    32 reduction elements (three blocks per CU for 128-row tiles), 256-row tiles when
+//    the reduction is 768 or longer; 8193..32768 rows, two stages of 64 (two blocks per
+//    CU) on 128 x 96 tiles when 96 divides N <= 192, else 128 x 64; up to 8192 rows,
+//    three stages of 64 on 128-row tiles;
 //  * generic kernel (narrow or 8-multiple channels): 256-row tiles unless that leaves
 //    fewer than 512 blocks.
 TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
@@ -1137,7 +1159,8 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
     if (blocks128 < 400 && bn > 64) bn = 64;
     bm = 128;
     if (m_max > 32768) {
-      variant = ktot >= 1024 ? kVariantLds : kVariantDirect;
+      variant = kVariantDma32;
+      bm = ktot >= 768 ? 256 : 128;
     } else if (m_max > 8192) {
       variant = kVariantDma2;
       bn = (nout % 96 == 0 && nout <= 192) ? 96 : 64;
