@@ -42,8 +42,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-events", action="store_true", help="skip the instrumented (per-kernel timing) steps")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
-    ap.add_argument("--serial", action="store_true",
-                    help="run the whole step on one stream (default: weight gradients on a second stream)")
+    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
+                    help="1: the whole step on one stream; 2: weight gradients on a second stream, "
+                         "overlapping the data gradients (measured no faster: every kernel fills the GPU)")
+    ap.add_argument("--serial", action="store_true", help="same as --streams 1")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
     return ap.parse_args()
@@ -247,7 +249,8 @@ def main():
     ws_side = torch.empty_like(ws)
     for l in layers:
         l.bind_ws(ws, ws_side)
-    side = None if args.serial else torch.cuda.Stream()  # default priority
+    two = args.streams == 2 and not args.serial
+    side = torch.cuda.Stream() if two else None  # default priority
     torch.cuda.synchronize()
     step_flops = sum(3 * l.flops for l in layers)
 
@@ -342,7 +345,7 @@ def main():
                    "config_index": wl.index, "batch": wl.n, "input": "640x640", "layers": len(layers),
                    "mode": "set", "step_gflop": round(step_flops / 1e9, 2),
                    "launch": "hip graph replay" if graph is not None else "eager",
-                   "streams": 1 if args.serial else 2},
+                   "streams": 2 if two else 1},
         "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": roofline,
     }

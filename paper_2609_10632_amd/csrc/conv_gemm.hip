@@ -1,20 +1,22 @@
-// Implicit-GEMM convolution on gfx950 MFMA, second generation (bf16 in, fp32 accumulate).
+// Implicit-GEMM convolution on gfx950 MFMA (bf16 in, fp32 accumulate).
 //
 // Computes the GEMM family described with ConvGemmArgs: the forward convolution (one
 // phase) and all stride phases of a data gradient (one launch, blockIdx.z = phase).
-//
-// Differences from the first kernel, all aimed at keeping the MFMA pipes fed:
-//  * the gathered operand A bypasses LDS: each wave loads its own MFMA A fragments
-//    (16 contiguous bytes per lane) from global memory into a register ring several
-//    steps deep; only the weight tile B, shared by the four waves, goes through LDS;
-//  * the gather address of an A fragment costs a bit test and a 64-bit add: every row
-//    keeps a pointer to its source pixel and a bitmask of the taps that land inside the
-//    image, and the per-tap pixel offsets sit in LDS; padding lanes read a zero constant,
-//    so every step issues the same loads and waits are counted exactly;
-//  * 32x32x16 MFMAs (the full-rate bf16 form on gfx950) on 256- or 128-row tiles
-//    (4 waves) by up to 128 columns;
-//  * the epilogue stages fp32 results through LDS and writes whole 16-byte vectors of
-//    8 channels (bf16, rounded once, after the optional accumulate).
+// Two kernels:
+//  * convdma_kernel, for source channel counts that are multiples of 16 and at least 32
+//    (every layer of the detector but the image input): both operands reach LDS through
+//    loads that write LDS directly, in 2 or 3 stages;
+//  * convgemm_kernel, for any channel count that is a multiple of 8 (the image input,
+//    repacked to 8 channels): each wave loads its own MFMA A fragments (16 contiguous
+//    bytes per lane) from global memory into a register ring several steps deep; only
+//    the weight tile B, shared by the four waves, goes through LDS.  Every row keeps a
+//    pointer to its source pixel and a bitmask of the taps that land inside the image;
+//    padding lanes read a zero constant, so every step issues the same loads and waits
+//    are counted exactly.
+// Both use 32x32x16 MFMAs (the full-rate bf16 form on gfx950) with 4 waves split along M,
+// and share one epilogue: optional per-tile batch-statistics partials, then fp32 results
+// staged through LDS and written as 16-byte vectors of 8 channels (bf16, rounded once,
+// after the optional accumulate).
 #include <cstdlib>
 #include <type_traits>
 
@@ -445,12 +447,12 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
 // Fast path for source channel counts that are multiples of 16 and at least 32 (every
 // layer of the detector except the 3-channel image).
 //
-// Both operands are staged through LDS.  The gathered operand is loaded coalesced: a
-// thread always loads the same 16-byte chunk c (8 channels) of the 64-element reduction
-// step, and the 8 threads with the same row cover the row's 128 contiguous bytes, so one
-// wave instruction reads 8 whole rows.  (Gathering MFMA fragments straight from global
-// memory reads 32 rows per instruction; the L1 path's cost grows with the rows, not the
-// bytes, an instruction touches, and that design stalled on it.)
+// Both operands are staged through LDS and the gathered operand is loaded coalesced: a
+// thread always loads the same 16-byte chunk (8 channels) of the step's reduction
+// elements, and the threads with the same row cover the row's contiguous bytes, so one
+// wave instruction reads whole rows -- 8 or 16 of them.  (Gathering MFMA fragments
+// straight from global memory reads 32 rows per instruction; the L1 path's cost grows
+// with the rows, not the bytes, an instruction touches, and that design stalled on it.)
 //
 // Loads are raw buffer loads.  The gather base sits halo_px pixels before the first
 // image of the tile, so every in-image address is a non-negative 32-bit offset: row
@@ -459,9 +461,7 @@ __global__ __launch_bounds__(256) void convgemm_kernel(ConvGemmArgs a) {
 // answers with zeros; so does a weight row past nout or a reduction index past ktot.
 // Each thread walks its own reduction position (tap, channel) with adds and selects:
 // 16-multiple channel counts never split a chunk between taps, and with 32 or more
-// channels a 64-element step crosses at most two tap boundaries.
-constexpr int GK16 = 64;
-constexpr int GROW16 = GK16 + 8;  // 144-byte LDS rows: 16 lanes reading 16 rows hit 16 distinct bank groups
+// channels a step of up to 64 elements crosses at most two tap boundaries.
 constexpr uint32_t kOob = 0x80000000u;  // a buffer offset past every range below
 constexpr int kRecords = 0x7ffffff0;    // buffer range (bytes); in-range offsets stay below kOob - 2^24
 
@@ -469,178 +469,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) 
   // raw buffer, stride 0, range kRecords; word 3 = 0x00020000 (32-bit data format, the
   // setting for linear loads on this architecture)
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, kRecords, 0x00020000);
-}
-
-template <int TM, int TN>
-struct LdsShape {
-  using S = GemmShape<TM, TN>;
-  static constexpr int AV = S::BM / 32;                    // A chunks per thread per step
-  static constexpr int BV = (S::BN * 8 + 255) / 256;       // B chunks per thread per step
-  static constexpr int A_BYTES = 2 * S::BM * GROW16 * 2;   // double-buffered A tile
-  static constexpr int B_BYTES = 2 * S::BN * GROW16 * 2;
-  static constexpr int SM = A_BYTES + B_BYTES > S::STAGE_BYTES ? A_BYTES + B_BYTES : S::STAGE_BYTES;
-};
-
-template <int TM, int TN, int D>
-__global__ __launch_bounds__(256) void convlds_kernel(ConvGemmArgs a) {
-  using S = GemmShape<TM, TN>;
-  using L = LdsShape<TM, TN>;
-  constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM, AV = L::AV, BV = L::BV;
-  static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
-
-  __shared__ __attribute__((aligned(16))) unsigned char smem[L::SM];
-  __shared__ int64_t s_dst[BM];
-  __shared__ float s_red[4][BN];
-  __shared__ float s_mean[BN];
-  typedef bf16_t ATile[BM][GROW16];
-  typedef bf16_t BTile[BN][GROW16];
-  ATile* As = reinterpret_cast<ATile*>(smem);
-  BTile* Bs = reinterpret_cast<BTile*>(smem + L::A_BYTES);
-
-  const TileId T = tile_id(a.remap != 0);
-  const GemmPhase& P = a.ph[T.ph];
-  const int m0 = T.mt * BM;
-  if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
-  const int n0 = T.nt * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, half = lane >> 5;
-  const int ck = tid & 7, rg = tid >> 3;  // this thread's load chunk and row within a 32-row group
-
-  const Geo G = load_geo(P);
-  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, G, m0 + r);
-
-  // A: gather base = first image of the tile, moved back by the halo (carried by toff0)
-  const uint32_t img0 = fdiv((uint32_t)m0, G.div_ghw);
-  const __amdgpu_buffer_rsrc_t rsA =
-      buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
-  uint32_t vrow[AV], vmask[AV];  // rows q*32 + rg of the tile
-#pragma unroll
-  for (int q = 0; q < AV; ++q) row_gather(a, G, m0 + q * 32 + rg, img0, vrow[q], vmask[q]);
-  // B: rows j*32 + rg of the weight tile, chunk ck
-  const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
-  const int p_tw = P.tw, p_ktot = P.ktot, cs = a.cs;
-  const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
-  uint32_t voffb[BV];
-#pragma unroll
-  for (int j = 0; j < BV; ++j) {
-    const int row = j * 32 + rg, o = n0 + row;
-    voffb[j] = (row < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + ck * 8) * 2) : kOob;
-  }
-  // this thread's reduction position: channel ch of tap `tap` (column tcol of its grid
-  // row), byte offset toff of the tap
-  int ch = ck * 8, tap = 0, tcol = 0;
-  uint32_t toff = (uint32_t)P.toff0;
-  auto wrap_taps = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int w = 0; w < 2; ++w) {
-      const bool wrap = ch >= cs;
-      ch = wrap ? ch - cs : ch;
-      tap += wrap ? 1 : 0;
-      tcol += wrap ? 1 : 0;
-      const bool rw = tcol == p_tw;
-      tcol = rw ? 0 : tcol;
-      toff += wrap ? (rw ? p_rstep : p_cstep) : 0u;
-    }
-  };
-  wrap_taps();
-  const int nk = (p_ktot + GK16 - 1) / GK16;
-  __syncthreads();
-
-  u32x4 ra[D][AV], rbv[D][BV];
-  // loads of step kt into a ring slot; the A walk advances by one step
-  auto load = [&](int kt, u32x4 (&xa)[AV], u32x4 (&xb)[BV]) __attribute__((always_inline)) {
-    const uint32_t lo = toff + 2u * (uint32_t)ch;
-    const int tq = tap < 31 ? tap : 31;  // past the last tap: bit 31 is clear
-#pragma unroll
-    for (int q = 0; q < AV; ++q) {
-      const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[q], tq, 1);
-      const uint32_t vo = (t & (vrow[q] + lo)) | (~t & kOob);
-      xa[q] = __builtin_amdgcn_raw_buffer_load_b128(rsA, vo, 0u, 0);
-    }
-    const int kb = kt * GK16;
-    const bool kin = kb + ck * 8 < p_ktot;
-#pragma unroll
-    for (int j = 0; j < BV; ++j) xb[j] = __builtin_amdgcn_raw_buffer_load_b128(rsB, kin ? voffb[j] : kOob, (uint32_t)kb * 2, 0);
-    ch += GK16;
-    wrap_taps();
-  };
-  auto store = [&](int buf, const u32x4 (&xa)[AV], const u32x4 (&xb)[BV]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int q = 0; q < AV; ++q) *reinterpret_cast<u32x4*>(&As[buf][q * 32 + rg][ck * 8]) = xa[q];
-#pragma unroll
-    for (int j = 0; j < BV; ++j)
-      if (BV * 32 == BN || j * 32 + rg < BN) *reinterpret_cast<u32x4*>(&Bs[buf][j * 32 + rg][ck * 8]) = xb[j];
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  // multiply the tiles in LDS buffer buf: fragments of k-slice ks+1 are read while the
-  // MFMAs of slice ks run
-  auto read_frags = [&](int buf, int ks, u32x4 (&af)[TM], u32x4 (&bf)[TN]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-      af[i] = *reinterpret_cast<const u32x4*>(&As[buf][wave * WTM + i * 32 + l32][ks * 16 + half * 8]);
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      bf[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][j * 32 + l32][ks * 16 + half * 8]);
-  };
-  auto compute = [&](int buf) __attribute__((always_inline)) {
-    u32x4 af[2][TM], bf[2][TN];
-    read_frags(buf, 0, af[0], bf[0]);
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      if (ks < 3) read_frags(buf, ks + 1, af[(ks + 1) & 1], bf[(ks + 1) & 1]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[ks & 1][i], bf[ks & 1][j], acc[i][j]);
-    }
-  };
-  // step kt (ring slot of step kt+1 = nxt): stage step kt+1 in LDS, fetch step kt+1+D
-  // into the freed slot, multiply the tiles of step kt
-  auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
-    constexpr int u = decltype(uc)::value;
-    constexpr int nxt = (u + 1) % D;
-    compute(kt & 1);
-    store((kt + 1) & 1, ra[nxt], rbv[nxt]);
-    load(kt + 1 + D, ra[nxt], rbv[nxt]);
-    __syncthreads();
-  };
-  // Prologue: step 0 goes to LDS; steps 1..D are left in flight, in the order the
-  // steady state issues them, so the loop is entered with the same pending loads as it
-  // loops back with and every wait counts exactly.
-  if (nk > 0) {
-    load(0, ra[0], rbv[0]);
-    store(0, ra[0], rbv[0]);
-    if constexpr (D > 1) load(1, ra[1], rbv[1]);
-    if constexpr (D > 2) load(2, ra[2], rbv[2]);
-    if constexpr (D > 3) load(3, ra[3], rbv[3]);
-    load(D, ra[0], rbv[0]);
-    __syncthreads();
-  }
-  int kb = 0;
-  for (; kb + D <= nk; kb += D) {
-    step(Ic<0>{}, kb);
-    if constexpr (D > 1) step(Ic<1 % D>{}, kb + 1);
-    if constexpr (D > 2) step(Ic<2 % D>{}, kb + 2);
-    if constexpr (D > 3) step(Ic<3 % D>{}, kb + 3);
-  }
-  if constexpr (D > 1) {
-    if (kb < nk) step(Ic<0>{}, kb);
-  }
-  if constexpr (D > 2) {
-    if (kb + 1 < nk) step(Ic<1 % D>{}, kb + 1);
-  }
-  if constexpr (D > 3) {
-    if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
-  }
-  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
 }
 
 // ---------------------------------------------------------------------------
@@ -867,170 +695,6 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, reinterpret_cast<unsigned char*>(sA0), s_dst, s_red, s_mean);
 }
 
-// ---------------------------------------------------------------------------
-// Register-direct variant of the fast path: the gathered operand bypasses LDS.  Each
-// wave loads its own MFMA A fragments (16 contiguous bytes per lane: 8 channels of one
-// pixel at one tap) with buffer loads straight into a register ring; only the weight
-// tile goes through LDS.  It needs far less LDS than the staged kernel (two or more
-// blocks per CU), but one fragment load touches 32 rows, so the L1 path caps it; it
-// wins where the reduction is short and blocks are many.  The k-slice position is the
-// same for the whole wave and walks the taps on the scalar unit.
-template <int TM, int TN, int D>
-__global__ __launch_bounds__(256) void convdirect_kernel(ConvGemmArgs a) {
-  using S = GemmShape<TM, TN>;
-  constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM;
-  constexpr int BV = (BN * 8 + 255) / 256;
-  constexpr int B_BYTES16 = 2 * BN * GROW16 * 2;
-  constexpr int SM = B_BYTES16 > S::STAGE_BYTES ? B_BYTES16 : S::STAGE_BYTES;
-  static_assert(D >= 1 && D <= 4, "prefetch depth 1..4");
-
-  __shared__ __attribute__((aligned(16))) unsigned char smem[SM];
-  __shared__ int64_t s_dst[BM];
-  __shared__ float s_red[4][BN];
-  __shared__ float s_mean[BN];
-  typedef bf16_t BTile[BN][GROW16];
-  BTile* Bs = reinterpret_cast<BTile*>(smem);
-
-  const TileId T = tile_id(a.remap != 0);
-  const GemmPhase& P = a.ph[T.ph];
-  const int m0 = T.mt * BM;
-  if (m0 >= P.m) return;
-  const int n0 = T.nt * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l32 = lane & 31, half = lane >> 5;
-
-  const Geo G = load_geo(P);
-  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, G, m0 + r);
-
-  const uint32_t img0 = fdiv((uint32_t)m0, G.div_ghw);
-  const __amdgpu_buffer_rsrc_t rsA =
-      buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
-  uint32_t vrow[TM], vmask[TM];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    row_gather(a, G, m0 + wave * WTM + i * 32 + l32, img0, vrow[i], vmask[i]);
-    vrow[i] += half * 16;
-  }
-  const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
-  const int p_tw = P.tw, p_ktot = P.ktot;
-  const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
-  uint32_t voffb[BV];
-  int bk[BV], brow[BV], bch[BV];
-#pragma unroll
-  for (int j = 0; j < BV; ++j) {
-    const int v = tid + 256 * j;
-    brow[j] = v >> 3;
-    bch[j] = v & 7;
-    bk[j] = bch[j] * 8;
-    const int o = n0 + brow[j];
-    voffb[j] = (brow[j] < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + bk[j]) * 2) : kOob;
-  }
-  int tap = 0, tcol = 0;
-  uint32_t toff = (uint32_t)P.toff0, cb = 0;
-  const uint32_t cs2 = (uint32_t)a.cs * 2;
-  const int nk = (p_ktot + GK16 - 1) / GK16;
-  __syncthreads();
-
-  u32x4 ra[D][4 * TM], rbv[D][BV];
-  auto load_a = [&](u32x4 (&xa)[4 * TM]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const uint32_t so = toff + cb;
-      const int tq = tap < 31 ? tap : 31;
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[i], tq, 1);
-        const uint32_t vo = (t & vrow[i]) | (~t & kOob);
-        xa[ks * TM + i] = __builtin_amdgcn_raw_buffer_load_b128(rsA, vo, so, 0);
-      }
-      cb += 32;
-      const bool wrap = cb == cs2;
-      cb = wrap ? 0u : cb;
-      tap += wrap ? 1 : 0;
-      tcol += wrap ? 1 : 0;
-      const bool rw = tcol == p_tw;
-      tcol = rw ? 0 : tcol;
-      toff += wrap ? (rw ? p_rstep : p_cstep) : 0u;
-    }
-  };
-  auto load_b = [&](int kt, u32x4 (&xb)[BV]) __attribute__((always_inline)) {
-    const int kb = kt * GK16;
-#pragma unroll
-    for (int j = 0; j < BV; ++j) {
-      const uint32_t vo = (kb + bk[j] < p_ktot) ? voffb[j] : kOob;
-      xb[j] = __builtin_amdgcn_raw_buffer_load_b128(rsB, vo, (uint32_t)kb * 2, 0);
-    }
-  };
-  auto store_b = [&](int buf, const u32x4 (&xb)[BV]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < BV; ++j)
-      if (BV * 256 == BN * 8 || brow[j] < BN) *reinterpret_cast<u32x4*>(&Bs[buf][brow[j]][bch[j] * 8]) = xb[j];
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  auto compute = [&](int buf, const u32x4 (&xa)[4 * TM]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      u32x4 bfr[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const u32x4*>(&Bs[buf][j * 32 + l32][ks * 16 + half * 8]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(xa[ks * TM + i], bfr[j], acc[i][j]);
-    }
-  };
-  auto step = [&](auto uc, int kt) __attribute__((always_inline)) {
-    constexpr int u = decltype(uc)::value;
-    constexpr int nxt = (u + 1) % D;
-    store_b((kt + 1) & 1, rbv[nxt]);
-    load_b(kt + 1 + D, rbv[nxt]);
-    compute(kt & 1, ra[u]);
-    load_a(ra[u]);
-    __syncthreads();
-  };
-  // prologue in steady-state issue order (see the staged kernel)
-  auto prologue = [&](auto dc) __attribute__((always_inline)) {
-    constexpr int d = decltype(dc)::value;
-    load_b(d + 1, rbv[(d + 1) % D]);
-    load_a(ra[d]);
-  };
-  if (nk > 0) {
-    load_b(0, rbv[0]);
-    store_b(0, rbv[0]);
-    prologue(Ic<0>{});
-    if constexpr (D > 1) prologue(Ic<1>{});
-    if constexpr (D > 2) prologue(Ic<2>{});
-    if constexpr (D > 3) prologue(Ic<3>{});
-    __syncthreads();
-  }
-  int kb = 0;
-  for (; kb + D <= nk; kb += D) {
-    step(Ic<0>{}, kb);
-    if constexpr (D > 1) step(Ic<1 % D>{}, kb + 1);
-    if constexpr (D > 2) step(Ic<2 % D>{}, kb + 2);
-    if constexpr (D > 3) step(Ic<3 % D>{}, kb + 3);
-  }
-  if constexpr (D > 1) {
-    if (kb < nk) step(Ic<0>{}, kb);
-  }
-  if constexpr (D > 2) {
-    if (kb + 1 < nk) step(Ic<1 % D>{}, kb + 1);
-  }
-  if constexpr (D > 3) {
-    if (kb + 2 < nk) step(Ic<2 % D>{}, kb + 2);
-  }
-  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
-}
-
 struct GInst {
   int tm, tn, d;  // 32-row tiles per wave (4 waves along M), 32-col tiles, prefetch depth (generic kernel)
 };
@@ -1045,9 +709,6 @@ constexpr GInst kG[] = {
     {1, 1, 4},  // 7: 128 x 32
 };
 
-// prefetch depths (ring slots) of the two fast paths
-constexpr int d_lds(const GInst& c) { return c.tm == 2 ? 2 : 3; }
-constexpr int d_direct(const GInst& c) { return c.tm * c.tn >= 6 ? 2 : 3; }
 
 template <int I>
 hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
@@ -1056,11 +717,7 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
   int mmax = 0;
   for (int p = 0; p < a.nphase; ++p) mmax = a.ph[p].m > mmax ? a.ph[p].m : mmax;
   dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN), (unsigned)a.nphase);
-  if (variant == kVariantLds)
-    hipLaunchKernelGGL((convlds_kernel<c.tm, c.tn, d_lds(c)>), grid, dim3(256), 0, s, a);
-  else if (variant == kVariantDirect)
-    hipLaunchKernelGGL((convdirect_kernel<c.tm, c.tn, d_direct(c)>), grid, dim3(256), 0, s, a);
-  else if (variant == kVariantDma3)
+  if (variant == kVariantDma3)
     hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3, 64>), grid, dim3(256), 0, s, a);
   else if (variant == kVariantDma2)
     hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 2, 64>), grid, dim3(256), 0, s, a);

@@ -33,7 +33,7 @@ void trace_end(int cls, hipStream_t s);
 
 // conv GEMM kernel variants: generic (source channels a multiple of 8), and the two fast
 // paths for 16-multiple channel counts of at least 32 (LDS-staged, register-direct)
-enum { kVariantGeneric = 0, kVariantLds = 1, kVariantDirect = 2, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5 };
+enum { kVariantGeneric = 0, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5 };
 struct TileCfg {
   int bm, bn;
   int id;       // instantiation id
