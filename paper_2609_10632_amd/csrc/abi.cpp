@@ -161,16 +161,16 @@ numbat_status check_conv(const numbat_conv_problem* p, ConvDesc* d) {
   return NUMBAT_OK;
 }
 
-// Inputs with fewer than 8 channels (the RGB image) are repacked into 8-channel pixels
-// in the workspace (channels ci..7 zero, weights likewise), so every convolution runs on
-// the 16-byte-vector kernels.
+// Inputs with fewer than 8 channels (the RGB image) have kernels of their own for the
+// forward (reduction packed densely) and the data gradient (one thread per input pixel);
+// the weight gradient repacks the input into 8-channel pixels in the workspace (channels
+// ci..7 zero) and runs the 16-byte-vector kernel.
 bool narrow(const ConvDesc& d) { return d.ci % 8 != 0; }
 size_t x8_bytes(const ConvDesc& d) { return round_up((size_t)d.n * d.h * d.w * 16, 256); }
-size_t w8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 16, 256); }
 
 TileCfg fwd_tile(const ConvDesc& d) {
-  const int cs = narrow(d) ? 8 : d.ci;
-  return convgemm_pick(d.m, d.co, cs, d.kh * d.kw * cs);
+  if (narrow(d)) return narrow_pick(d.co);
+  return convgemm_pick(d.m, d.co, d.ci, d.kh * d.kw * d.ci);
 }
 
 size_t fwd_stats_bytes(const ConvDesc& d) {
@@ -179,13 +179,13 @@ size_t fwd_stats_bytes(const ConvDesc& d) {
   return round_up((size_t)mt * d.co * sizeof(float2), 256);
 }
 
-size_t fwd_ws(const ConvDesc& d) { return fwd_stats_bytes(d) + (narrow(d) ? x8_bytes(d) + w8_bytes(d) : 0); }
+size_t fwd_ws(const ConvDesc& d) { return fwd_stats_bytes(d); }
 
-// data gradient: re-laid-out weights (channels padded to 8 for a narrow input) and, for a
-// narrow input, the 8-channel gradient the GEMM writes before the ci channels are taken
-size_t dgrad_cpad(const ConvDesc& d) { return narrow(d) ? 8 : d.ci; }
+// data gradient: the weights re-laid out per stride phase (as fp32 [kh][kw][co][ci] for a
+// narrow input)
 size_t bwd_data_ws(const ConvDesc& d) {
-  return round_up((size_t)d.kh * d.kw * dgrad_cpad(d) * d.co * 2, 256) + (narrow(d) ? x8_bytes(d) : 0);
+  return narrow(d) ? round_up((size_t)d.kh * d.kw * d.co * d.ci * sizeof(float), 256)
+                   : round_up((size_t)d.kh * d.kw * d.ci * d.co * 2, 256);
 }
 
 size_t dw8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 8 * sizeof(float), 256); }
@@ -358,7 +358,7 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
     return fail(NUMBAT_ERR_ALIGN, "x and w must be 2-byte aligned");
   if (batch_stats != nullptr && (reinterpret_cast<uintptr_t>(batch_stats) & 3u))
     return fail(NUMBAT_ERR_ALIGN, "batch_stats must be 4-byte aligned");
-  const size_t need = (batch_stats ? fwd_stats_bytes(d) : 0) + (vec_in ? 0 : x8_bytes(d) + w8_bytes(d));
+  const size_t need = batch_stats ? fwd_stats_bytes(d) : 0;
   st = check_ws(ws, ws_bytes, need);
   if (st != NUMBAT_OK) return st;
 
@@ -369,20 +369,8 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
   float2* part = batch_stats ? reinterpret_cast<float2*>(wsp) : nullptr;
   const bf16_t* src = static_cast<const bf16_t*>(x);
   const bf16_t* wt = static_cast<const bf16_t*>(w);
-  int64_t src_pix = d.x_pix;
-  int cs = d.ci;
-  if (!vec_in) {
-    bf16_t* x8 = reinterpret_cast<bf16_t*>(wsp + (batch_stats ? fwd_stats_bytes(d) : 0));
-    bf16_t* w8 = reinterpret_cast<bf16_t*>(reinterpret_cast<char*>(x8) + x8_bytes(d));
-    e = pack8_launch(src, d.x_pix, d.ci, (int64_t)d.n * d.h * d.w, x8, s);
-    if (e != hipSuccess) return hip_fail(e, "input repack launch");
-    e = pack8_launch(wt, d.ci, d.ci, (int64_t)d.co * d.kh * d.kw, w8, s);
-    if (e != hipSuccess) return hip_fail(e, "weight repack launch");
-    src = x8;
-    wt = w8;
-    src_pix = 8;
-    cs = 8;
-  }
+  const int64_t src_pix = d.x_pix;
+  const int cs = d.ci;
   ConvGemmArgs g;
   std::memset(&g, 0, sizeof g);
   g.src = src;
@@ -413,7 +401,7 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
   for (int r = 0; r < d.kh; ++r)
     for (int q = 0; q < d.kw; ++q)
       P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
-  e = convgemm_launch(g, t, s, KC_CONV_FWD);
+  e = vec_in ? convgemm_launch(g, t, s, KC_CONV_FWD) : convnarrow_launch(g, t, s);
   if (e != hipSuccess) return hip_fail(e, "conv forward launch");
   if (batch_stats) {
     const int mt = (int)((d.m + t.bm - 1) / t.bm);
@@ -436,8 +424,35 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   st = check_ws(ws, ws_bytes, bwd_data_ws(d));
   if (st != NUMBAT_OK) return st;
 
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (narrow(d)) {
+    NarrowDgradArgs na;
+    na.dy = static_cast<const bf16_t*>(dy);
+    na.dy_pix = d.y_pix;
+    na.wt = static_cast<const bf16_t*>(w);
+    na.dx = static_cast<bf16_t*>(dx);
+    na.dx_pix = d.x_pix;
+    na.n = d.n;
+    na.h = d.h;
+    na.w = d.w;
+    na.co = d.co;
+    na.kh = d.kh;
+    na.kw = d.kw;
+    na.sh = d.sh;
+    na.sw = d.sw;
+    na.ph = d.ph;
+    na.pw = d.pw;
+    na.ho = d.ho;
+    na.wo = d.wo;
+    na.accumulate = accumulate ? 1 : 0;
+    e = dgrad_narrow_launch(na, d.ci, static_cast<float*>(ws), s);
+    if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+    return ok();
+  }
+
   // stride phases (a, b): input rows h = a + sh*i read output rows p = i + (a + ph - r) / sh
-  const int cpad = (int)dgrad_cpad(d);
+  const int cpad = d.ci;
   PhaseTaps ph[16];
   int first[16];
   int nphase = 0, total = 0;
@@ -463,23 +478,10 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
       total += f.count;
       ++nphase;
     }
-  hipStream_t s = static_cast<hipStream_t>(stream);
   bf16_t* wt = static_cast<bf16_t*>(ws);
-  hipError_t e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, cpad, first, ph,
+  e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, cpad, first, ph,
                                       nphase, s);
   if (e != hipSuccess) return hip_fail(e, "data-gradient weight re-layout launch");
-  // a narrow input's gradient is computed as 8 channels (padding channels have zero
-  // weights) into the workspace, so the GEMM writes whole 16-byte vectors; with
-  // accumulate the workspace first receives dx, so the sum is formed in fp32 and rounded
-  // once as on the direct path
-  bf16_t* dx8 = nullptr;
-  if (narrow(d)) {
-    dx8 = reinterpret_cast<bf16_t*>(static_cast<char*>(ws) + round_up((size_t)d.kh * d.kw * cpad * d.co * 2, 256));
-    if (accumulate) {
-      e = pack8_launch(static_cast<const bf16_t*>(dx), d.x_pix, d.ci, (int64_t)d.n * d.h * d.w, dx8, s);
-      if (e != hipSuccess) return hip_fail(e, "gradient repack launch");
-    }
-  }
   // all stride phases in launches of up to kMaxPhases phases (blockIdx.z = phase)
   ConvGemmArgs g;
   std::memset(&g, 0, sizeof g);
@@ -491,8 +493,8 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   g.nout = cpad;
   g.nimg = d.n;
   g.gstride_h = g.gstride_w = 1;
-  g.dst = dx8 ? dx8 : static_cast<bf16_t*>(dx);
-  g.dst_pix = dx8 ? 8 : d.x_pix;
+  g.dst = static_cast<bf16_t*>(dx);
+  g.dst_pix = d.x_pix;
   g.hd = d.h;
   g.wd = d.w;
   g.dstep_h = d.sh;
@@ -533,10 +535,6 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   if (g.nphase > 0) {
     e = convgemm_launch(g, convgemm_pick(mmax, cpad, d.co, ktmax), s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
-  }
-  if (dx8) {
-    e = unpack8_launch(dx8, d.ci, (int64_t)d.n * d.h * d.w, static_cast<bf16_t*>(dx), d.x_pix, s);
-    if (e != hipSuccess) return hip_fail(e, "gradient channel extraction launch");
   }
   return ok();
 }

@@ -695,6 +695,141 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, reinterpret_cast<unsigned char*>(sA0), s_dst, s_red, s_mean);
 }
 
+// ---------------------------------------------------------------------------
+// Forward convolution of a narrow input (fewer than 8 channels: the RGB image).  The
+// reduction k = (tap, channel) is packed densely (K = taps * ci, e.g. 27, padded to a
+// multiple of 16), so an MFMA A fragment -- 8 consecutive k of one output pixel -- is
+// gathered element by element: a per-k table in LDS holds each k's offset from the
+// pixel's anchor and its tap, and a tap outside the image reads a zero.  The weights
+// (OHWI is already [o][k]) sit in LDS for the whole block.  One pass over K, then the
+// shared epilogue (statistics partials, 16-byte output vectors).
+template <int TM, int TN>
+struct NarrowShape {
+  using G = GemmShape<TM, TN>;
+  static constexpr int KMAX = ((kMaxTaps * 7 + 15) / 16) * 16;  // 176
+  static constexpr int BROW = KMAX + 8;                           // bf16 per weight row (odd multiple of 16 bytes)
+  static constexpr int B_BYTES = G::BN * BROW * 2;
+  static constexpr int SM = B_BYTES > G::STAGE_BYTES ? B_BYTES : G::STAGE_BYTES;
+};
+
+template <int TM, int TN>
+__global__ __launch_bounds__(256) void convnarrow_kernel(ConvGemmArgs a) {
+  using G = GemmShape<TM, TN>;
+  using Sh = NarrowShape<TM, TN>;
+  constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM, BROW = Sh::BROW;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[Sh::SM];
+  __shared__ int32_t s_koff[Sh::KMAX];  // element offset of k from the pixel's anchor
+  __shared__ int32_t s_ktap[Sh::KMAX];  // tap of k (31 past K: bit 31 of a tap mask is clear)
+  __shared__ int64_t s_dst[BM];
+  __shared__ float s_red[4][BN];
+  __shared__ float s_mean[BN];
+  bf16_t* Bs = reinterpret_cast<bf16_t*>(smem);
+
+  const TileId T{(int)blockIdx.x, (int)blockIdx.y, 0};
+  const GemmPhase& P = a.ph[0];
+  const int m0 = T.mt * BM, n0 = T.nt * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int ktot = P.ktot, nks = (ktot + 15) / 16, kp = nks * 16;
+
+  for (int k = tid; k < kp; k += 256) {
+    int off = 0, tap = 31;
+    if (k < ktot) {
+      tap = k / a.cs;
+      const int c = k - tap * a.cs;
+      const int o = P.off[tap];
+      off = (int)(((int16_t)(o & 0xffff) * a.ws + (o >> 16)) * a.src_pix) + c;
+    }
+    s_koff[k] = off;
+    s_ktap[k] = tap;
+  }
+  for (int e = tid; e < BN * kp; e += 256) {
+    const int r = e / kp, k = e - r * kp, o = n0 + r;
+    Bs[r * BROW + k] = (o < a.nout && k < ktot) ? P.wt[(int64_t)o * ktot + k] : (bf16_t)0;
+  }
+  for (int r = tid; r < BM; r += 256) {
+    const int m = m0 + r;
+    int64_t d = -1;
+    if (m < P.m) {
+      uint32_t img, gi, gj;
+      grid_pos((uint32_t)m, P, img, gi, gj);
+      d = (((int64_t)img * a.hd + (int)gi * a.dstep_h + P.doff_h) * a.wd + (int)gj * a.dstep_w + P.doff_w) *
+          a.dst_pix;
+    }
+    s_dst[r] = d;
+  }
+  // this lane's rows: anchor element (the tap (0, 0) pixel before padding) and the taps
+  // inside the image
+  const bf16_t* rowp[TM];
+  uint32_t rmask[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = m0 + wave * WTM + i * 32 + l32;
+    rowp[i] = a.src;
+    rmask[i] = 0;
+    if (m < P.m) {
+      uint32_t img, gi, gj;
+      grid_pos((uint32_t)m, P, img, gi, gj);
+      const int ih0 = (int)gi * a.gstride_h, iw0 = (int)gj * a.gstride_w;
+      rowp[i] = a.src + ((int64_t)img * a.hs * a.ws + (int64_t)ih0 * a.ws + iw0) * a.src_pix;
+      uint32_t mk = 0;
+      for (int t = 0; t < P.taps; ++t) {
+        const int off = P.off[t];
+        const int ih = ih0 + (int)(int16_t)(off & 0xffff), iw = iw0 + (off >> 16);
+        if ((unsigned)ih < (unsigned)a.hs && (unsigned)iw < (unsigned)a.ws) mk |= 1u << t;
+      }
+      rmask[i] = mk;
+    }
+  }
+  __syncthreads();
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  const bf16_t* zp = reinterpret_cast<const bf16_t*>(&kZero16);
+  for (int ks = 0; ks < nks; ++ks) {
+    const int kb = ks * 16 + half * 8;
+    int koff[8];
+    uint32_t ktap[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      koff[e] = s_koff[kb + e];
+      ktap[e] = (uint32_t)s_ktap[kb + e];
+    }
+    u32x4 af[TM], bf[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      uint32_t h[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = (rmask[i] >> ktap[e]) & 1u;
+        h[e] = (uint32_t)*(ok ? rowp[i] + koff[e] : zp);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) af[i][q] = h[2 * q] | (h[2 * q + 1] << 16);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bf[j] = *reinterpret_cast<const u32x4*>(&Bs[(j * 32 + l32) * BROW + kb]);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
+  }
+  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
+}
+
+template <int TN>
+hipError_t launch_narrow(const ConvGemmArgs& a, hipStream_t s) {
+  using G = GemmShape<2, TN>;
+  dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
+  hipLaunchKernelGGL((convnarrow_kernel<2, TN>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 struct GInst {
   int tm, tn, d;  // 32-row tiles per wave (4 waves along M), 32-col tiles, prefetch depth (generic kernel)
 };
@@ -838,6 +973,18 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
   bn = kG[id].tn * 32;
 #endif
   return TileCfg{bm, bn, id, variant};
+}
+
+// narrow input (ci < 8): 256-row tiles, 32 or 64 columns
+TileCfg narrow_pick(int nout) { return TileCfg{256, nout <= 32 ? 32 : 64, -1, kVariantGeneric}; }
+
+hipError_t convnarrow_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s) {
+  if (a.nphase != 1 || a.ph[0].ktot > NarrowShape<2, 2>::KMAX || a.ph[0].taps > kMaxTaps)
+    return hipErrorInvalidValue;
+  trace_begin(KC_CONV_FWD, s);
+  const hipError_t e = t.bn == 32 ? launch_narrow<1>(a, s) : launch_narrow<2>(a, s);
+  trace_end(KC_CONV_FWD, s);
+  return e;
 }
 
 hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls) {

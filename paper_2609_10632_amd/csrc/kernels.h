@@ -91,12 +91,29 @@ struct ConvGemmArgs {
 TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot);
 // a is taken by value: the launcher completes the tap-walk fields
 hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls);
+// forward convolution of a narrow input (cs = ci < 8, one phase, wt = OHWI weights with
+// K = taps * ci packed densely); rows per tile and columns per tile of narrow_pick
+TileCfg narrow_pick(int nout);
+hipError_t convnarrow_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s);
 
 // 8-channel repacking of a narrow (ci < 8) NHWC tensor, and extraction of ci channels
 // from a weight gradient computed on the repacked layout
 hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s);
 hipError_t unpack_dw_launch(const float* dw8, float* dw, int64_t rows, int ci, int accumulate, hipStream_t s);
 hipError_t unpack8_launch(const bf16_t* src8, int ci, int64_t n, bf16_t* dst, int64_t dst_pix, hipStream_t s);
+
+// data gradient of a narrow input (ci < 8), one thread per input pixel
+struct NarrowDgradArgs {
+  const bf16_t* dy;
+  int64_t dy_pix;
+  const bf16_t* wt;  // OHWI, [co][kh][kw][ci]
+  bf16_t* dx;
+  int64_t dx_pix;
+  int32_t n, h, w, co, kh, kw, sh, sw, ph, pw, ho, wo;
+  int32_t accumulate;
+};
+// wf: workspace for the weights as fp32 [kh][kw][co][ci] (kh * kw * co * ci * 4 bytes)
+hipError_t dgrad_narrow_launch(const NarrowDgradArgs& a, int ci, float* wf, hipStream_t s);
 
 // merge per-tile (mean, M2) partials into batch mean / biased variance, fixed order
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,
