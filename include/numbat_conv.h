@@ -128,8 +128,8 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
  * batch_stats: NULL, or fp32 [2*c_out] receiving the batch mean (first c_out entries) and
  * biased batch variance (next c_out) of every output channel over the n*ho*wo rows, taken
  * from the fp32 accumulators before rounding (BN statistics in fp32, Sec. 3.2).
- * ws: numbat_workspace_size(NUMBAT_OP_CONV_FWD) bytes; it may be NULL only when batch_stats
- * is NULL and c_in is a multiple of 8 (a narrower input is repacked into the workspace). */
+ * ws: numbat_workspace_size(NUMBAT_OP_CONV_FWD) bytes (per-tile statistics partials); it
+ * may be NULL when batch_stats is NULL. */
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream);
 
@@ -137,7 +137,9 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
  *   dx[n,h,w,c] = sum over (p,q,r,s,o) with p*stride_h - pad_h + r = h and
  *                 q*stride_w - pad_w + s = w of  w[o,r,s,c] * dy[n,p,q,o].
  * dy: bf16 NHWC [n,ho,wo,c_out] (y_pixel_stride); dx: bf16 NHWC [n,h,w,c_in] (x_pixel_stride).
- * accumulate != 0: dx += result (sum formed in fp32, rounded once), else dx = result. */
+ * accumulate != 0: dx += result (sum formed in fp32, rounded once), else dx = result.
+ * ws: numbat_workspace_size(NUMBAT_OP_CONV_BWD_DATA) bytes (the weights re-laid out per
+ * stride phase). */
 numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
                                    int accumulate, void* ws, size_t ws_bytes, void* stream);
 
@@ -145,7 +147,9 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
  * fp32 master weights, Table 1 precision row):
  *   dw[o,r,s,c] = sum_{n,p,q} dy[n,p,q,o] * x[n, p*stride_h - pad_h + r, q*stride_w - pad_w + s, c].
  * accumulate != 0: dw += result, else dw = result.  The sum over n*ho*wo rows is split into
- * fixed ranges reduced in a fixed order, so the result is bitwise reproducible. */
+ * fixed ranges reduced in a fixed order, so the result is bitwise reproducible.
+ * ws: numbat_workspace_size(NUMBAT_OP_CONV_BWD_WEIGHT) bytes (split partials; for c_in < 8
+ * also the input repacked to 8 channels). */
 numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x, const void* dy, float* dw,
                                      int accumulate, void* ws, size_t ws_bytes, void* stream);
 
