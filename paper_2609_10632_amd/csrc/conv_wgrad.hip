@@ -22,7 +22,7 @@ namespace {
 template <int V>
 using Ic = std::integral_constant<int, V>;
 
-constexpr int BR = 64;           // reduction pixels per step
+constexpr int kSplitQuantum = 64;  // pixel splits are whole multiples of this
 constexpr int BNK = 128;         // k columns per tile
 constexpr uint32_t kOobW = 0x80000000u;
 constexpr int kRecW = 0x7ffffff0;
@@ -59,19 +59,22 @@ __device__ __forceinline__ v2u_t table_read(const uint2* p) {
   return r;
 }
 
-template <int TMO, int S>
+template <int TMO, int S, int BR>
 struct WgDmaShape {
   static constexpr int BMO = 64 * TMO;
-  static constexpr int D_ELEMS = TMO * BR * 64;  // dy: TMO sub-tiles of [64 px][64 ch]
-  static constexpr int X_ELEMS = 2 * BR * 64;    // x: 2 sub-tiles of [64 px][64 k]
-  static constexpr int LOADS = 2 * TMO + 4;      // load instructions per thread per step
+  static constexpr int D_ELEMS = TMO * BR * 64;  // dy: TMO sub-tiles of [BR px][64 ch]
+  static constexpr int X_ELEMS = 2 * BR * 64;    // x: 2 sub-tiles of [BR px][64 k]
+  static constexpr int RBW = BR / 32;            // 8-pixel row blocks per wave per sub-tile
+  static constexpr int LOADS = (TMO + 2) * RBW;  // load instructions per thread per step
   static constexpr int PENDING = (S - 2) * LOADS;
+  static constexpr int LDS_BYTES = S * (D_ELEMS + X_ELEMS) * 2 + 2 * BR * 8;
 };
 
-template <int TMO, int S>
+template <int TMO, int S, int BR>
 __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div_wo, FastDiv div_howo) {
-  using Sh = WgDmaShape<TMO, S>;
-  constexpr int BMO = Sh::BMO, TM = TMO, TN = 2, LOADS = Sh::LOADS;
+  using Sh = WgDmaShape<TMO, S, BR>;
+  constexpr int BMO = Sh::BMO, TM = TMO, TN = 2, RBW = Sh::RBW;
+  static_assert(BR == 32 || BR == 64, "pixels per step");
   static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
   static_assert(Sh::PENDING <= 63, "load counter range");
 
@@ -176,25 +179,28 @@ __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div
     const __amdgpu_buffer_rsrc_t rd = wrsrc(a.dy + p0 * a.dy_pix);
     const int64_t left64 = rend - p0;
     const int left = left64 <= 0 ? 0 : (left64 >= BR ? BR : (int)left64);
-    const v2u_t e0 = table_read(&s_pix[st & 1][wave * 8 + prow]);
-    const v2u_t e1 = table_read(&s_pix[st & 1][(wave + 4) * 8 + prow]);
+    v2u_t e[RBW];
 #pragma unroll
-    for (int t = 0; t < LOADS; ++t) {
-      const int rb = wave + 4 * (t & 1);  // row block
-      const int px = rb * 8 + prow;       // pixel of the step
-      if (t < 2 * TMO) {
-        const int h = t >> 1;
+    for (int u = 0; u < RBW; ++u) e[u] = table_read(&s_pix[st & 1][(wave + 4 * u) * 8 + prow]);
+#pragma unroll
+    for (int h = 0; h < TMO; ++h)
+#pragma unroll
+      for (int u = 0; u < RBW; ++u) {
+        const int rb = wave + 4 * u;  // row block
+        const int px = rb * 8 + prow;  // pixel of the step
         const uint32_t ok = 0u - (uint32_t)(px < left);
         const uint32_t vo = (ok & ((uint32_t)px * dpix2 + dcol[h])) | (~ok & kOobW);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (wlds_void_t*)(D + h * BR * 64 + rb * 8 * 64), 16, vo, 0, 0, 0);
-      } else {
-        const int h = (t - 2 * TMO) >> 1;
-        const v2u_t e = (t & 1) ? e1 : e0;
-        const uint32_t tb = (uint32_t)__builtin_amdgcn_sbfe((int)e.y, xtap[h], 1);
-        const uint32_t vo = (tb & (e.x + xcol[h])) | (~tb & kOobW);
+      }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int u = 0; u < RBW; ++u) {
+        const int rb = wave + 4 * u;
+        const uint32_t tb = (uint32_t)__builtin_amdgcn_sbfe((int)e[u].y, xtap[h], 1);
+        const uint32_t vo = (tb & (e[u].x + xcol[h])) | (~tb & kOobW);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (wlds_void_t*)(X + h * BR * 64 + rb * 8 * 64), 16, vo, 0, 0, 0);
       }
-    }
   };
 
   f32x16 acc[TM][TN];
@@ -361,18 +367,49 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float4* part, 
 
 }  // namespace
 
-// output-channel tile: 128 rows (twice the multiply per loaded x tile of 64 rows, which
-// outweighs the padding of channel counts like 192), 64 when one such tile covers c_out
-int wgrad_bmo(int co) { return co <= 64 ? 64 : 128; }
+// Kernel configuration for a weight gradient: output-channel tile 64*tmo (1..3), pixels
+// per step br (32 or 64), LDS stages.  Chosen from the problem only, so the workspace size
+// and the launch agree.
+struct WgCfg {
+  int tmo, stages, br;
+};
+static WgCfg wgrad_cfg(int co) {
+  // 128-channel tiles where they pad c_out no more than 64-channel ones (fewer re-reads of
+  // x), else 64 (three blocks per CU instead of two); two stages of 64 pixels.  Fitted to
+  // a sweep of tile, stages and pixels per step over the detector's layers (32 pixels per
+  // step and 192-channel tiles lost everywhere)
+  const bool wide = co > 64 && (co + 127) / 128 * 128 == (co + 63) / 64 * 64;
+  WgCfg c{wide ? 2 : 1, 2, 64};
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_WG_TMO")) c.tmo = atoi(e);
+  if (const char* e = getenv("NUMBAT_WG_STAGES")) c.stages = atoi(e);
+  if (const char* e = getenv("NUMBAT_WG_BR")) c.br = atoi(e);
+#endif
+  return c;
+}
+// blocks of a configuration resident on one CU: the smaller of what LDS and what the
+// registers allow (the register counts are those the compiler gives these kernels: a
+// block is one wave per SIMD, 512 registers per lane)
+static int wgrad_blocks_per_cu(const WgCfg& c) {
+  const int bytes = c.stages * (c.tmo + 2) * c.br * 128 + 2 * c.br * 8 + 1024;
+  const int by_lds = (160 * 1024) / bytes;
+  const int regs = c.tmo == 1 ? (c.br == 32 ? 104 : (c.stages == 3 ? 176 : 136))
+                 : c.tmo == 2 ? (c.br == 32 ? 144 : (c.stages == 3 ? 264 : 176))
+                              : (c.br == 32 ? 208 : 264);
+  const int by_regs = 512 / regs;
+  int b = by_lds < by_regs ? by_lds : by_regs;
+  return b < 1 ? 1 : (b > 4 ? 4 : b);
+}
 
 int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
-  const int bmo = wgrad_bmo(co);
+  const WgCfg c = wgrad_cfg(co);
+  const int bmo = 64 * c.tmo;
   const int tiles = (int)(((co + bmo - 1) / bmo) * ((ktot + BNK - 1) / BNK));
-  const int64_t steps = (m + BR - 1) / BR;
-  // Two blocks fit per CU (LDS), 512 on the chip: as many splits as keep the grid within
-  // one such round (a few blocks past it would cost a whole second round); at least 16
-  // steps per split, at most 256 splits, partials at most 64 MiB
-  int64_t slots = 512;
+  const int64_t steps = (m + kSplitQuantum - 1) / kSplitQuantum;
+  // As many splits as keep the grid within one round of resident blocks (a few blocks
+  // past it would cost a whole second round); at least 16 quanta per split, at most 256
+  // splits, partials at most 64 MiB
+  int64_t slots = 256 * wgrad_blocks_per_cu(c);
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_WG_SLOTS")) slots = atoi(e);
 #endif
@@ -384,29 +421,24 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   while (splits > 1 && splits * part_bytes > (64ll << 20)) --splits;
   if (splits < 1) splits = 1;
   const int64_t steps_per = (steps + splits - 1) / splits;
-  *rows_per_split = steps_per * BR;
+  *rows_per_split = steps_per * kSplitQuantum;
   splits = (int)((m + *rows_per_split - 1) / *rows_per_split);
   return (int)(splits < 1 ? 1 : splits);
 }
 
 namespace {
-// two LDS stages: two blocks per CU for 128-channel tiles, which measured faster on every
-// layer of the detector than one block with three stages
-template <int TMO>
-hipError_t launch_w(const WgradArgs& a, int stages, hipStream_t s) {
+template <int TMO, int S, int BR>
+hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   constexpr int BMO = 64 * TMO;
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
-  trace_begin(KC_WGRAD, s);
-#ifdef NUMBAT_TUNING
-  if (stages == 3)
-    hipLaunchKernelGGL((wgrad_dma_kernel<TMO, 3>), grid, dim3(256), 0, s, a, dwo, dhw);
-  else
-#endif
-    hipLaunchKernelGGL((wgrad_dma_kernel<TMO, 2>), grid, dim3(256), 0, s, a, dwo, dhw);
-  (void)stages;
-  trace_end(KC_WGRAD, s);
+  hipLaunchKernelGGL((wgrad_dma_kernel<TMO, S, BR>), grid, dim3(256), 0, s, a, dwo, dhw);
   return hipGetLastError();
+}
+template <int TMO>
+hipError_t launch_w_tmo(const WgradArgs& a, const WgCfg& c, hipStream_t s) {
+  if (c.br == 32) return c.stages == 3 ? launch_w<TMO, 3, 32>(a, s) : launch_w<TMO, 2, 32>(a, s);
+  return c.stages == 3 ? launch_w<TMO, 3, 64>(a, s) : launch_w<TMO, 2, 64>(a, s);
 }
 }  // namespace
 
@@ -415,12 +447,17 @@ hipError_t wgrad_launch(const WgradArgs& args, hipStream_t s) {
   // XCD-aware tile order: the tiles of one pixel split share an XCD and its L2 (9% less
   // weight-gradient time over the detector's layers than the launch order)
   a.remap = 1;
-  int stages = 2;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_REMAP_WG")) a.remap = atoi(e);
-  if (const char* e = getenv("NUMBAT_WG_STAGES")) stages = atoi(e);
 #endif
-  return wgrad_bmo(a.co) == 64 ? launch_w<1>(a, stages, s) : launch_w<2>(a, stages, s);
+  const WgCfg c = wgrad_cfg(a.co);
+  trace_begin(KC_WGRAD, s);
+  hipError_t e;
+  if (c.tmo == 1) e = launch_w_tmo<1>(a, c, s);
+  else if (c.tmo == 3) e = launch_w_tmo<3>(a, c, s);
+  else e = launch_w_tmo<2>(a, c, s);
+  trace_end(KC_WGRAD, s);
+  return e;
 }
 
 hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
