@@ -562,8 +562,6 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   const int kc = (lane % CPR) ^ (((wave * RPI + lrow) / WIN) % CPR);
 
   const Geo Ge = load_geo(P);
-  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, Ge, m0 + r);
-
   const uint32_t img0 = fdiv((uint32_t)m0, Ge.div_ghw);
   const __amdgpu_buffer_rsrc_t rsA =
       buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
@@ -676,6 +674,9 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
     if constexpr (S > 2) issue(Ic<1>{}, 1);
     if constexpr (S > 3) issue(Ic<2>{}, 2);
   }
+  // destination offsets of the tile's rows, needed only by the epilogue: computed while
+  // the first stages load (the first step's barrier publishes them)
+  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, Ge, m0 + r);
   int kb = 0;
   for (; kb + S <= nk; kb += S) {
     step(Ic<0>{}, kb);
