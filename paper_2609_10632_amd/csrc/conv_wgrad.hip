@@ -387,29 +387,15 @@ static WgCfg wgrad_cfg(int co) {
 #endif
   return c;
 }
-// blocks of a configuration resident on one CU: the smaller of what LDS and what the
-// registers allow (the register counts are those the compiler gives these kernels: a
-// block is one wave per SIMD, 512 registers per lane)
-static int wgrad_blocks_per_cu(const WgCfg& c) {
-  const int bytes = c.stages * (c.tmo + 2) * c.br * 128 + 2 * c.br * 8 + 1024;
-  const int by_lds = (160 * 1024) / bytes;
-  const int regs = c.tmo == 1 ? (c.br == 32 ? 104 : (c.stages == 3 ? 176 : 136))
-                 : c.tmo == 2 ? (c.br == 32 ? 144 : (c.stages == 3 ? 264 : 176))
-                              : (c.br == 32 ? 208 : 264);
-  const int by_regs = 512 / regs;
-  int b = by_lds < by_regs ? by_lds : by_regs;
-  return b < 1 ? 1 : (b > 4 ? 4 : b);
-}
-
 int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   const WgCfg c = wgrad_cfg(co);
   const int bmo = 64 * c.tmo;
   const int tiles = (int)(((co + bmo - 1) / bmo) * ((ktot + BNK - 1) / BNK));
   const int64_t steps = (m + kSplitQuantum - 1) / kSplitQuantum;
-  // As many splits as keep the grid within one round of resident blocks (a few blocks
-  // past it would cost a whole second round); at least 16 quanta per split, at most 256
-  // splits, partials at most 64 MiB
-  int64_t slots = 256 * wgrad_blocks_per_cu(c);
+  // As many splits as fill 512 block slots (two per CU; with three blocks resident per
+  // CU, 768 slots measured slower: shorter splits, more partials to reduce); at least 16
+  // quanta per split, at most 256 splits, partials at most 64 MiB
+  int64_t slots = 512;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_WG_SLOTS")) slots = atoi(e);
 #endif
