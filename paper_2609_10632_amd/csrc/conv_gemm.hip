@@ -126,15 +126,18 @@ __device__ __forceinline__ void row_gather(const ConvGemmArgs& a, const Geo& G, 
   geo_pos((uint32_t)m, G, img, gi, gj);
   const int ih0 = (int)gi * a.gstride_h, iw0 = (int)gj * a.gstride_w;
   vrow = (uint32_t)((((int64_t)(img - img0) * a.hs + ih0) * a.ws + iw0) * (a.src_pix * 2));
+  // (kernel sides are at most 5: fixed-trip, branch-free loops)
   uint32_t cols = 0;
-  for (int j = 0; j < G.tw; ++j) {
+#pragma unroll
+  for (int j = 0; j < 5; ++j) {
     const int iw = iw0 + G.dw0 + j * G.tsw;
-    cols |= ((unsigned)iw < (unsigned)a.ws ? 1u : 0u) << j;
+    cols |= (j < G.tw && (unsigned)iw < (unsigned)a.ws ? 1u : 0u) << j;
   }
   uint32_t mk = 0;
-  for (int i = 0; i < G.th; ++i) {
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
     const int ih = ih0 + G.dh0 + i * G.tsh;
-    mk |= ((unsigned)ih < (unsigned)a.hs ? cols : 0u) << (i * G.tw);
+    mk |= (i < G.th && (unsigned)ih < (unsigned)a.hs ? cols : 0u) << (i * G.tw);
   }
   vmask = mk;  // bits >= taps stay clear, so a walk past the last tap reads zeros
 }
@@ -547,10 +550,26 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
     else return sB3;
   };
 
-  const TileId T = tile_id(a.remap != 0);
+  // (launch order: the XCD-aware order measured no faster for these GEMMs; a constant
+  // keeps the block's first loads from waiting on a kernel argument)
+  const TileId T = tile_id(false);
   const GemmPhase& P = a.ph[T.ph];
+  const Geo Ge = load_geo(P);
+  {
+    // every kernel argument the prologue needs, loaded at once and completed before the
+    // early-exit test (otherwise the compiler splits them into dependent rounds after it)
+    const bf16_t* src = a.src;
+    const bf16_t* wt = P.wt;
+    const int64_t spx = a.src_pix;
+    const int hs = a.hs, ws = a.ws, cs = a.cs, nout = a.nout, halo = a.halo_px, gsh = a.gstride_h,
+              gsw = a.gstride_w, kt = P.ktot, tw = P.tw, t0 = P.toff0, cst = P.cstep, rst = P.rstep;
+    asm volatile("" ::"s"(src), "s"(wt), "s"(spx), "s"(hs), "s"(ws), "s"(cs), "s"(nout), "s"(halo), "s"(gsh),
+                 "s"(gsw), "s"(kt), "s"(tw), "s"(t0), "s"(cst), "s"(rst), "s"(Ge.m), "s"(Ge.gh), "s"(Ge.gw),
+                 "s"(Ge.th), "s"(Ge.dh0), "s"(Ge.dw0), "s"(Ge.tsh), "s"(Ge.tsw), "s"(Ge.div_gw.mul),
+                 "s"(Ge.div_gw.shift), "s"(Ge.div_ghw.mul), "s"(Ge.div_ghw.shift));
+  }
   const int m0 = T.mt * BM;
-  if (m0 >= P.m) return;  // this phase has fewer tiles; uniform exit before any barrier
+  if (m0 >= Ge.m) return;  // this phase has fewer tiles; uniform exit before any barrier
   const int n0 = T.nt * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -561,7 +580,6 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   const int lrow = lane / CPR;
   const int kc = (lane % CPR) ^ (((wave * RPI + lrow) / WIN) % CPR);
 
-  const Geo Ge = load_geo(P);
   const uint32_t img0 = fdiv((uint32_t)m0, Ge.div_ghw);
   const __amdgpu_buffer_rsrc_t rsA =
       buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
