@@ -1,5 +1,5 @@
 // Auxiliary kernels of the convolution passes on gfx950: the fixed-order merge of the
-// forward's per-tile batch-statistics partials, the data-gradient weight re-layout, the
+// forward's per-tile batch-statistics partials, the data-gradient weight re-layouts, the
 // 8-channel repacking that lets a 3-channel image input use the weight-gradient kernel,
 // and the direct data gradient of such an input.
 #include "kernels.h"
@@ -165,8 +165,8 @@ hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int
 
 // ---------------------------------------------------------------------------
 // 8-channel repacking: dst[i][0..7] = (src[i*src_pix + c] for c < ci, then zeros).  Used
-// for the image input (ci = 3) and its weights, so the forward and the weight gradient
-// run on the 16-byte-vector kernels.
+// for the image input (ci = 3) of the weight gradient, so it runs on the 16-byte-vector
+// kernel; unpack_dw_kernel then keeps the ci real columns of the 8-column result.
 
 namespace {
 
@@ -189,18 +189,6 @@ __global__ void unpack_dw_kernel(const float* dw8, float* dw, int64_t rows, int 
   }
 }
 
-// dst[i*dst_pix + c] (+)= src[i][c] for c < ci: the narrow channels of an 8-channel bf16
-// tensor (the data gradient of a 3-channel input, which the GEMM writes padded to 8)
-__global__ void unpack8_kernel(const uint4* src, int ci, int64_t n, bf16_t* dst, int64_t dst_pix) {
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const uint4 v = src[i];
-    const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-      if (c < ci) dst[i * dst_pix + c] = (bf16_t)(wd[c >> 1] >> (16 * (c & 1)));
-  }
-}
-
 int blocks_for(int64_t n) {
   int64_t b = (n + 255) / 256;
   if (b > 16384) b = 16384;
@@ -212,14 +200,6 @@ int blocks_for(int64_t n) {
 hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s) {
   trace_begin(KC_PACK, s);
   hipLaunchKernelGGL(pack8_kernel, dim3(blocks_for(n)), dim3(256), 0, s, src, src_pix, ci, n, reinterpret_cast<uint4*>(dst));
-  trace_end(KC_PACK, s);
-  return hipGetLastError();
-}
-
-hipError_t unpack8_launch(const bf16_t* src8, int ci, int64_t n, bf16_t* dst, int64_t dst_pix, hipStream_t s) {
-  trace_begin(KC_PACK, s);
-  hipLaunchKernelGGL(unpack8_kernel, dim3(blocks_for(n)), dim3(256), 0, s, reinterpret_cast<const uint4*>(src8), ci, n, dst,
-                     dst_pix);
   trace_end(KC_PACK, s);
   return hipGetLastError();
 }

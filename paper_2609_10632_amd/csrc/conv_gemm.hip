@@ -2,18 +2,20 @@
 //
 // Computes the GEMM family described with ConvGemmArgs: the forward convolution (one
 // phase) and all stride phases of a data gradient (one launch, blockIdx.z = phase).
-// Two kernels:
+// Three kernels:
 //  * convdma_kernel, for source channel counts that are multiples of 16 and at least 32
 //    (every layer of the detector but the image input): both operands reach LDS through
 //    loads that write LDS directly, in 2 or 3 stages;
-//  * convgemm_kernel, for any channel count that is a multiple of 8 (the image input,
-//    repacked to 8 channels): each wave loads its own MFMA A fragments (16 contiguous
-//    bytes per lane) from global memory into a register ring several steps deep; only
-//    the weight tile B, shared by the four waves, goes through LDS.  Every row keeps a
+//  * convgemm_kernel, for any other channel count that is a multiple of 8 (and tiles
+//    whose address span exceeds 31 bits): each wave loads its own MFMA A fragments (16
+//    contiguous bytes per lane) from global memory into a register ring several steps
+//    deep; only the weight tile B, shared by the four waves, goes through LDS;
+//  * convnarrow_kernel, forward only, for fewer than 8 channels (the RGB image): the
+//    reduction (tap, channel) is packed densely and gathered element by element.  Every row keeps a
 //    pointer to its source pixel and a bitmask of the taps that land inside the image;
 //    padding lanes read a zero constant, so every step issues the same loads and waits
 //    are counted exactly.
-// Both use 32x32x16 MFMAs (the full-rate bf16 form on gfx950) with 4 waves split along M,
+// All use 32x32x16 MFMAs (the full-rate bf16 form on gfx950) with 4 waves split along M,
 // and share one epilogue: optional per-tile batch-statistics partials, then fp32 results
 // staged through LDS and written as 16-byte vectors of 8 channels (bf16, rounded once,
 // after the optional accumulate).

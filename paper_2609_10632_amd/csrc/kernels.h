@@ -100,7 +100,6 @@ hipError_t convnarrow_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_
 // from a weight gradient computed on the repacked layout
 hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s);
 hipError_t unpack_dw_launch(const float* dw8, float* dw, int64_t rows, int ci, int accumulate, hipStream_t s);
-hipError_t unpack8_launch(const bf16_t* src8, int ci, int64_t n, bf16_t* dst, int64_t dst_pix, hipStream_t s);
 
 // data gradient of a narrow input (ci < 8), one thread per input pixel
 struct NarrowDgradArgs {
