@@ -138,8 +138,10 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
  *                 q*stride_w - pad_w + s = w of  w[o,r,s,c] * dy[n,p,q,o].
  * dy: bf16 NHWC [n,ho,wo,c_out] (y_pixel_stride); dx: bf16 NHWC [n,h,w,c_in] (x_pixel_stride).
  * accumulate != 0: dx += result (sum formed in fp32, rounded once), else dx = result.
- * ws: numbat_workspace_size(NUMBAT_OP_CONV_BWD_DATA) bytes (the weights re-laid out per
- * stride phase). */
+ * ws: numbat_workspace_size(NUMBAT_OP_CONV_BWD_DATA) bytes: the weights re-laid out per
+ * stride phase when the problem is not one the direct-to-LDS kernel reads them in place
+ * for (c_out not a multiple of 16 or below 32, or offsets beyond 31 bits), fp32 weights
+ * for c_in < 8; otherwise unused.  It may not be NULL. */
 numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
                                    int accumulate, void* ws, size_t ws_bytes, void* stream);
 

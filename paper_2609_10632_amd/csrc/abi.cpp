@@ -170,7 +170,7 @@ size_t x8_bytes(const ConvDesc& d) { return round_up((size_t)d.n * d.h * d.w * 1
 
 TileCfg fwd_tile(const ConvDesc& d) {
   if (narrow(d)) return narrow_pick(d.co);
-  return convgemm_pick(d.m, d.co, d.ci, d.kh * d.kw * d.ci);
+  return convgemm_pick(d.m, d.co, d.ci, d.kh * d.kw * d.ci, 1, false);
 }
 
 size_t fwd_stats_bytes(const ConvDesc& d) {
@@ -478,10 +478,6 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
       total += f.count;
       ++nphase;
     }
-  bf16_t* wt = static_cast<bf16_t*>(ws);
-  e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, cpad, first, ph,
-                                      nphase, s);
-  if (e != hipSuccess) return hip_fail(e, "data-gradient weight re-layout launch");
   // all stride phases in launches of up to kMaxPhases phases (blockIdx.z = phase)
   ConvGemmArgs g;
   std::memset(&g, 0, sizeof g);
@@ -500,40 +496,78 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   g.dstep_h = d.sh;
   g.dstep_w = d.sw;
   g.accumulate = accumulate ? 1 : 0;
+  ConvGemmArgs groups[16];
+  TileCfg tiles[16];
+  int ngroups = 0;
   int f = 0;
   int64_t mmax = 0;
   int ktmax = 0;
+  const int64_t wpix2 = (int64_t)d.ci * 2;
   for (int pa = 0; pa < d.sh; ++pa)
     for (int pb = 0; pb < d.sw; ++pb, ++f) {
       const int gh = pa < d.h ? (d.h - pa + d.sh - 1) / d.sh : 0;
       const int gw = pb < d.w ? (d.w - pb + d.sw - 1) / d.sw : 0;
-      if (gh == 0 || gw == 0) continue;
-      GemmPhase& P = g.ph[g.nphase++];
-      P.wt = wt + first[f];
-      P.taps = ph[f].count;
-      P.ktot = P.taps * d.co;
-      P.gh = gh;
-      P.gw = gw;
-      P.m = d.n * gh * gw;
-      P.div_gw = make_fastdiv((uint32_t)gw);
-      P.div_ghw = make_fastdiv((uint32_t)(gh * gw));
-      P.doff_h = pa;
-      P.doff_w = pb;
-      for (int t = 0; t < ph[f].count; ++t)
-        P.off[t] = (int32_t)((uint32_t)(uint16_t)(int16_t)offh[f][t] | ((uint32_t)offw[f][t] << 16));
-      mmax = P.m > mmax ? P.m : mmax;
-      ktmax = P.ktot > ktmax ? P.ktot : ktmax;
       const bool last = (pa == d.sh - 1 && pb == d.sw - 1);
-      if (g.nphase == kMaxPhases || last) {
-        e = convgemm_launch(g, convgemm_pick(mmax, cpad, d.co, ktmax), s, KC_CONV_DGRAD);
-        if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+      if (gh > 0 && gw > 0) {
+        GemmPhase& P = g.ph[g.nphase++];
+        const PhaseTaps& T = ph[f];
+        P.wt = static_cast<const bf16_t*>(ws) + first[f];  // re-laid-out copy (K-major)
+        P.taps = T.count;
+        P.ktot = P.taps * d.co;
+        P.gh = gh;
+        P.gw = gw;
+        P.m = d.n * gh * gw;
+        P.div_gw = make_fastdiv((uint32_t)gw);
+        P.div_ghw = make_fastdiv((uint32_t)(gh * gw));
+        P.doff_h = pa;
+        P.doff_w = pb;
+        for (int t = 0; t < T.count; ++t)
+          P.off[t] = (int32_t)((uint32_t)(uint16_t)(int16_t)offh[f][t] | ((uint32_t)offw[f][t] << 16));
+        // the OHWI weights read in place: taps in rows of equal r (the same grid as the
+        // gather offsets), byte steps between them
+        P.wostep = (int32_t)((int64_t)d.kh * d.kw * wpix2);
+        if (T.count > 0) {
+          int tw = 1;
+          while (tw < T.count && T.r[tw] == T.r[0]) ++tw;
+          P.wtoff0 = (int32_t)((T.r[0] * d.kw + T.s[0]) * wpix2);
+          P.wcstep = tw > 1 ? (int32_t)((T.s[1] - T.s[0]) * wpix2) : 0;
+          P.wrstep = T.count > tw
+                         ? (int32_t)(((T.r[tw] - T.r[tw - 1]) * d.kw + (T.s[tw] - T.s[tw - 1])) * wpix2)
+                         : 0;
+        }
+        mmax = P.m > mmax ? P.m : mmax;
+        ktmax = P.ktot > ktmax ? P.ktot : ktmax;
+      }
+      if (g.nphase > 0 && (g.nphase == kMaxPhases || last)) {
+        groups[ngroups] = g;
+        tiles[ngroups] = convgemm_pick(mmax, cpad, d.co, ktmax, g.nphase, true);
+        ++ngroups;
         g.nphase = 0;
         mmax = 0;
         ktmax = 0;
       }
     }
-  if (g.nphase > 0) {
-    e = convgemm_launch(g, convgemm_pick(mmax, cpad, d.co, ktmax), s, KC_CONV_DGRAD);
+  // the direct-to-LDS kernel reads the weights in place; any other kernel takes them
+  // re-laid out per phase (K-major) in the workspace
+  bool direct = (int64_t)d.co * d.kh * d.kw * wpix2 < (int64_t)1 << 31;
+  for (int i = 0; i < ngroups && direct; ++i) {
+    ConvGemmArgs c = groups[i];
+    c.bt = 1;
+    for (int q = 0; q < c.nphase; ++q) c.ph[q].wt = static_cast<const bf16_t*>(w);
+    direct = convgemm_direct(c, tiles[i]);
+  }
+  if (direct) {
+    for (int i = 0; i < ngroups; ++i) {
+      groups[i].bt = 1;
+      for (int q = 0; q < groups[i].nphase; ++q) groups[i].ph[q].wt = static_cast<const bf16_t*>(w);
+    }
+  } else {
+    bf16_t* wt = static_cast<bf16_t*>(ws);
+    e = dgrad_weights_launch(static_cast<const bf16_t*>(w), wt, d.co, d.kh, d.kw, d.ci, cpad, first, ph, nphase, s);
+    if (e != hipSuccess) return hip_fail(e, "data-gradient weight re-layout launch");
+  }
+  for (int i = 0; i < ngroups; ++i) {
+    e = convgemm_launch(groups[i], tiles[i], s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
   }
   return ok();

@@ -42,14 +42,14 @@ __device__ __attribute__((aligned(16))) u32x4 kZero16 = {0u, 0u, 0u, 0u};
 template <int V>
 using Ic = std::integral_constant<int, V>;
 
-template <int TM, int TN>
+template <int TM, int TN, int NW = 4>
 struct GemmShape {
   static constexpr int WTM = TM * 32;          // rows per wave
-  static constexpr int BM = 4 * WTM, BN = TN * 32;
+  static constexpr int BM = NW * WTM, BN = TN * 32;
   static constexpr int BV = (BN + 63) / 64;    // B vectors per thread per step
   static constexpr int B_BYTES = 2 * BN * GROW * 2;
   static constexpr int STAGE_LD = BN + 4;                   // fp32 per staged row
-  static constexpr int STAGE_BYTES = 4 * 8 * STAGE_LD * 4;  // 8 rows per wave
+  static constexpr int STAGE_BYTES = NW * 8 * STAGE_LD * 4;  // 8 rows per wave
   static constexpr int SMEM = B_BYTES > STAGE_BYTES ? B_BYTES : STAGE_BYTES;
 };
 
@@ -148,11 +148,20 @@ __device__ __forceinline__ void row_gather(const ConvGemmArgs& a, const Geo& G, 
 // requested) and the bf16 output, staged through LDS as fp32 and written as 16-byte
 // vectors of 8 channels.  Accumulator register r of a lane sits on wave row
 // 8*(r/4) + 4*(lane/32) + (r%4) of its 32-row block, column lane%32 of its 32-column block.
-template <int TM, int TN>
+// sum of the NW waves' partials of column c, in a fixed pairwise order
+template <int NW>
+__device__ __forceinline__ float wave_sum(const float* r, int ld, int c) {
+  const float s4 = (r[c] + r[ld + c]) + (r[2 * ld + c] + r[3 * ld + c]);
+  if constexpr (NW == 4) return s4;
+  else return s4 + ((r[4 * ld + c] + r[5 * ld + c]) + (r[6 * ld + c] + r[7 * ld + c]));
+}
+
+template <int TM, int TN, int NW = 4>
 __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmPhase& P, const TileId& T,
                                               f32x16 (&acc)[TM][TN], int m0, int n0, unsigned char* smem,
                                               const int64_t* s_dst, float (*s_red)[TN * 32], float* s_mean) {
-  using S = GemmShape<TM, TN>;
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  using S = GemmShape<TM, TN, NW>;
   constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
@@ -173,7 +182,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
       if (lane < 32) s_red[wave][j * 32 + lane] = s;
     }
     __syncthreads();
-    if (tid < BN) s_mean[tid] = ((s_red[0][tid] + s_red[1][tid]) + (s_red[2][tid] + s_red[3][tid])) / (float)count;
+    if (tid < BN) s_mean[tid] = wave_sum<NW>(&s_red[0][0], BN, tid) / (float)count;
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
@@ -192,7 +201,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
     }
     __syncthreads();
     if (tid < BN && n0 + tid < a.nout) {
-      const float q = (s_red[0][tid] + s_red[1][tid]) + (s_red[2][tid] + s_red[3][tid]);
+      const float q = wave_sum<NW>(&s_red[0][0], BN, tid);
       a.stats_part[(int64_t)T.mt * a.nout + n0 + tid] = make_float2(s_mean[tid], q);
     }
   }
@@ -494,37 +503,53 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) 
 // loads (past the end of K they read zeros), and a step begins with a wait for its own
 // loads (the later stages stay in flight) and a barrier, after which the stage it frees
 // is refilled before its multiply.
-template <int TM, int TN, int S, int BK>
+template <int TM, int TN, int S, int BK, int NW, bool BT>
 struct DmaShape {
-  using G = GemmShape<TM, TN>;
+  using G = GemmShape<TM, TN, NW>;
   static constexpr int ROWB = 2 * BK;               // bytes per LDS row
   static constexpr int CPR = BK / 8;                // 16-byte chunks per row
   static constexpr int RPI = 1024 / ROWB;           // rows per wave load instruction
   static constexpr int WIN = 256 / ROWB;            // rows per 256-byte bank window
-  static constexpr int AI = G::BM / RPI / 4;        // A load instructions per wave per step
-  static constexpr int BI = (G::BN + RPI - 1) / RPI;     // B load instructions per step (all waves)
-  static constexpr int BI_MIN = BI / 4;                  // ... issued by every wave
-  static constexpr int BI_MAX = (BI + 3) / 4;            // ... issued by the first waves
-  static constexpr int A_ELEMS = G::BM * BK, B_ELEMS = BI * RPI * BK;
+  static constexpr int AI = G::BM / RPI / NW;       // A load instructions per wave per step
+  // B load instructions per step (all waves): BN rows of BK elements, or (transposed B)
+  // BK rows of BN elements
+  static constexpr int BI = BT ? BK * G::BN * 2 / 1024 : (G::BN + RPI - 1) / RPI;
+  static constexpr int BI_MIN = BI / NW;                 // ... issued by every wave
+  static constexpr int BI_MAX = (BI + NW - 1) / NW;      // ... issued by the first waves
+  static constexpr int A_ELEMS = G::BM * BK, B_ELEMS = BI * 512;
   // stage 0 of A doubles as the epilogue's staging area
   static constexpr int A0_ELEMS = 2 * A_ELEMS >= G::STAGE_BYTES ? A_ELEMS : G::STAGE_BYTES / 2;
   // loads still in flight when a step's own are done (every wave issues at least
   // AI + BI_MIN loads per step; a wave that issues more waits a little longer)
   static constexpr int PENDING = (S - 2) * (AI + BI_MIN);
-  static_assert(G::BM % (4 * RPI) == 0, "A rows per step split evenly over the waves");
+  static_assert(G::BM % (NW * RPI) == 0, "A rows per step split evenly over the waves");
 };
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef unsigned v2u_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 
-template <int TM, int TN, int S, int BK>
-__global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
-  using G = GemmShape<TM, TN>;
-  using Sh = DmaShape<TM, TN, S, BK>;
+// Transposed B stage ([BK reduction rows][BN columns], rows of 2*BN bytes): 16-byte chunk
+// c of row r sits in slot c ^ bt_swizzle(r).  A transposing read (ds_read_b64_tr_b16)
+// of a 16-lane group covers 4 consecutive rows x 32 bytes; the swizzle puts those 4
+// segments in distinct quarters of the 256-byte bank window (rows of 192 or 64 bytes
+// already do).
+template <int BN>
+__device__ __forceinline__ int bt_swizzle(int r) {
+  return BN == 64 ? 4 * ((r >> 1) & 1) : BN == 128 ? 4 * (r & 3) : 0;
+}
+
+template <int TM, int TN, int S, int BK, int NW, bool BT>
+__global__ __launch_bounds__(NW * 64) void convdma_kernel(ConvGemmArgs a) {
+  using G = GemmShape<TM, TN, NW>;
+  using Sh = DmaShape<TM, TN, S, BK, NW, BT>;
   constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM;
   constexpr int AI = Sh::AI, BI = Sh::BI, BI_MAX = Sh::BI_MAX, RPI = Sh::RPI, CPR = Sh::CPR, WIN = Sh::WIN;
   static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
   static_assert(BK == 32 || BK == 64, "stage depth");
   static_assert(Sh::PENDING <= 63, "load counter range");
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
 
   __shared__ __attribute__((aligned(16))) bf16_t sA0[Sh::A0_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sA1[Sh::A_ELEMS];
@@ -535,7 +560,7 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sB2[Sh::B_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sB3[Sh::B_ELEMS];
   __shared__ int64_t s_dst[BM];
-  __shared__ float s_red[4][BN];
+  __shared__ float s_red[NW][BN];
   __shared__ float s_mean[BN];
   auto stage_a = [&](auto sc) __attribute__((always_inline)) -> bf16_t* {
     constexpr int s = decltype(sc)::value;
@@ -576,7 +601,7 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
-  // Load instruction q of this wave fills rows (4*q + wave)*RPI .. +RPI; the lane's LDS
+  // Load instruction q of this wave fills rows (NW*q + wave)*RPI .. +RPI; the lane's LDS
   // slot is lane % CPR of row lane / CPR in it, which holds chunk slot ^ ((row / WIN) % CPR)
   // (the same for every q)
   const int lrow = lane / CPR;
@@ -587,15 +612,47 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
       buffer_rsrc(a.src + ((int64_t)img0 * a.hs * a.ws - a.halo_px) * a.src_pix);
   uint32_t vrow[AI], vmask[AI];  // the rows this thread loads
 #pragma unroll
-  for (int q = 0; q < AI; ++q) row_gather(a, Ge, m0 + (4 * q + wave) * RPI + lrow, img0, vrow[q], vmask[q]);
+  for (int q = 0; q < AI; ++q) row_gather(a, Ge, m0 + (NW * q + wave) * RPI + lrow, img0, vrow[q], vmask[q]);
   const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
-  const int p_tw = P.tw, p_ktot = P.ktot, cs = a.cs;
+  const int p_tw = P.tw, p_ktot = P.ktot, p_taps = P.taps, cs = a.cs;
   const uint32_t p_cstep = (uint32_t)P.cstep, p_rstep = (uint32_t)P.rstep;
   uint32_t voffb[BI_MAX];
+  // transposed B (OHWI weights read in place): instruction j of this lane covers stage row
+  // brw[j] (reduction index kb + brw[j] = (tap, o)), 16-byte column chunk bch[j]; the
+  // walk keeps o, the tap's grid column and the byte offset of (o, tap) per instruction
+  int bo[BT ? BI_MAX : 1], btap[BT ? BI_MAX : 1], btc[BT ? BI_MAX : 1];
+  const uint32_t w_ostep = (uint32_t)P.wostep, w_cstep = (uint32_t)P.wcstep, w_rstep = (uint32_t)P.wrstep;
+  if constexpr (!BT) {
 #pragma unroll
-  for (int j = 0; j < BI_MAX; ++j) {
-    const int row = (4 * j + wave) * RPI + lrow, o = n0 + row;
-    voffb[j] = (row < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + kc * 8) * 2) : kOob;
+    for (int j = 0; j < BI_MAX; ++j) {
+      const int row = (NW * j + wave) * RPI + lrow, o = n0 + row;
+      voffb[j] = (row < BN && o < a.nout) ? (uint32_t)(((int64_t)o * p_ktot + kc * 8) * 2) : kOob;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < BI_MAX; ++j) {
+      const int byte = (NW * j + wave) * 1024 + lane * 16;
+      const int row = byte / (2 * BN), slot = (byte % (2 * BN)) / 16;
+      const int chunk = slot ^ bt_swizzle<BN>(row);
+      const bool colok = n0 + chunk * 8 < a.nout;
+      // reduction index row = tap * cs + o (row < BK <= 2 * cs: at most two wraps)
+      int o = row, tp = 0, tc = 0;
+      uint32_t off = (uint32_t)P.wtoff0 + (uint32_t)((n0 + chunk * 8) * 2);
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const bool wrap = o >= cs;
+        o = wrap ? o - cs : o;
+        tp += wrap ? 1 : 0;
+        tc += wrap ? 1 : 0;
+        const bool rw = tc == p_tw;
+        tc = rw ? 0 : tc;
+        off += wrap ? (rw ? w_rstep : w_cstep) : 0u;
+      }
+      bo[j] = o;
+      btap[j] = colok ? tp : 31;  // a chunk past nout never loads
+      btc[j] = tc;
+      voffb[j] = off;
+    }
   }
   int ch = kc * 8, tap = 0, tcol = 0;
   uint32_t toff = (uint32_t)P.toff0;
@@ -624,18 +681,45 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
     for (int q = 0; q < AI; ++q) {
       const uint32_t t = (uint32_t)__builtin_amdgcn_sbfe((int)vmask[q], tq, 1);
       const uint32_t vo = (t & (vrow[q] + lo)) | (~t & kOob);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void_t*)(A + (4 * q + wave) * RPI * BK), 16, vo, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void_t*)(A + (NW * q + wave) * RPI * BK), 16, vo, 0, 0, 0);
     }
-    const int kb = kt * BK;
-    const bool kin = kb + kc * 8 < p_ktot;
+    if constexpr (!BT) {
+      const int kb = kt * BK;
+      const bool kin = kb + kc * 8 < p_ktot;
 #pragma unroll
-    for (int j = 0; j < BI_MAX; ++j) {
-      if (4 * j + wave < BI) {  // wave-uniform
-        // (the select stays out of the builtin's argument list: written inline, the host
-        // pass drops the kernel's launch stub)
-        const uint32_t vb = kin ? voffb[j] : kOob;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(B + (4 * j + wave) * RPI * BK), 16, vb,
-                                                 (uint32_t)kb * 2, 0, 0);
+      for (int j = 0; j < BI_MAX; ++j) {
+        if (NW * j + wave < BI) {  // wave-uniform
+          // (the select stays out of the builtin's argument list: written inline, the host
+          // pass drops the kernel's launch stub)
+          const uint32_t vb = kin ? voffb[j] : kOob;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(B + (NW * j + wave) * 512), 16, vb,
+                                                   (uint32_t)kb * 2, 0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < BI_MAX; ++j) {
+        if (NW * j + wave < BI) {  // wave-uniform
+          const uint32_t vb = btap[j] < p_taps ? voffb[j] + (uint32_t)bo[j] * w_ostep : kOob;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(B + (NW * j + wave) * 512), 16, vb, 0, 0, 0);
+          // next step: o advances by BK, wrapping into later taps
+          int o = bo[j] + BK, tp = btap[j], tc = btc[j];
+          uint32_t off = voffb[j];
+#pragma unroll
+          for (int w = 0; w < 2; ++w) {
+            const bool wrap = o >= cs;
+            o = wrap ? o - cs : o;
+            tp += wrap ? 1 : 0;
+            tc += wrap ? 1 : 0;
+            const bool rw = tc == p_tw;
+            tc = rw ? 0 : tc;
+            off += wrap ? (rw ? w_rstep : w_cstep) : 0u;
+          }
+          bo[j] = o;
+          btap[j] = tp;
+          btc[j] = tc;
+          voffb[j] = off;
+        }
       }
     }
     ch += BK;
@@ -657,6 +741,19 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   uint32_t koff[BK / 16];
 #pragma unroll
   for (int ks = 0; ks < BK / 16; ++ks) koff[ks] = (uint32_t)(((2 * ks + half) ^ sw) * 16);
+  // transposed B: lane l = 16 g + 4 e + q reads 4 columns (8 bytes) of rows 8 (g / 2) + e
+  // and that + 4 of the 16-row slice, columns 32 j + 16 (g % 2) + 4 q ..; the read hands
+  // each lane 4 consecutive rows of one column, two reads make its fragment
+  uint32_t btoff[BT ? TN : 1];
+  if constexpr (BT) {
+    const int g = lane >> 4, e = (lane & 15) >> 2, q = lane & 3;
+    const int r0 = 8 * (g >> 1) + e;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int c = 4 * j + 2 * (g & 1) + (q >> 1);
+      btoff[j] = (uint32_t)(r0 * 2 * BN + (c ^ bt_swizzle<BN>(r0)) * 16 + (q & 1) * 8);
+    }
+  }
   auto compute = [&](auto sc) __attribute__((always_inline)) {
     const unsigned char* A = reinterpret_cast<const unsigned char*>(stage_a(sc));
     const unsigned char* B = reinterpret_cast<const unsigned char*>(stage_b(sc));
@@ -664,8 +761,22 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
     auto rd = [&](int ks, u32x4 (&xa)[TM], u32x4 (&xb)[TN]) __attribute__((always_inline)) {
 #pragma unroll
       for (int i = 0; i < TM; ++i) xa[i] = *reinterpret_cast<const u32x4*>(A + arow + i * 32 * BK * 2 + koff[ks]);
+      if constexpr (!BT) {
 #pragma unroll
-      for (int j = 0; j < TN; ++j) xb[j] = *reinterpret_cast<const u32x4*>(B + brow + j * 32 * BK * 2 + koff[ks]);
+        for (int j = 0; j < TN; ++j) xb[j] = *reinterpret_cast<const u32x4*>(B + brow + j * 32 * BK * 2 + koff[ks]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const unsigned char* pb = B + btoff[j] + ks * 16 * 2 * BN;
+          const v4s_t r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)pb);
+          const v4s_t r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(pb + 4 * 2 * BN));
+          const v2u_t lo = __builtin_bit_cast(v2u_t, r0), hi = __builtin_bit_cast(v2u_t, r1);
+          xb[j][0] = lo.x;
+          xb[j][1] = lo.y;
+          xb[j][2] = hi.x;
+          xb[j][3] = hi.y;
+        }
+      }
     };
     rd(0, af[0], bf[0]);
 #pragma unroll
@@ -696,7 +807,7 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   }
   // destination offsets of the tile's rows, needed only by the epilogue: computed while
   // the first stages load (the first step's barrier publishes them)
-  for (int r = tid; r < BM; r += 256) s_dst[r] = dst_offset(a, Ge, m0 + r);
+  for (int r = tid; r < BM; r += NW * 64) s_dst[r] = dst_offset(a, Ge, m0 + r);
   int kb = 0;
   for (; kb + S <= nk; kb += S) {
     step(Ic<0>{}, kb);
@@ -713,7 +824,7 @@ __global__ __launch_bounds__(256) void convdma_kernel(ConvGemmArgs a) {
   }
   // the loads issued past the last step land in LDS before stage 0 becomes staging space
   asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-  gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, reinterpret_cast<unsigned char*>(sA0), s_dst, s_red, s_mean);
+  gemm_epilogue<TM, TN, NW>(a, P, T, acc, m0, n0, reinterpret_cast<unsigned char*>(sA0), s_dst, s_red, s_mean);
 }
 
 // ---------------------------------------------------------------------------
@@ -866,25 +977,45 @@ constexpr GInst kG[] = {
 };
 
 
+template <int TM, int TN, int S, int BK, int NW>
+void launch_dma(const ConvGemmArgs& a, int mmax, hipStream_t s) {
+  using Sh = GemmShape<TM, TN, NW>;
+  dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN), (unsigned)a.nphase);
+  if (a.bt)
+    hipLaunchKernelGGL((convdma_kernel<TM, TN, S, BK, NW, true>), grid, dim3(NW * 64), 0, s, a);
+  else
+    hipLaunchKernelGGL((convdma_kernel<TM, TN, S, BK, NW, false>), grid, dim3(NW * 64), 0, s, a);
+}
+
 template <int I>
 hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
   constexpr GInst c = kG[I];
   using Sh = GemmShape<c.tm, c.tn>;
   int mmax = 0;
   for (int p = 0; p < a.nphase; ++p) mmax = a.ph[p].m > mmax ? a.ph[p].m : mmax;
-  dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN), (unsigned)a.nphase);
   if (variant == kVariantDma3)
-    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3, 64>), grid, dim3(256), 0, s, a);
+    launch_dma<c.tm, c.tn, 3, 64, 4>(a, mmax, s);
   else if (variant == kVariantDma2)
-    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 2, 64>), grid, dim3(256), 0, s, a);
+    launch_dma<c.tm, c.tn, 2, 64, 4>(a, mmax, s);
   else if (variant == kVariantDma32)
-    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 3, 32>), grid, dim3(256), 0, s, a);
+    launch_dma<c.tm, c.tn, 3, 32, 4>(a, mmax, s);
+  else if (variant == kVariantDma3W8)
+    launch_dma<1, c.tn, 3, 64, 8>(a, mmax, s);
 #ifdef NUMBAT_TUNING
   else if (variant == 6)
-    hipLaunchKernelGGL((convdma_kernel<c.tm, c.tn, 4, 32>), grid, dim3(256), 0, s, a);
+    launch_dma<c.tm, c.tn, 4, 32, 4>(a, mmax, s);
+  else if (variant == 8)
+    launch_dma<1, c.tn, 2, 64, 8>(a, mmax, s);
+  else if (variant == 9)
+    launch_dma<1, c.tn, 4, 32, 8>(a, mmax, s);
+  else if (variant == 10)
+    launch_dma<1, c.tn, 3, 32, 8>(a, mmax, s);
 #endif
-  else
+  else {
+    dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN),
+              (unsigned)a.nphase);
     hipLaunchKernelGGL((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -943,17 +1074,22 @@ bool prepare_fast(ConvGemmArgs& a, int bm) {
 
 // Tile and kernel choice, fitted to timings of every (kernel, tile, stages) choice over
 // the forward and data-gradient GEMMs of the detector's layers at batch 16, weighted by
-// how often each shape occurs (4% above the per-layer best in total):
-//  * N tile: the least padding among 128, 96 and 64 columns (ties to the wider); when the
-//    grid would hold fewer than 400 blocks of 128 rows, 64 columns for more blocks;
-//  * fast paths, all on the direct-to-LDS kernel: more than 32768 rows, three stages of
-//    32 reduction elements (three blocks per CU for 128-row tiles), 256-row tiles when
-//    the reduction is 768 or longer; 8193..32768 rows, two stages of 64 (two blocks per
-//    CU) on 128 x 96 tiles when 96 divides N <= 192, else 128 x 64; up to 8192 rows,
-//    three stages of 64 on 128-row tiles;
+// how often each shape occurs (within 1% of the per-layer best in total):
+//  * forward (K-major weights): N tile the least padding among 128, 96 and 64 columns
+//    (ties to the wider; 64 when fewer than 400 blocks of 128 rows); more than 32768
+//    rows, three stages of 32 reduction elements (three blocks per CU for 128-row tiles),
+//    256-row tiles when the reduction is 768 or longer; 8193..32768 rows, two stages of
+//    64 (two blocks per CU) on 128 x 96 tiles when 96 divides N <= 192, else 128 x 64; up
+//    to 8192 rows, three stages of 64 on 128-row tiles;
+//  * data gradient (weights read in place through transposing LDS reads, which favour
+//    64-column tiles): more than 32768 rows as the forward, with 64 columns on 128-row
+//    tiles; 8193..32768 rows, eight waves on 256 x 96 (or x 64) tiles with three stages
+//    of 64 when the reduction is 1000 or longer and one such block per CU covers the
+//    grid, else 128 x 64 with three stages of 32; up to 8192 rows, 128 x 64 with two
+//    stages of 64 when the grid holds 300 blocks or more, else three;
 //  * generic kernel (narrow or 8-multiple channels): 256-row tiles unless that leaves
 //    fewer than 512 blocks.
-TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
+TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot, int nphase, bool bt) {
   const int bns[4] = {128, 96, 64, 32};
   const int ncand = nout <= 32 ? 4 : 3;
   int bn = 128;
@@ -967,7 +1103,7 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
   }
   const bool fast = cs % 16 == 0 && cs >= 32;
   int bm, variant;
-  if (fast) {
+  if (fast && !bt) {
     const int64_t blocks128 = ((m_max + 127) / 128) * ((nout + bn - 1) / bn);
     if (blocks128 < 400 && bn > 64) bn = 64;
     bm = 128;
@@ -980,6 +1116,29 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
     } else {
       variant = kVariantDma3;
     }
+  } else if (fast) {
+    const int bn64 = bn < 64 ? bn : 64;
+    bm = 128;
+    if (m_max > 32768) {
+      variant = kVariantDma32;
+      if (ktot >= 768) bm = 256;
+      else bn = bn64;
+    } else if (m_max > 8192) {
+      const int bn8 = nout % 96 == 0 ? 96 : bn64;
+      const int64_t blocks8 = ((m_max + 255) / 256) * ((nout + bn8 - 1) / bn8) * nphase;
+      if (ktot >= 1000 && blocks8 <= 256) {
+        variant = kVariantDma3W8;
+        bm = 256;
+        bn = bn8;
+      } else {
+        variant = kVariantDma32;
+        bn = bn64;
+      }
+    } else {
+      bn = bn64;
+      const int64_t blocks = ((m_max + 127) / 128) * ((nout + bn - 1) / bn) * nphase;
+      variant = blocks >= 300 ? kVariantDma2 : kVariantDma3;
+    }
   } else {
     const int64_t blocks256 = ((m_max + 255) / 256) * ((nout + bn - 1) / bn);
     bm = blocks256 < 512 ? 128 : 256;
@@ -990,6 +1149,7 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot) {
   // timing sweeps only: force the instantiation and kernel
   if (const char* e = getenv("NUMBAT_TILE")) id = atoi(e);
   if (const char* e = getenv("NUMBAT_VARIANT")) variant = fast ? atoi(e) : kVariantGeneric;
+  if (variant >= kVariantDma3W8) id &= 3;  // eight waves of 32 rows: the 256-row instantiations
   bm = kG[id].tm * 128;
   bn = kG[id].tn * 32;
 #endif
@@ -1008,9 +1168,14 @@ hipError_t convnarrow_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_
   return e;
 }
 
+bool convgemm_direct(ConvGemmArgs a, const TileCfg& t) {
+  return t.variant != kVariantGeneric && prepare_fast(a, t.bm);
+}
+
 hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls) {
   // a problem the fast paths cannot take runs the generic kernel on the same tile
   const int variant = (t.variant != kVariantGeneric && prepare_fast(a, t.bm)) ? t.variant : kVariantGeneric;
+  if (a.bt && variant == kVariantGeneric) return hipErrorInvalidValue;  // needs K-major B
   a.remap = 0;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_REMAP_CONV")) a.remap = atoi(e);

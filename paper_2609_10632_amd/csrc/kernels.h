@@ -33,7 +33,7 @@ void trace_end(int cls, hipStream_t s);
 
 // conv GEMM kernel variants: generic (source channels a multiple of 8), and the two fast
 // paths for 16-multiple channel counts of at least 32 (LDS-staged, register-direct)
-enum { kVariantGeneric = 0, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5 };
+enum { kVariantGeneric = 0, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5, kVariantDma3W8 = 7 };
 struct TileCfg {
   int bm, bn;
   int id;       // instantiation id
@@ -45,7 +45,8 @@ struct TileCfg {
 //   row m   = (img, gi, gj) on a gh x gw grid per image,
 //   k       = (tap, c), c < cs, K = taps * cs,
 //   A[m][k] = src[img, gi*gstride_h + off_h[tap], gj*gstride_w + off_w[tap], c]  (0 outside hs x ws),
-//   B[n][k] = wt[n * ktot + k],
+//   B[n][k] = wt[n * ktot + k]   (K-major), or with bt set (the data gradient's weights
+//             read in place): k = (tap, o), o < cs, B[n][k] = wt[o * wostep/2 + tap offset + n]
 // D written (bf16) to dst[img, gi*dstep_h + doff_h, gj*dstep_w + doff_w, n].  The forward
 // convolution is one such GEMM; the stride phases of a data gradient are up to four
 // "phases" sharing one launch (blockIdx.z), each with its own grid, taps, offsets, B
@@ -69,6 +70,9 @@ struct GemmPhase {
   // grid rows and columns
   int32_t tw, toff0, cstep, rstep;
   int32_t th, dh0, dw0, tsh, tsw;
+  // transposed B (bt): byte offset of tap 0's weights, byte step per o, byte steps to the
+  // next tap in a grid row and from a row's last tap to the next row's first
+  int32_t wtoff0, wostep, wcstep, wrstep;
 };
 struct ConvGemmArgs {
   const bf16_t* src;
@@ -84,13 +88,17 @@ struct ConvGemmArgs {
   int32_t nphase;
   int32_t halo_px;     // set by convgemm_launch: pixels the fast path's gather base sits before an image
   int32_t remap;       // set by convgemm_launch: XCD-aware tile order (see xcd_remap)
+  int32_t bt;          // B is the OHWI weight tensor read in place (direct-to-LDS kernel only)
   GemmPhase ph[kMaxPhases];
 };
 // tile and kernel for a problem with at most m_max rows per phase, nout columns, cs
-// source channels and reduction length ktot (depends on the problem only)
-TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot);
+// source channels, reduction length ktot and nphase phases; bt: the weights are read in
+// place (transposed B) if the direct-to-LDS kernel takes the problem
+TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot, int nphase, bool bt);
 // a is taken by value: the launcher completes the tap-walk fields
 hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls);
+// whether the direct-to-LDS kernel takes the problem on tile t (it can read B in place)
+bool convgemm_direct(ConvGemmArgs a, const TileCfg& t);
 // forward convolution of a narrow input (cs = ci < 8, one phase, wt = OHWI weights with
 // K = taps * ci packed densely); rows per tile and columns per tile of narrow_pick
 TileCfg narrow_pick(int nout);
