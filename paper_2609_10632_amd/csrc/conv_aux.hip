@@ -349,7 +349,297 @@ __global__ __launch_bounds__(256) void dgrad_narrow_kernel(NarrowDgradArgs a, co
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Data gradient of a narrow input on MFMA, for c_out a multiple of 16 up to 64 and
+// kh*kw*ci <= 32 (the RGB image layer).  Per output-gradient pixel q the products with
+// every (tap, channel) form one small GEMM row,
+//   Z[q][(r, s, c)] = sum over o of dy[q][o] * W[o][r][s][c]   (N = kh*kw*ci <= 32, K = c_out),
+// and each input pixel p then sums the Z entries of the (q, r, s) that reach it:
+//   dx[p][c] = sum over (r, s) with p = q*stride - pad + (r, s) of Z[q][(r, s, c)].
+// A block owns a TH x TW patch of dx and loads the dy pixels its taps reach (the patch
+// plus a halo) once: [q][c_out] bf16 rows in LDS, the weights as [n = (r,s,c)][o].  Each
+// wave multiplies 32-row blocks of q with 32x32x16 MFMAs, the fp32 Z replaces dy in LDS,
+// and each thread sums the ci channels of its dx pixels (fp32, rounded once).
+constexpr int kNqMax = 192;   // dy pixels per block (six 32-row MFMA blocks)
+constexpr int kNarrowKp = 72; // bf16 per LDS row of dy and of the weights (c_out <= 64, odd multiple of 16 bytes)
+constexpr int kZp = 33;       // fp32 per LDS row of Z
+
+__device__ __forceinline__ int floordiv(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+
+// Patch geometry: image, first input row and column, and the dy rows/columns reached.
+struct NarrowPatch {
+  int img, i0, j0, i1, j1, qr0, qc0, nqc, nq;
+};
+__device__ __forceinline__ NarrowPatch narrow_patch(const NarrowDgradArgs& a, int pid, int th, int lgtw, int ntw,
+                                                    int nth, int kh, int kw, int sh, int sw) {
+  NarrowPatch P;
+  const int tj = pid % ntw, r = pid / ntw;
+  const int ti = r % nth;
+  P.img = r / nth;
+  P.i0 = ti * th;
+  P.j0 = tj << lgtw;
+  P.i1 = min(P.i0 + th, a.h);
+  P.j1 = min(P.j0 + (1 << lgtw), a.w);
+  const int qr0 = max(floordiv(P.i0 + a.ph - kh + 1 + sh - 1, sh), 0);
+  const int qc0 = max(floordiv(P.j0 + a.pw - kw + 1 + sw - 1, sw), 0);
+  const int qr1 = min(floordiv(P.i1 - 1 + a.ph, sh), a.ho - 1);
+  const int qc1 = min(floordiv(P.j1 - 1 + a.pw, sw), a.wo - 1);
+  P.qr0 = qr0;
+  P.qc0 = qc0;
+  P.nqc = max(qc1 - qc0 + 1, 0);
+  P.nq = max(qr1 - qr0 + 1, 0) * P.nqc;  // <= kNqMax (the host sizes the patch)
+  return P;
+}
+
+// Each block walks patches blockIdx.x, + gridDim.x, ...; the dy loads of its next patch
+// are in flight while it multiplies and sums the current one.  KS (square kernel side),
+// SS (square stride), TH, LGTW (patch rows, log2 patch columns) and CO are compile-time
+// for the RGB image layer and 0 (taken from the arguments) otherwise: the index
+// arithmetic, not the data, bounds this kernel.
+template <int CI, int KS, int SS, int TH, int LGTW, int CO>
+__global__ __launch_bounds__(256) void dgrad_narrow_mfma_kernel(NarrowDgradArgs a, int th_, int lgtw_, int ntw,
+                                                                int nth, int npatch) {
+  const int kh = KS ? KS : a.kh, kw = KS ? KS : a.kw, sh = SS ? SS : a.sh, sw = SS ? SS : a.sw;
+  const int th = TH ? TH : th_, lgtw = LGTW ? LGTW : lgtw_;
+  const int tw = 1 << lgtw;
+  __shared__ __attribute__((aligned(16))) unsigned char s_buf[kNqMax * kNarrowKp * 2 > kNqMax * kZp * 4
+                                                                  ? kNqMax * kNarrowKp * 2
+                                                                  : kNqMax * kZp * 4];
+  __shared__ __attribute__((aligned(16))) bf16_t s_w[32 * kNarrowKp];
+  bf16_t* s_dy = reinterpret_cast<bf16_t*>(s_buf);
+  float* s_z = reinterpret_cast<float*>(s_buf);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int nn = kh * kw * CI;
+  const int co = CO ? CO : a.co, cch = co >> 3, nks = co >> 4;
+  constexpr int kWLoads = 32 * 64 / 2 / 256;  // nn * co / 2 <= 1024 words
+  constexpr int kQLoads = kNqMax / 32;        // pixel rounds of 32
+  const int c8 = tid & 7;
+
+  // dy rows of a patch's reached pixels, 16-byte chunks: thread t loads chunk t % 8 of
+  // pixels t / 8, + 32, + 64, ... (walked without division)
+  auto load_dy = [&](const NarrowPatch& P, uint4 (&dv)[kQLoads]) __attribute__((always_inline)) {
+    const int nqc = max(P.nqc, 1);
+    int q = tid >> 3, qi = q / nqc, qj = q - qi * nqc;
+#pragma unroll
+    for (int u = 0; u < kQLoads; ++u) {
+      dv[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (c8 < cch && q < P.nq)
+        dv[u] = *reinterpret_cast<const uint4*>(a.dy + (((int64_t)P.img * a.ho + P.qr0 + qi) * a.wo + P.qc0 + qj) *
+                                                           a.dy_pix +
+                                                c8 * 8);
+      q += 32;
+      qj += 32;
+      while (qj >= nqc) {
+        qj -= nqc;
+        ++qi;
+      }
+    }
+  };
+
+  int pid = blockIdx.x;
+  NarrowPatch P = narrow_patch(a, pid, th, lgtw, ntw, nth, kh, kw, sh, sw);
+  uint4 dv[kQLoads];
+  load_dy(P, dv);
+  // weights as [n][o] (zero rows past nn): the OHWI tensor [o][n] is read contiguously
+  // (4-byte words: nn * co is even since co is) and scattered into LDS
+  {
+    const int nw = (nn * co) >> 1;
+    uint32_t wv[kWLoads];
+#pragma unroll
+    for (int u = 0; u < kWLoads; ++u) {
+      const int e = tid + 256 * u;
+      wv[u] = e < nw ? reinterpret_cast<const uint32_t*>(a.wt)[e] : 0u;
+    }
+    for (int e = tid; e < (32 - nn) * (kNarrowKp / 2); e += 256)
+      reinterpret_cast<uint32_t*>(s_w + nn * kNarrowKp)[e] = 0u;
+#pragma unroll
+    for (int u = 0; u < kWLoads; ++u) {
+      const int e = tid + 256 * u;
+      if (e < nw) {
+        const int o = (2 * e) / nn, n = 2 * e - o * nn;
+        s_w[n * kNarrowKp + o] = (bf16_t)(wv[u] & 0xffffu);
+        const int n1 = n + 1 < nn ? n + 1 : 0, o1 = n + 1 < nn ? o : o + 1;
+        s_w[n1 * kNarrowKp + o1] = (bf16_t)(wv[u] >> 16);
+      }
+    }
+  }
+
+  for (; pid < npatch; pid += gridDim.x) {
+    const int nqp = (P.nq + 31) & ~31;
+#pragma unroll
+    for (int u = 0; u < kQLoads; ++u) {
+      const int q = (tid >> 3) + 32 * u;
+      if (c8 < cch && q < nqp) *reinterpret_cast<uint4*>(&s_dy[q * kNarrowKp + c8 * 8]) = dv[u];
+    }
+    __syncthreads();
+    const int nxt = pid + (int)gridDim.x;
+    const NarrowPatch Pn = narrow_patch(a, nxt < npatch ? nxt : pid, th, lgtw, ntw, nth, kh, kw, sh, sw);
+    if (nxt < npatch) load_dy(Pn, dv);
+
+    // Z blocks: wave w takes 32-row blocks w and w + 4 (all fragments read before the
+    // first multiply; rows past the patch's pixels are zero)
+    f32x16 acc[2];
+    const int nblk = nqp >> 5;
+    u32x4 bfr[4], af[2][4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      if (ks < nks) bfr[ks] = *reinterpret_cast<const u32x4*>(&s_w[l32 * kNarrowKp + ks * 16 + half * 8]);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int row = min(wave + 4 * u, kNqMax / 32 - 1) * 32 + l32;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        if (ks < nks) af[u][ks] = *reinterpret_cast<const u32x4*>(&s_dy[row * kNarrowKp + ks * 16 + half * 8]);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[u][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        if (ks < nks) acc[u] = mfma32x32x16(af[u][ks], bfr[ks], acc[u]);
+    }
+    __syncthreads();  // every dy read is done before Z overwrites it
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int blk = wave + 4 * u;
+      if (blk < nblk) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = blk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          s_z[row * kZp + l32] = acc[u][r];
+        }
+      }
+    }
+    __syncthreads();
+
+    if constexpr (SS == 2 && TH > 0 && LGTW > 0) {
+      // stride 2: wave w sums the input pixels of parity class (w / 2, w % 2), which all
+      // take the same taps (rows r = (i + ph) mod 2, + 2; columns alike), so the loops
+      // are uniform and every Z read of a pixel is issued before the first add (an
+      // out-of-range tap reads a clamped entry and adds nothing)
+      constexpr int TWC = (1 << LGTW) / 2, THC = TH / 2, RG = 64 / TWC;
+      static_assert(64 % TWC == 0, "class columns divide the wave");
+      const int ca = wave >> 1, cb = wave & 1;
+      const int r0 = (ca + a.ph) & 1, s0 = (cb + a.pw) & 1;
+      const int j = P.j0 + cb + 2 * (lane % TWC);
+      const int qlast = P.nq > 0 ? P.nq - 1 : 0;
+      for (int ri = lane / TWC; ri < THC; ri += RG) {
+        const int i = P.i0 + ca + 2 * ri;
+        if (i >= P.i1 || j >= P.j1) continue;
+        float zv[(KS + 1) / 2][(KS + 1) / 2][CI];
+        bool ok[(KS + 1) / 2][(KS + 1) / 2];
+#pragma unroll
+        for (int dr = 0; dr < (KS + 1) / 2; ++dr)
+#pragma unroll
+          for (int ds = 0; ds < (KS + 1) / 2; ++ds) {
+            const int r = r0 + 2 * dr, s = s0 + 2 * ds;
+            const int qi = (i + a.ph - r) >> 1, qj = (j + a.pw - s) >> 1;
+            ok[dr][ds] = r < KS && s < KS && qi >= 0 && qi < a.ho && qj >= 0 && qj < a.wo;
+            int q = (qi - P.qr0) * P.nqc + (qj - P.qc0);
+            q = ok[dr][ds] ? q : 0;
+            q = q < qlast ? q : qlast;
+            const int n = ok[dr][ds] ? (r * KS + s) * CI : 0;
+#pragma unroll
+            for (int c = 0; c < CI; ++c) zv[dr][ds][c] = s_z[q * kZp + n + c];
+          }
+        float sum[CI];
+#pragma unroll
+        for (int c = 0; c < CI; ++c) {
+          sum[c] = 0.f;
+#pragma unroll
+          for (int dr = 0; dr < (KS + 1) / 2; ++dr)
+#pragma unroll
+            for (int ds = 0; ds < (KS + 1) / 2; ++ds) sum[c] += ok[dr][ds] ? zv[dr][ds][c] : 0.f;
+        }
+        bf16_t* d = a.dx + (((int64_t)P.img * a.h + i) * a.w + j) * a.dx_pix;
+#pragma unroll
+        for (int c = 0; c < CI; ++c) {
+          const float v = a.accumulate ? sum[c] + bf2f(d[c]) : sum[c];
+          d[c] = (bf16_t)f2bf(v);
+        }
+      }
+    } else {
+      // each thread sums the CI channels of the input pixels of one patch column, in rows
+      // tid / tw, + 256 / tw, ...: the taps that reach row i are r = (i + ph) mod sh, + sh,
+      // ..., reading dy rows (i + ph) div sh, - 1, ... (columns alike)
+      {
+        const int jj = tid & (tw - 1);
+        const int j = P.j0 + jj, uj = j + a.pw;
+        const int qj0 = uj / sw, sj0 = uj - qj0 * sw;
+        const int rstep = 256 >> lgtw;
+        for (int i = P.i0 + (tid >> lgtw); i < P.i1 && j < P.j1; i += rstep) {
+          float sum[CI];
+#pragma unroll
+          for (int c = 0; c < CI; ++c) sum[c] = 0.f;
+          const int ui = i + a.ph;
+          const int qi0 = ui / sh, ri0 = ui - qi0 * sh;
+          for (int r = ri0, qi = qi0; r < kh && qi >= 0; r += sh, --qi) {
+            if (qi >= a.ho) continue;
+            const float* zr = s_z + (qi - P.qr0) * P.nqc * kZp + r * kw * CI;
+            for (int s = sj0, qj = qj0; s < kw && qj >= 0; s += sw, --qj) {
+              if (qj >= a.wo) continue;
+              const float* z = zr + (qj - P.qc0) * kZp + s * CI;
+#pragma unroll
+              for (int c = 0; c < CI; ++c) sum[c] += z[c];
+            }
+          }
+          bf16_t* d = a.dx + (((int64_t)P.img * a.h + i) * a.w + j) * a.dx_pix;
+#pragma unroll
+          for (int c = 0; c < CI; ++c) {
+            const float v = a.accumulate ? sum[c] + bf2f(d[c]) : sum[c];
+            d[c] = (bf16_t)f2bf(v);
+          }
+        }
+      }
+    }
+    __syncthreads();  // Z reads are done before the next patch's dy is stored
+    P = Pn;
+  }
+}
+
 hipError_t dgrad_narrow_launch(const NarrowDgradArgs& a, int ci, float* wf, hipStream_t s) {
+  // MFMA path: c_out a multiple of 16 up to 64, kh*kw*ci <= 32, 16-byte dy rows, 4-byte
+  // aligned weights; the patch is the largest of these whose reached dy pixels fit the block
+  if (a.co % 16 == 0 && a.co <= 64 && a.kh * a.kw * ci <= 32 && a.dy_pix % 8 == 0 &&
+      (reinterpret_cast<uintptr_t>(a.dy) & 15) == 0 && (reinterpret_cast<uintptr_t>(a.wt) & 3) == 0 && a.n <= 65535) {
+    static const int cand[][3] = {{8, 64, 6}, {4, 64, 6}, {8, 32, 5}, {4, 32, 5}, {8, 16, 4},
+                                  {4, 16, 4},  {2, 16, 4}, {2, 8, 3},  {1, 8, 3}};
+    int th = 0, tw = 0, lgtw = 0;
+    for (const auto& c : cand) {
+      const int qr = (c[0] - 1 + a.kh - 1) / a.sh + 1, qc = (c[1] - 1 + a.kw - 1) / a.sw + 1;
+      if (qr * qc <= kNqMax) {
+        th = c[0];
+        tw = c[1];
+        lgtw = c[2];
+        break;
+      }
+    }
+    const int ntw = tw > 0 ? (a.w + tw - 1) / tw : 0, nth = th > 0 ? (a.h + th - 1) / th : 0;
+    const int64_t npatch = (int64_t)ntw * nth * a.n;
+    if (npatch > 0 && npatch < 0x7fffffff) {
+      dim3 grid((unsigned)(npatch < 1280 ? npatch : 1280));  // five blocks per CU
+      trace_begin(KC_CONV_DGRAD, s);
+      const int np = (int)npatch;
+      if (ci == 3 && a.kh == 3 && a.kw == 3 && a.sh == 2 && a.sw == 2 && a.co == 48 && th == 8 && lgtw == 6) {
+        hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<3, 3, 2, 8, 6, 48>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np);
+      } else {
+        switch (ci) {
+          case 1: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<1, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 2: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<2, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 3: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<3, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 4: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<4, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 5: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<5, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 6: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<6, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 7: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<7, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          default: trace_end(KC_CONV_DGRAD, s); return hipErrorInvalidValue;
+        }
+      }
+      trace_end(KC_CONV_DGRAD, s);
+      return hipGetLastError();
+    }
+  }
   const int ghm = (a.h + a.sh - 1) / a.sh, gwm = (a.w + a.sw - 1) / a.sw;
   const int64_t blocks = ((int64_t)a.n * ghm * ((gwm + 63) / 64) + 3) / 4;  // 4 waves of 64 pixels
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;

@@ -43,6 +43,10 @@ CONV_CASES = [
     (1, 13, 17, 2, 32, 3, 3),
     (1, 12, 12, 6, 40, 5, 4),
     (3, 66, 70, 3, 48, 3, 2),
+    # narrow data gradients on MFMA: several patches with halos, ragged edges
+    (1, 37, 75, 3, 64, 3, 1),
+    (1, 41, 67, 2, 32, 3, 2),
+    (1, 20, 30, 1, 16, 5, 1),
 ]
 
 
