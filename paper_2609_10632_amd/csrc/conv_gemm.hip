@@ -954,6 +954,119 @@ __global__ __launch_bounds__(256) void convnarrow_kernel(ConvGemmArgs a) {
   gemm_epilogue<TM, TN>(a, P, T, acc, m0, n0, smem, s_dst, s_red, s_mean);
 }
 
+// ---------------------------------------------------------------------------
+// Forward convolution of the RGB image layer (3 channels, 3x3, stride 2, padding 1;
+// output rows a multiple of 4 and columns of 64): a block computes a 4 x 64 patch of
+// output pixels.  The 9 x 129 input pixels it reads are loaded once into LDS, each
+// padded to 4 channels (8 bytes, the fourth zero), and the reduction is ordered as
+// k = 16 r + 4 s + c (tap row r, tap column s, channel c; zero weights at c = 3 and
+// past s = 2), so the 8 consecutive k of an MFMA fragment are 16 aligned bytes of one
+// input row (s = 0, 1), or 8 bytes (s = 2) and four zeros.  Wave w owns output row w of
+// the patch.  The weights, as [o][k], stay in LDS; then the shared epilogue.
+constexpr int kStemCols = 129, kStemPitch = 130;  // input pixels per patch row, LDS pitch (pixels)
+constexpr int kStemKp = 56;                       // bf16 per weight row (48 + 8)
+
+__global__ __launch_bounds__(256) void convstem_kernel(ConvGemmArgs a) {
+  using G = GemmShape<2, 2>;
+  constexpr int BN = G::BN;
+  constexpr int PATCH = 9 * kStemPitch * 8;  // bytes
+  constexpr int SM = PATCH > G::STAGE_BYTES ? PATCH : G::STAGE_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[SM];
+  __shared__ __attribute__((aligned(16))) bf16_t s_w[BN * kStemKp];
+  __shared__ int64_t s_dst[256];
+  __shared__ float s_red[4][BN];
+  __shared__ float s_mean[BN];
+  const GemmPhase& P = a.ph[0];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  // tile: blockIdx.x = patch column, blockIdx.y = patch row, blockIdx.z = image
+  const int oj0 = blockIdx.x * 64, oi0 = blockIdx.y * 4, img = blockIdx.z;
+  const int ntc = P.gw >> 6, ntr = P.gh >> 2;
+  const TileId T{(int)((img * ntr + blockIdx.y) * ntc + blockIdx.x), 0, 0};
+  const int m0 = T.mt * 256;
+
+  // input patch: rows 2 oi0 - 1 + pr, columns 2 oj0 - 1 + pc; all loads first
+  constexpr int kPix = 9 * kStemCols, kRounds = (kPix + 255) / 256;
+  uint32_t lo[kRounds], hi[kRounds];
+#pragma unroll
+  for (int u = 0; u < kRounds; ++u) {
+    const int e = tid + 256 * u;
+    const int pr = e / kStemCols, pc = e - pr * kStemCols;
+    const int ih = 2 * oi0 - 1 + pr, iw = 2 * oj0 - 1 + pc;
+    lo[u] = hi[u] = 0u;
+    if (e < kPix && (unsigned)ih < (unsigned)a.hs && (unsigned)iw < (unsigned)a.ws) {
+      const bf16_t* px = a.src + (((int64_t)img * a.hs + ih) * a.ws + iw) * a.src_pix;
+      lo[u] = (uint32_t)px[0] | ((uint32_t)px[1] << 16);
+      hi[u] = (uint32_t)px[2];
+    }
+  }
+  // weights [o][k = 16 r + 4 s + c] from OHWI [o][r][s][c]: zeros first, then the
+  // tensor read contiguously (2-byte elements, loads issued before the stores)
+  for (int e = tid; e < BN * kStemKp / 2; e += 256) reinterpret_cast<uint32_t*>(s_w)[e] = 0u;
+  constexpr int kWRounds = 64 * 27 / 256 + 1;
+  bf16_t wv[kWRounds];
+  const int nwt = a.nout * 27;
+#pragma unroll
+  for (int u = 0; u < kWRounds; ++u) {
+    const int e = tid + 256 * u;
+    wv[u] = e < nwt ? P.wt[e] : (bf16_t)0;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kWRounds; ++u) {
+    const int e = tid + 256 * u;
+    if (e < nwt) {
+      const int o = e / 27, k = e - o * 27;
+      const int r = k / 9, sc = k - r * 9, s = sc / 3, c = sc - s * 3;
+      s_w[o * kStemKp + r * 16 + s * 4 + c] = wv[u];
+    }
+  }
+  for (int r = tid; r < 256; r += 256) {
+    const int oi = oi0 + (r >> 6), oj = oj0 + (r & 63);
+    s_dst[r] = (((int64_t)img * a.hd + oi) * a.wd + oj) * a.dst_pix;
+  }
+#pragma unroll
+  for (int u = 0; u < kRounds; ++u) {
+    const int e = tid + 256 * u;
+    if (e < kPix) {
+      const int pr = e / kStemCols, pc = e - pr * kStemCols;
+      *reinterpret_cast<uint2*>(smem + (pr * kStemPitch + pc) * 8) = make_uint2(lo[u], hi[u]);
+    }
+  }
+  __syncthreads();
+
+  // A fragment of output pixel (row wave, column 32 i + l32), tap row ks: input patch row
+  // 2 wave + ks, columns 2 oj + half * 2 (16 bytes: s = 0, 1) or + 2 (8 bytes: s = 2)
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < 3; ++ks) {
+    u32x4 af[2], bf[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const unsigned char* px = smem + ((2 * wave + ks) * kStemPitch + 2 * (32 * i + l32)) * 8;
+      if (half == 0) {
+        af[i] = *reinterpret_cast<const u32x4*>(px);
+      } else {
+        const uint2 v = *reinterpret_cast<const uint2*>(px + 16);
+        af[i] = u32x4{v.x, v.y, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) bf[j] = *reinterpret_cast<const u32x4*>(&s_w[(j * 32 + l32) * kStemKp + ks * 16 + half * 8]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
+  }
+  gemm_epilogue<2, 2>(a, P, T, acc, m0, 0, smem, s_dst, s_red, s_mean);
+}
+
 template <int TN>
 hipError_t launch_narrow(const ConvGemmArgs& a, hipStream_t s) {
   using G = GemmShape<2, TN>;
@@ -1159,9 +1272,29 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot, int nphase, boo
 // narrow input (ci < 8): 256-row tiles, 32 or 64 columns
 TileCfg narrow_pick(int nout) { return TileCfg{256, nout <= 32 ? 32 : 64, -1, kVariantGeneric}; }
 
+// the RGB image layer's shape: 3 channels, 3x3 taps at offsets -1..1, stride 2, at most
+// 64 output channels, output rows a multiple of 4 and columns of 64, 256-row tiles
+bool stem_shape(const ConvGemmArgs& a, const TileCfg& t) {
+  const GemmPhase& P = a.ph[0];
+  if (a.nphase != 1 || a.cs != 3 || P.taps != 9 || a.gstride_h != 2 || a.gstride_w != 2 || a.nout > 64 ||
+      t.bm != 256 || P.gh % 4 != 0 || P.gw % 64 != 0 || a.nimg > 65535 || P.gh / 4 > 65535)
+    return false;
+  for (int r = 0; r < 3; ++r)
+    for (int q = 0; q < 3; ++q)
+      if (P.off[r * 3 + q] != (int32_t)((uint32_t)(uint16_t)(int16_t)(r - 1) | ((uint32_t)(q - 1) << 16))) return false;
+  return true;
+}
+
 hipError_t convnarrow_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s) {
   if (a.nphase != 1 || a.ph[0].ktot > NarrowShape<2, 2>::KMAX || a.ph[0].taps > kMaxTaps)
     return hipErrorInvalidValue;
+  if (stem_shape(a, t)) {
+    trace_begin(KC_CONV_FWD, s);
+    dim3 grid((unsigned)(a.ph[0].gw / 64), (unsigned)(a.ph[0].gh / 4), (unsigned)a.nimg);
+    hipLaunchKernelGGL(convstem_kernel, grid, dim3(256), 0, s, a);
+    trace_end(KC_CONV_FWD, s);
+    return hipGetLastError();
+  }
   trace_begin(KC_CONV_FWD, s);
   const hipError_t e = t.bn == 32 ? launch_narrow<1>(a, s) : launch_narrow<2>(a, s);
   trace_end(KC_CONV_FWD, s);

@@ -47,6 +47,9 @@ CONV_CASES = [
     (1, 37, 75, 3, 64, 3, 1),
     (1, 41, 67, 2, 32, 3, 2),
     (1, 20, 30, 1, 16, 5, 1),
+    # the image layer's forward kernel: 4 x 64 output patches
+    (2, 24, 256, 3, 48, 3, 2),
+    (1, 8, 128, 3, 32, 3, 2),
 ]
 
 
