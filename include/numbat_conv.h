@@ -151,7 +151,9 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
  * accumulate != 0: dw += result, else dw = result.  The sum over n*ho*wo rows is split into
  * fixed ranges reduced in a fixed order, so the result is bitwise reproducible.
  * ws: numbat_workspace_size(NUMBAT_OP_CONV_BWD_WEIGHT) bytes (split partials; for c_in < 8
- * also the input repacked to 8 channels). */
+ * also the input repacked to 8 channels, except for the RGB image layer's shape -- 3
+ * channels, 3x3, stride 2, padding 1, c_out <= 64 and a multiple of 8, output rows a
+ * multiple of 4 and columns of 64 -- whose kernel needs only its per-block partials). */
 numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x, const void* dy, float* dw,
                                      int accumulate, void* ws, size_t ws_bytes, void* stream);
 

@@ -190,7 +190,22 @@ size_t bwd_data_ws(const ConvDesc& d) {
 
 size_t dw8_bytes(const ConvDesc& d) { return round_up((size_t)d.co * d.kh * d.kw * 8 * sizeof(float), 256); }
 
+// the RGB image layer's shape, whose weight gradient has a kernel of its own
+bool stem_wgrad(const ConvDesc& d) {
+  return d.ci == 3 && d.kh == 3 && d.kw == 3 && d.sh == 2 && d.sw == 2 && d.ph == 1 && d.pw == 1 && d.co <= 64 &&
+         d.co % 8 == 0 && d.ho % 4 == 0 && d.wo % 64 == 0;
+}
+int64_t stem_wgrad_blocks(const ConvDesc& d) {
+  const int64_t np = (int64_t)d.n * (d.ho / 4) * (d.wo / 64);
+  return np < 512 ? np : 512;
+}
+
 size_t bwd_weight_ws(const ConvDesc& d, int* splits, int64_t* rps) {
+  if (stem_wgrad(d)) {  // per-block partials [blocks][c_out][27]
+    if (splits) *splits = 0;
+    if (rps) *rps = 0;
+    return round_up((size_t)stem_wgrad_blocks(d) * d.co * 27 * sizeof(float), 256);
+  }
   const int ci = narrow(d) ? 8 : d.ci;
   const int ktot = d.kh * d.kw * ci;
   int64_t r = 0;
@@ -597,6 +612,34 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   if (st != NUMBAT_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
+  if (stem_wgrad(d)) {
+    WgradArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.x = static_cast<const bf16_t*>(x);
+    a.x_pix = d.x_pix;
+    a.dy = static_cast<const bf16_t*>(dy);
+    a.dy_pix = d.y_pix;
+    a.n = d.n;
+    a.h = d.h;
+    a.w = d.w;
+    a.ci = d.ci;
+    a.co = d.co;
+    a.kh = d.kh;
+    a.kw = d.kw;
+    a.sh = d.sh;
+    a.sw = d.sw;
+    a.ph = d.ph;
+    a.pw = d.pw;
+    a.ho = d.ho;
+    a.wo = d.wo;
+    a.m = d.m;
+    a.ktot = 27;
+    a.out = dw;
+    a.accumulate = accumulate ? 1 : 0;
+    e = wgrad_stem_launch(a, static_cast<float*>(ws), s);
+    if (e != hipSuccess) return hip_fail(e, "image-layer weight-gradient launch");
+    return ok();
+  }
   const int ci = narrow(d) ? 8 : d.ci;
   const int ktot = d.kh * d.kw * ci;
   char* wsp = static_cast<char*>(ws);

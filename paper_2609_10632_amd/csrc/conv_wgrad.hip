@@ -470,4 +470,184 @@ hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, fl
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Weight gradient of the RGB image layer (3 channels, 3x3, stride 2, padding 1, at most
+// 64 output channels, a multiple of 8; output rows a multiple of 4 and columns of 64):
+//   dW[o][(r, s, c)] = sum over q of dy[q][o] * x[2 qi - 1 + r][2 qj - 1 + s][c].
+// A block walks 4 x 64 patches of q (the next patch's loads in flight): dy rows and the
+// 9 x 129 input pixels the patch reaches go to LDS once; the input pixels, padded to 4
+// channels, are expanded into the patch's reduction rows X[q][16 r + 4 s + c] (zero at
+// c = 3 and past s = 2), and dy^T X accumulates on 32x32x16 MFMAs whose operands come
+// out of the [q][64] tiles through transposing reads (the q-major layout and swizzle of
+// the general kernel).  Each wave takes a quarter of the patch's q; the waves' sums are
+// added in a fixed order and each block writes one partial [o][27] for the split
+// reduction.
+namespace {
+constexpr int kStemXCols = 129, kStemXPitch = 130;  // input pixels per patch row, LDS pitch
+
+__global__ __launch_bounds__(256) void wgrad_stem_kernel(WgradArgs a, int npatch, float* part) {
+  __shared__ __attribute__((aligned(16))) unsigned char s_tiles[2 * 256 * 128];  // dy, X; then wave sums
+  __shared__ __attribute__((aligned(16))) unsigned char s_x[9 * kStemXPitch * 8];
+  unsigned char* s_dy = s_tiles;
+  unsigned char* s_col = s_tiles + 256 * 128;
+  float* s_red = reinterpret_cast<float*>(s_tiles);  // [4][64][48]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5;
+  const int ntc = a.wo >> 6, ntr = a.ho >> 2;
+  const int cch = a.co >> 3;  // 16-byte dy chunks per pixel
+
+  // global loads of patch pid: dy chunk (q = tid / 8 + 32 u, chunk tid % 8), input pixels
+  // e = tid + 256 u of the 9 x 129 patch (three 2-byte channels each)
+  constexpr int kDyRounds = 256 * 8 / 256, kXPix = 9 * kStemXCols, kXRounds = (kXPix + 255) / 256;
+  uint4 dv[kDyRounds];
+  uint32_t xlo[kXRounds], xhi[kXRounds];
+  auto load = [&](int pid) __attribute__((always_inline)) {
+    const int tj = pid % ntc, rr = pid / ntc;
+    const int ti = rr % ntr, img = rr / ntr;
+    const int oi0 = ti * 4, oj0 = tj * 64;
+    const int c = tid & 7;
+#pragma unroll
+    for (int u = 0; u < kDyRounds; ++u) {
+      const int q = (tid >> 3) + 32 * u;
+      dv[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (c < cch)
+        dv[u] = *reinterpret_cast<const uint4*>(a.dy + (((int64_t)img * a.ho + oi0 + (q >> 6)) * a.wo + oj0 + (q & 63)) *
+                                                           a.dy_pix +
+                                                c * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < kXRounds; ++u) {
+      const int e = tid + 256 * u;
+      const int pr = e / kStemXCols, pc = e - pr * kStemXCols;
+      const int ih = 2 * oi0 - 1 + pr, iw = 2 * oj0 - 1 + pc;
+      xlo[u] = xhi[u] = 0u;
+      if (e < kXPix && (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w) {
+        const bf16_t* px = a.x + (((int64_t)img * a.h + ih) * a.w + iw) * a.x_pix;
+        xlo[u] = (uint32_t)px[0] | ((uint32_t)px[1] << 16);
+        xhi[u] = (uint32_t)px[2];
+      }
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // transposing-read offsets (the general kernel's): lane j of a 16-lane group reads 4
+  // channels of q row 4 rd + j / 4 of the slice's half; 32-channel block jb
+  const uint32_t rbase = (uint32_t)((8 * half + ((lane & 15) >> 2)) * 128 + (lane & 1) * 8);
+  const uint32_t slot0 = (uint32_t)((2 * ((lane >> 4) & 1) + ((lane >> 1) & 1)) ^ (4 * ((lane >> 3) & 1)));
+  const uint32_t toff[2] = {rbase + slot0 * 16, rbase + (slot0 ^ 4u) * 16};
+  auto frag = [&](const unsigned char* T, int jb, int ks) __attribute__((always_inline)) -> u32x4 {
+    const unsigned char* p = T + toff[jb] + ks * 16 * 128;
+    const v4s_t r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wlds_v4s_t*)p);
+    const v4s_t r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((wlds_v4s_t*)(p + 4 * 128));
+    const v2u_t lo = __builtin_bit_cast(v2u_t, r0), hi = __builtin_bit_cast(v2u_t, r1);
+    u32x4 f;
+    f[0] = lo.x;
+    f[1] = lo.y;
+    f[2] = hi.x;
+    f[3] = hi.y;
+    return f;
+  };
+
+  int pid = blockIdx.x;
+  if (pid < npatch) load(pid);
+  for (; pid < npatch; pid += gridDim.x) {
+    // stage: dy chunk c of row q in slot c ^ 4 ((q >> 1) & 1); input pixels padded to 4 channels
+    {
+      const int c = tid & 7;
+#pragma unroll
+      for (int u = 0; u < kDyRounds; ++u) {
+        const int q = (tid >> 3) + 32 * u;
+        if (c < cch) *reinterpret_cast<uint4*>(s_dy + q * 128 + ((c ^ (4 * ((q >> 1) & 1))) * 16)) = dv[u];
+      }
+#pragma unroll
+      for (int u = 0; u < kXRounds; ++u) {
+        const int e = tid + 256 * u;
+        if (e < kXPix) {
+          const int pr = e / kStemXCols, pc = e - pr * kStemXCols;
+          *reinterpret_cast<uint2*>(s_x + (pr * kStemXPitch + pc) * 8) = make_uint2(xlo[u], xhi[u]);
+        }
+      }
+    }
+    __syncthreads();
+    if (pid + (int)gridDim.x < npatch) load(pid + (int)gridDim.x);
+    // reduction rows: X[q][chunk 2r] = input pixels (2 qi + r, 2 qj .. 2 qj + 1),
+    // X[q][chunk 2r + 1] = pixel (2 qi + r, 2 qj + 2) and four zeros
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+      const int e = tid + 256 * u;  // (q, r) pairs: 768
+      const int q = e / 3, r = e - q * 3;
+      const unsigned char* src = s_x + ((2 * (q >> 6) + r) * kStemXPitch + 2 * (q & 63)) * 8;
+      const u32x4 v0 = *reinterpret_cast<const u32x4*>(src);
+      const uint2 v1 = *reinterpret_cast<const uint2*>(src + 16);
+      const int sw = 4 * ((q >> 1) & 1);
+      *reinterpret_cast<u32x4*>(s_col + q * 128 + (((2 * r) ^ sw) * 16)) = v0;
+      *reinterpret_cast<u32x4*>(s_col + q * 128 + (((2 * r + 1) ^ sw) * 16)) = u32x4{v1.x, v1.y, 0u, 0u};
+    }
+    __syncthreads();
+    // wave w: q slices w, w + 4, w + 8, w + 12 (16 q each)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int ks = wave + 4 * k;
+      const u32x4 a0 = frag(s_dy, 0, ks), a1 = frag(s_dy, 1, ks);
+      const u32x4 b0 = frag(s_col, 0, ks), b1 = frag(s_col, 1, ks);
+      acc[0][0] = mfma32x32x16(a0, b0, acc[0][0]);
+      acc[0][1] = mfma32x32x16(a0, b1, acc[0][1]);
+      acc[1][0] = mfma32x32x16(a1, b0, acc[1][0]);
+      acc[1][1] = mfma32x32x16(a1, b1, acc[1][1]);
+    }
+    __syncthreads();  // tiles are free for the next patch
+  }
+  // wave sums [o][n' < 48] in LDS, then a fixed-order sum over the waves per output
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int o = i * 32 + 8 * (r >> 2) + 4 * half + (r & 3), n = j * 32 + (lane & 31);
+        if (n < 48) s_red[(wave * 64 + o) * 48 + n] = acc[i][j][r];
+      }
+  __syncthreads();
+  const int nout = a.co * 27;
+  for (int e = tid; e < nout; e += 256) {
+    const int o = e / 27, k = e - o * 27;
+    const int r = k / 9, sc = k - r * 9, s = sc / 3, c = sc - s * 3;
+    const int n = 16 * r + 4 * s + c;
+    const float v = (s_red[(0 * 64 + o) * 48 + n] + s_red[(1 * 64 + o) * 48 + n]) +
+                    (s_red[(2 * 64 + o) * 48 + n] + s_red[(3 * 64 + o) * 48 + n]);
+    part[(int64_t)blockIdx.x * nout + e] = v;
+  }
+}
+}  // namespace
+
+bool wgrad_stem_shape(const WgradArgs& a) {
+  return a.ci == 3 && a.kh == 3 && a.kw == 3 && a.sh == 2 && a.sw == 2 && a.ph == 1 && a.pw == 1 && a.co <= 64 &&
+         a.co % 8 == 0 && a.ho % 4 == 0 && a.wo % 64 == 0 && a.dy_pix % 8 == 0 &&
+         (reinterpret_cast<uintptr_t>(a.dy) & 15) == 0;
+}
+
+int wgrad_stem_blocks(const WgradArgs& a) {
+  const int64_t npatch = (int64_t)a.n * (a.ho / 4) * (a.wo / 64);
+  return (int)(npatch < 512 ? npatch : 512);  // two blocks per CU
+}
+
+hipError_t wgrad_stem_launch(const WgradArgs& a, float* part, hipStream_t s) {
+  const int64_t npatch = (int64_t)a.n * (a.ho / 4) * (a.wo / 64);
+  if (!wgrad_stem_shape(a) || npatch <= 0 || npatch >= 0x7fffffff) return hipErrorInvalidValue;
+  const int nb = wgrad_stem_blocks(a);
+  trace_begin(KC_WGRAD, s);
+  hipLaunchKernelGGL(wgrad_stem_kernel, dim3((unsigned)nb), dim3(256), 0, s, a, (int)npatch, part);
+  trace_end(KC_WGRAD, s);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(part, nb, (int64_t)a.co * 27, a.out, a.accumulate, s);
+}
+
 }  // namespace numbat

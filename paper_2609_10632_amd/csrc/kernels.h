@@ -154,6 +154,13 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split);
 hipError_t wgrad_launch(const WgradArgs& a, hipStream_t s);
 hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, float* dw, int accumulate,
                                 hipStream_t s);
+// weight gradient of the RGB image layer's shape (3 channels, 3x3, stride 2, padding 1,
+// c_out <= 64 and a multiple of 8, output rows a multiple of 4 and columns of 64):
+// per-block partials [blocks][c_out][27] in part, then their split reduction into a.out
+// (accumulate honoured); x is read with any pixel stride
+bool wgrad_stem_shape(const WgradArgs& a);
+int wgrad_stem_blocks(const WgradArgs& a);
+hipError_t wgrad_stem_launch(const WgradArgs& a, float* part, hipStream_t s);
 
 // BN + SiLU
 struct BnArgs {
