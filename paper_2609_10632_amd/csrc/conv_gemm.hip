@@ -537,7 +537,7 @@ typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 // already do).
 template <int BN>
 __device__ __forceinline__ int bt_swizzle(int r) {
-  return BN == 64 ? 4 * ((r >> 1) & 1) : BN == 128 ? 4 * (r & 3) : 0;
+  return (BN == 64 || BN == 192) ? 4 * ((r >> 1) & 1) : BN == 128 ? 4 * (r & 3) : 0;
 }
 
 template <int TM, int TN, int S, int BK, int NW, bool BT>
@@ -1112,17 +1112,17 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
     launch_dma<c.tm, c.tn, 2, 64, 4>(a, mmax, s);
   else if (variant == kVariantDma32)
     launch_dma<c.tm, c.tn, 3, 32, 4>(a, mmax, s);
-  else if (variant == kVariantDma3W8)
-    launch_dma<1, c.tn, 3, 64, 8>(a, mmax, s);
+  else if (variant == kVariantDma3W8 && c.tn <= 4)
+    launch_dma<1, c.tn <= 4 ? c.tn : 4, 3, 64, 8>(a, mmax, s);
 #ifdef NUMBAT_TUNING
   else if (variant == 6)
     launch_dma<c.tm, c.tn, 4, 32, 4>(a, mmax, s);
-  else if (variant == 8)
-    launch_dma<1, c.tn, 2, 64, 8>(a, mmax, s);
-  else if (variant == 9)
-    launch_dma<1, c.tn, 4, 32, 8>(a, mmax, s);
-  else if (variant == 10)
-    launch_dma<1, c.tn, 3, 32, 8>(a, mmax, s);
+  else if (variant == 8 && c.tn <= 4)
+    launch_dma<1, c.tn <= 4 ? c.tn : 4, 2, 64, 8>(a, mmax, s);
+  else if (variant == 9 && c.tn <= 4)
+    launch_dma<1, c.tn <= 4 ? c.tn : 4, 4, 32, 8>(a, mmax, s);
+  else if (variant == 10 && c.tn <= 4)
+    launch_dma<1, c.tn <= 4 ? c.tn : 4, 3, 32, 8>(a, mmax, s);
 #endif
   else {
     dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN),
@@ -1191,9 +1191,12 @@ bool prepare_fast(ConvGemmArgs& a, int bm) {
 //  * forward (K-major weights): N tile the least padding among 128, 96 and 64 columns
 //    (ties to the wider; 64 when fewer than 400 blocks of 128 rows); more than 32768
 //    rows, three stages of 32 reduction elements (three blocks per CU for 128-row tiles),
-//    256-row tiles when the reduction is 768 or longer; 8193..32768 rows, two stages of
-//    64 (two blocks per CU) on 128 x 96 tiles when 96 divides N <= 192, else 128 x 64; up
-//    to 8192 rows, three stages of 64 on 128-row tiles;
+//    256-row tiles when the reduction is 768 or longer, 64 columns when it is shorter
+//    than 512 and 64 divides N; 8193..32768 rows, two stages of 64 (two blocks per CU) on
+//    128 x 96 tiles when 96 divides N <= 192, else 128 x 64; up to 8192 rows, reductions
+//    of 3000 or more into N >= 256: three stages of 64 on 128 x 96 (else x 128) tiles
+//    when one block per CU covers the grid; otherwise 128 x 64 tiles, two stages of 64
+//    when the grid exceeds 256 blocks, else three;
 //  * data gradient (weights read in place through transposing LDS reads, which favour
 //    64-column tiles): more than 32768 rows as the forward, with 64 columns on 128-row
 //    tiles; 8193..32768 rows, eight waves on 256 x 96 (or x 64) tiles with three stages
@@ -1217,17 +1220,25 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot, int nphase, boo
   const bool fast = cs % 16 == 0 && cs >= 32;
   int bm, variant;
   if (fast && !bt) {
-    const int64_t blocks128 = ((m_max + 127) / 128) * ((nout + bn - 1) / bn);
+    const int64_t mt = (m_max + 127) / 128;
+    const int64_t blocks128 = mt * ((nout + bn - 1) / bn);
     if (blocks128 < 400 && bn > 64) bn = 64;
     bm = 128;
     if (m_max > 32768) {
       variant = kVariantDma32;
       bm = ktot >= 768 ? 256 : 128;
+      if (ktot < 512 && nout % 64 == 0) bn = 64;
     } else if (m_max > 8192) {
       variant = kVariantDma2;
       bn = (nout % 96 == 0 && nout <= 192) ? 96 : 64;
-    } else {
+    } else if (ktot >= 3000 && nout >= 256) {
+      // long reductions: one 128 x 96 (or x 128) block per CU with three 64-deep stages,
+      // when the grid fits one round
       variant = kVariantDma3;
+      bn = (nout % 96 == 0 && mt * (nout / 96) <= 256) ? 96 : mt * ((nout + 127) / 128) <= 256 ? 128 : 64;
+    } else {
+      bn = 64;
+      variant = mt * ((nout + 63) / 64) > 256 ? kVariantDma2 : kVariantDma3;
     }
   } else if (fast) {
     const int bn64 = bn < 64 ? bn : 64;
