@@ -121,12 +121,12 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
   const RowLayout L = row_layout(a.c);
   if (t >= L.active) return;
   const int rr = t / L.cv, cb = (t - rr * L.cv) * 8;
-  float mu[8], sc[8], be[8];
+  // z = (y - mu) * gamma * rstd + beta, as one multiply-add per element
+  float sc[8], bz[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    mu[e] = mean_var[cb + e];
     sc[e] = gamma[cb + e] * (1.0f / sqrtf(mean_var[a.c + cb + e] + a.eps));
-    be[e] = beta[cb + e];
+    bz[e] = beta[cb + e] - mean_var[cb + e] * sc[e];
   }
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
       unpack8(yv[j], f);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float z = (f[e] - mu[e]) * sc[e] + be[e];
+        const float z = __builtin_fmaf(f[e], sc[e], bz[e]);
         o[e] = z * sigmoidf_fast(z);
       }
       if (res != nullptr) {
@@ -179,11 +179,12 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
 #pragma unroll
   for (int e = 0; e < 8; ++e) sdz[e] = sdx[e] = 0.f;
   if (t < L.active) {
-    float mu[8], rs[8], ga[8], be[8];
+    // xhat = (y - mu) * rstd as one multiply-add per element
+    float nm[8], rs[8], ga[8], be[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      mu[e] = save_mean[cb + e];
       rs[e] = save_rstd[cb + e];
+      nm[e] = -save_mean[cb + e] * rs[e];
       ga[e] = gamma[cb + e];
       be[e] = beta[cb + e];
     }
@@ -207,8 +208,8 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
         unpack8(yv[j], yy);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float xh = (yy[e] - mu[e]) * rs[e];
-          const float z = ga[e] * xh + be[e];
+          const float xh = __builtin_fmaf(yy[e], rs[e], nm[e]);
+          const float z = __builtin_fmaf(ga[e], xh, be[e]);
           const float sg = sigmoidf_fast(z);
           const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
           sdz[e] += dz;
@@ -279,16 +280,18 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, const 
   const int t = threadIdx.x;
   if (t >= L.active) return;
   const int rr = t / L.cv, cb = (t - rr * L.cv) * 8;
-  float mu[8], rs[8], ga[8], be[8], k1[8], k2[8], k3[8];
+  // xhat = (y - mu) * rstd and dy = k1 (dz - k2 - xhat k3) as multiply-adds:
+  // dy = k1 dz + (xhat (-k1 k3) - k1 k2)
+  float nm[8], rs[8], ga[8], be[8], k1[8], n12[8], n13[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    mu[e] = save_mean[cb + e];
     rs[e] = save_rstd[cb + e];
+    nm[e] = -save_mean[cb + e] * rs[e];
     ga[e] = gamma[cb + e];
     be[e] = beta[cb + e];
     k1[e] = coef[cb + e];
-    k2[e] = coef[c + cb + e];
-    k3[e] = coef[2 * c + cb + e];
+    n12[e] = -k1[e] * coef[c + cb + e];
+    n13[e] = -k1[e] * coef[2 * c + cb + e];
   }
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
@@ -313,11 +316,11 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, const 
       unpack8(yv[j], yy);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float xh = (yy[e] - mu[e]) * rs[e];
-        const float z = ga[e] * xh + be[e];
+        const float xh = __builtin_fmaf(yy[e], rs[e], nm[e]);
+        const float z = __builtin_fmaf(ga[e], xh, be[e]);
         const float sg = sigmoidf_fast(z);
         const float dz = gy[e] * sg * (1.0f + z * (1.0f - sg));
-        o[e] = k1[e] * (dz - k2[e] - xh * k3[e]);
+        o[e] = __builtin_fmaf(k1[e], dz, __builtin_fmaf(xh, n13[e], n12[e]));
       }
       *reinterpret_cast<uint4*>(dy + rj * a.dy_pix + cb) = pack8(o);
       if (res_grad != nullptr) {
