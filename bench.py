@@ -168,8 +168,9 @@ def committed_traffic(kernel_class, config_index, batch):
 
 
 def cpu_baseline(wl, threads_hint):
-    """The fp64 oracle on a bounded sample of the same workload: every layer at batch 1,
-    forward + BN/SiLU forward and backward + data and weight gradients."""
+    """The fp64 oracle on a bounded sample of the same workload: every layer at batch 2
+    (about 10 s on 16 host threads), forward + BN/SiLU forward and backward + data and
+    weight gradients."""
     import numpy as np
 
     import oracle
@@ -179,21 +180,22 @@ def cpu_baseline(wl, threads_hint):
     oracle.build(force=False)
     flops = 0.0
     t_total = 0.0
+    nb = 2
     for idx, l in enumerate(wl.layers):
         sid = lambda t: synth.stream_id(90 + wl.index, idx, t)
         b = synth.kaiming_uniform_bound(l.ci * l.k * l.k)
-        x = synth.bf16_to_f64(synth.bf16((1, l.h, l.h, l.ci), sid(synth.T_X)))
+        x = synth.bf16_to_f64(synth.bf16((nb, l.h, l.h, l.ci), sid(synth.T_X)))
         w = synth.bf16_to_f64(synth.bf16((l.co, l.k, l.k, l.ci), sid(synth.T_W), synth.UNIFORM, -b, b))
-        g = synth.bf16_to_f64(synth.bf16((1, l.ho, l.ho, l.co), sid(synth.T_G)))
-        s = ConvShape(1, l.h, l.h, l.ci, l.co, l.k, l.k, l.s, l.s, l.p, l.p)
+        g = synth.bf16_to_f64(synth.bf16((nb, l.ho, l.ho, l.co), sid(synth.T_G)))
+        s = ConvShape(nb, l.h, l.h, l.ci, l.co, l.k, l.k, l.s, l.s, l.p, l.p)
         ones, zeros = np.ones(l.co), np.zeros(l.co)
         t0 = time.perf_counter()
         f = oracle.block_fwd(x, w, s, ones, zeros, wl.eps)
         oracle.block_bwd(g, x, w, s, f, ones, zeros, wl.eps)
         t_total += time.perf_counter() - t0
-        flops += 3 * l.gemm_flops(1)
+        flops += 3 * l.gemm_flops(nb)
     return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": threads_hint, "kind": "oracle",
-            "sample": f"all {len(wl.layers)} layers at batch 1 (1/{wl.n} of the step): conv fwd + BN/SiLU fwd/bwd + "
+            "sample": f"all {len(wl.layers)} layers at batch {nb} ({nb}/{wl.n} of the step): conv fwd + BN/SiLU fwd/bwd + "
                       f"dgrad + wgrad in fp64; {flops / 1e9:.1f} GFLOP in {t_total:.1f} s"}
 
 
