@@ -235,13 +235,15 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
 }
 
 // --- backward finalize: fixed-order fp64 sums over blocks -> dbeta, dgamma and apply coefficients.
-// 8 channels per block, 32 groups of partial rows per channel (several loads in flight per lane).
+// 8 channels per block, 32 groups of partial rows per channel (several loads in flight per
+// lane); the group sums are combined by shuffles within each wave (8 groups) and then the
+// four wave sums, in a fixed order.
 constexpr int kFinCh = 8, kFinGroups = 32;
 __global__ __launch_bounds__(kFinCh * kFinGroups) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c,
                                                                               int64_t m, const float* save_rstd,
                                                                               const float* gamma, float* dgamma,
                                                                               float* dbeta, float* coef) {
-  __shared__ double sa[kFinGroups][kFinCh], sb[kFinGroups][kFinCh];
+  __shared__ double sa[kFinGroups / 8][kFinCh], sb[kFinGroups / 8][kFinCh];
   const int cl = threadIdx.x % kFinCh, gidx = threadIdx.x / kFinCh;
   const int ch = blockIdx.x * kFinCh + cl;
   double p = 0, q = 0;
@@ -253,14 +255,21 @@ __global__ __launch_bounds__(kFinCh * kFinGroups) void bn_bwd_finalize_kernel(co
       q += v.y;
     }
   }
-  sa[gidx][cl] = p;
-  sb[gidx][cl] = q;
+  // lanes 8 apart hold the same channel of neighbouring groups
+#pragma unroll
+  for (int d = 8; d < 64; d *= 2) {
+    p += __shfl_xor(p, d);
+    q += __shfl_xor(q, d);
+  }
+  const int wave = threadIdx.x / 64;
+  if ((threadIdx.x & 63) < kFinCh) {
+    sa[wave][cl] = p;
+    sb[wave][cl] = q;
+  }
   __syncthreads();
   if (gidx == 0 && ch < c) {
-    for (int k = 1; k < kFinGroups; ++k) {
-      p += sa[k][cl];
-      q += sb[k][cl];
-    }
+    p = (sa[0][cl] + sa[1][cl]) + (sa[2][cl] + sa[3][cl]);
+    q = (sb[0][cl] + sb[1][cl]) + (sb[2][cl] + sb[3][cl]);
     dbeta[ch] = (float)p;
     dgamma[ch] = (float)q;
     coef[ch] = gamma[ch] * save_rstd[ch];

@@ -18,14 +18,16 @@ namespace {
 
 // 8 channels per block, 128 groups of tiles per channel: consecutive lanes read the
 // partials of consecutive channels (64-byte segments) and each lane keeps several loads
-// in flight; the group sums are combined by a fixed pairwise tree.  (With 32 groups the
+// in flight; the group sums are combined in a fixed order (shuffles within a wave, then
+// a pairwise tree over the waves).  (With 32 groups the
 // 6400 tiles of the image-input layer took 25 dependent rounds of loads.)
 constexpr int kMergeCh = 8, kMergeGroups = 128;
 
 __global__ __launch_bounds__(kMergeCh * kMergeGroups) void stats_merge_kernel(const float2* part, int mtiles,
                                                                               int tile_rows, int64_t m, int c,
                                                                               float* mean_var) {
-  __shared__ double s1s[kMergeGroups][kMergeCh], s2s[kMergeGroups][kMergeCh], m2s[kMergeGroups][kMergeCh];
+  __shared__ double s1s[kMergeCh * kMergeGroups / 64][kMergeCh], s2s[kMergeCh * kMergeGroups / 64][kMergeCh],
+      m2s[kMergeCh * kMergeGroups / 64][kMergeCh];
   const int cl = threadIdx.x % kMergeCh;
   const int g = threadIdx.x / kMergeCh;
   const int ch = blockIdx.x * kMergeCh + cl;
@@ -54,23 +56,41 @@ __global__ __launch_bounds__(kMergeCh * kMergeGroups) void stats_merge_kernel(co
       m2 += (double)p.y;
     }
   }
-  s1s[g][cl] = s1;
-  s2s[g][cl] = s2;
-  m2s[g][cl] = m2;
-  __syncthreads();
+  // lanes 8 apart hold the same channel of neighbouring groups: shuffles combine the 8
+  // groups of a wave, then one thread per channel adds the 16 wave sums pairwise
 #pragma unroll
-  for (int h = kMergeGroups / 2; h > 0; h >>= 1) {
-    if (g < h) {
-      s1s[g][cl] += s1s[g + h][cl];
-      s2s[g][cl] += s2s[g + h][cl];
-      m2s[g][cl] += m2s[g + h][cl];
-    }
-    __syncthreads();
+  for (int d = 8; d < 64; d *= 2) {
+    s1 += __shfl_xor(s1, d);
+    s2 += __shfl_xor(s2, d);
+    m2 += __shfl_xor(m2, d);
   }
+  const int wave = threadIdx.x / 64;
+  if ((threadIdx.x & 63) < kMergeCh) {
+    s1s[wave][cl] = s1;
+    s2s[wave][cl] = s2;
+    m2s[wave][cl] = m2;
+  }
+  __syncthreads();
   if (g == 0 && ch < c) {
-    s1 = s1s[0][cl];
-    s2 = s2s[0][cl];
-    m2 = m2s[0][cl];
+    constexpr int NWv = kMergeCh * kMergeGroups / 64;  // 16 waves
+    double a1[NWv], a2[NWv], a3[NWv];
+#pragma unroll
+    for (int w = 0; w < NWv; ++w) {
+      a1[w] = s1s[w][cl];
+      a2[w] = s2s[w][cl];
+      a3[w] = m2s[w][cl];
+    }
+#pragma unroll
+    for (int h = NWv / 2; h > 0; h >>= 1)
+#pragma unroll
+      for (int w = 0; w < h; ++w) {
+        a1[w] += a1[w + h];
+        a2[w] += a2[w + h];
+        a3[w] += a3[w + h];
+      }
+    s1 = a1[0];
+    s2 = a2[0];
+    m2 = a3[0];
     const double n = (double)m;
     const double dm = s1 / n;
     mean_var[ch] = (float)(K + dm);
