@@ -50,6 +50,10 @@ CONV_CASES = [
     # the image layer's forward kernel: 4 x 64 output patches
     (2, 24, 256, 3, 48, 3, 2),
     (1, 8, 128, 3, 32, 3, 2),
+    # mid-size data gradient on eight-wave 256-row tiles (transposed weights), and a long
+    # reduction into 384 channels on one 128 x 96 block per CU
+    (2, 64, 80, 128, 128, 3, 1),
+    (2, 20, 20, 384, 384, 3, 1),
 ]
 
 
