@@ -54,6 +54,10 @@ CONV_CASES = [
     # reduction into 384 channels on one 128 x 96 block per CU
     (2, 64, 80, 128, 128, 3, 1),
     (2, 20, 20, 384, 384, 3, 1),
+    # in-place weights with an input channel count that ends mid-chunk (40 = 5 x 8), both
+    # strides
+    (2, 14, 10, 40, 48, 3, 1),
+    (2, 15, 17, 40, 32, 3, 2),
 ]
 
 
