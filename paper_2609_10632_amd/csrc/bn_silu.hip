@@ -189,7 +189,8 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
       be[e] = beta[cb + e];
     }
     const int64_t st = L.rows_per_iter;
-    // eight rows in flight: with the block count bn_reduce_blocks picks, one round
+    // eight rows in flight: with the block count bn_reduce_blocks picks, one round (apart
+    // from layers large enough to meet its block cap)
     for (int64_t r = r0 + rr; r < r1; r += 8 * st) {
       uint4 gv[8], yv[8];
 #pragma unroll
@@ -235,21 +236,22 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
 }
 
 // --- backward finalize: fixed-order fp64 sums over blocks -> dbeta, dgamma and apply coefficients.
-// 8 channels per block, 32 groups of partial rows per channel (several loads in flight per
+// 8 channels per block, G groups of partial rows per channel (a few loads in flight per
 // lane); the group sums are combined by shuffles within each wave (8 groups) and then the
-// four wave sums, in a fixed order.
-constexpr int kFinCh = 8, kFinGroups = 32;
-__global__ __launch_bounds__(kFinCh * kFinGroups) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c,
-                                                                              int64_t m, const float* save_rstd,
-                                                                              const float* gamma, float* dgamma,
-                                                                              float* dbeta, float* coef) {
-  __shared__ double sa[kFinGroups / 8][kFinCh], sb[kFinGroups / 8][kFinCh];
+// G/8 wave sums by a pairwise tree, in a fixed order that depends only on G.
+constexpr int kFinCh = 8;
+template <int G>
+__global__ __launch_bounds__(kFinCh * G) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c, int64_t m,
+                                                                     const float* save_rstd, const float* gamma,
+                                                                     float* dgamma, float* dbeta, float* coef) {
+  constexpr int NWV = G / 8;  // waves
+  __shared__ double sa[NWV][kFinCh], sb[NWV][kFinCh];
   const int cl = threadIdx.x % kFinCh, gidx = threadIdx.x / kFinCh;
   const int ch = blockIdx.x * kFinCh + cl;
   double p = 0, q = 0;
   if (ch < c) {
-#pragma unroll 8
-    for (int b = gidx; b < nblocks; b += kFinGroups) {
+#pragma unroll 4
+    for (int b = gidx; b < nblocks; b += G) {
       const float2 v = part[(int64_t)b * c + ch];
       p += v.x;
       q += v.y;
@@ -268,8 +270,21 @@ __global__ __launch_bounds__(kFinCh * kFinGroups) void bn_bwd_finalize_kernel(co
   }
   __syncthreads();
   if (gidx == 0 && ch < c) {
-    p = (sa[0][cl] + sa[1][cl]) + (sa[2][cl] + sa[3][cl]);
-    q = (sb[0][cl] + sb[1][cl]) + (sb[2][cl] + sb[3][cl]);
+    double ta[NWV], tb[NWV];
+#pragma unroll
+    for (int w = 0; w < NWV; ++w) {
+      ta[w] = sa[w][cl];
+      tb[w] = sb[w][cl];
+    }
+#pragma unroll
+    for (int h = NWV / 2; h >= 1; h /= 2)
+#pragma unroll
+      for (int w = 0; w < h; ++w) {
+        ta[w] += ta[w + h];
+        tb[w] += tb[w + h];
+      }
+    p = ta[0];
+    q = tb[0];
     dbeta[ch] = (float)p;
     dgamma[ch] = (float)q;
     coef[ch] = gamma[ch] * save_rstd[ch];
@@ -353,12 +368,20 @@ size_t reduce_smem(int c) {
 }  // namespace
 
 int bn_reduce_blocks(int64_t m, int c) {
-  // about 8 vectors of 8 channels per thread
+  // 8 rows per active thread: a block covers 8 * rows_per_iter rows, so every thread
+  // issues its loads in one round (counting all kThreads threads as active gave most
+  // layers a second, nearly empty round)
   int64_t vpt = 8;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_BN_VEC")) vpt = atoi(e);
 #endif
-  int64_t b = (m * (c / 8) + kThreads * vpt - 1) / (kThreads * vpt);
+  const int cv = c / 8;
+  int64_t rpi = cv > 0 ? kThreads / cv : 1;
+  if (rpi < 1) rpi = 1;
+  int64_t b = (m + rpi * vpt - 1) / (rpi * vpt);
+#ifdef NUMBAT_TUNING
+  if (getenv("NUMBAT_BN_OLD")) b = (m * (c / 8) + kThreads * vpt - 1) / (kThreads * vpt);
+#endif
   if (b > kMaxBlocks) b = kMaxBlocks;
   if (b < 1) b = 1;
   return (int)b;
@@ -424,8 +447,21 @@ hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, cons
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   trace_begin(KC_BN_BWD_FINALIZE, s);
-  hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3((a.c + kFinCh - 1) / kFinCh), dim3(kFinCh * kFinGroups), 0, s, part, nb,
-                     a.c, a.m, save_rstd, gamma, dgamma, dbeta, coef);
+  // about eight partial rows per lane
+  const dim3 fgrid((a.c + kFinCh - 1) / kFinCh);
+  int fg = nb <= 256 ? 32 : nb <= 512 ? 64 : 128;
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_BN_FING")) fg = atoi(e);
+#endif
+  if (fg == 128)
+    hipLaunchKernelGGL(bn_bwd_finalize_kernel<128>, fgrid, dim3(kFinCh * 128), 0, s, part, nb, a.c, a.m, save_rstd,
+                       gamma, dgamma, dbeta, coef);
+  else if (fg == 64)
+    hipLaunchKernelGGL(bn_bwd_finalize_kernel<64>, fgrid, dim3(kFinCh * 64), 0, s, part, nb, a.c, a.m, save_rstd,
+                       gamma, dgamma, dbeta, coef);
+  else
+    hipLaunchKernelGGL(bn_bwd_finalize_kernel<32>, fgrid, dim3(kFinCh * 32), 0, s, part, nb, a.c, a.m, save_rstd,
+                       gamma, dgamma, dbeta, coef);
   trace_end(KC_BN_BWD_FINALIZE, s);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
