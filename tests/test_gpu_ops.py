@@ -58,6 +58,11 @@ CONV_CASES = [
     # strides
     (2, 14, 10, 40, 48, 3, 1),
     (2, 15, 17, 40, 32, 3, 2),
+    # c_out of 192 and 576 (three and nine 64-channel weight-gradient tiles): 3x3, a ragged
+    # 1800-column reduction at stride 2, and 1x1
+    (2, 10, 12, 64, 192, 3, 1),
+    (1, 9, 11, 200, 576, 3, 2),
+    (2, 9, 7, 576, 192, 1, 1),
 ]
 
 
