@@ -44,9 +44,12 @@ def parse():
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
     ap.add_argument("--streams", type=int, default=2, choices=(1, 2),
                     help="1: the whole step on one stream; 2 (default): each layer's weight gradient on a "
-                         "second stream once its data gradient is issued, overlapping the next layer's "
-                         "latency-bound BN backward (1.6%% faster than one stream)")
+                         "second stream once its data gradient is done, overlapping the next layers' "
+                         "latency-bound BN backward")
     ap.add_argument("--serial", action="store_true", help="same as --streams 1")
+    ap.add_argument("--wgrad-order", choices=("deferred", "immediate"), default="deferred",
+                    help="two streams: enqueue layer L's weight gradient after layer L-1's BN backward "
+                         "(deferred, default) or right after layer L's data gradient (immediate)")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
     return ap.parse_args()
@@ -102,10 +105,17 @@ class Layer:
                               self.srstd, ws=self.ws, ws_bytes=self.ws_len)
         if e: e[2].record()
 
-    def bwd(self, ev=None, side=None):
+    def bwd(self, ev=None, side=None, pending=None, defer=True):
         """BN/SiLU backward, then the weight and data gradients.  With a side stream the
         weight gradient (which nothing later in the backward pass reads) runs there, on its
-        own workspace, overlapping the data gradient and the following layers."""
+        own workspace, overlapping the data gradient and the following layers.
+
+        With a side stream this returns a callable that enqueues this layer's weight
+        gradient (waiting for its data gradient); `pending` is the previous layer's.  In
+        a captured graph the data gradient's first dependant is then the next main-stream
+        kernel, which keeps the main chain on one hardware queue (enqueued first, the weight
+        gradient took the data gradient's queue and moved the main chain to another, and
+        every such hop cost a cross-queue wait of several microseconds)."""
         nb = self.nb
         e = ev.get(self.name) if ev else None
         if e: e[3].record()
@@ -115,14 +125,24 @@ class Layer:
         if side is not None:
             import torch
 
+            if pending is not None:
+                pending()
             # the data gradient first; the side stream's weight gradient then overlaps the
             # next layer's BN backward instead of competing with this data gradient
             nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
-            side.wait_stream(torch.cuda.current_stream())
-            with torch.cuda.stream(side):
-                nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws_side,
-                                          ws_bytes=self.ws_len)
-            return
+            done = torch.cuda.Event()
+            done.record()
+
+            def wgrad():
+                side.wait_event(done)
+                with torch.cuda.stream(side):
+                    nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws_side,
+                                              ws_bytes=self.ws_len)
+
+            if defer:
+                return wgrad
+            wgrad()
+            return None
         nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
         if e: e[5].record()
         nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
@@ -257,6 +277,7 @@ def main():
         l.bind_ws(ws, ws_side)
     two = args.streams == 2 and not args.serial
     side = torch.cuda.Stream() if two else None  # default priority
+    defer = args.wgrad_order == "deferred"
     torch.cuda.synchronize()
     step_flops = sum(3 * l.flops for l in layers)
 
@@ -266,8 +287,11 @@ def main():
         sd = side if overlap else None
         for l in layers:
             l.fwd(ev)
+        pending = None
         for l in reversed(layers):
-            l.bwd(ev, sd)
+            pending = l.bwd(ev, sd, pending, defer)
+        if pending is not None:
+            pending()
         if sd is not None:
             torch.cuda.current_stream().wait_stream(sd)
 
