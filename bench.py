@@ -50,6 +50,11 @@ def parse():
     ap.add_argument("--wgrad-order", choices=("deferred", "immediate"), default="deferred",
                     help="two streams: enqueue layer L's weight gradient after layer L-1's BN backward "
                          "(deferred, default) or right after layer L's data gradient (immediate)")
+    ap.add_argument("--wgrad-group", type=int, default=2,
+                    help="deferred order: enqueue the weight gradients in groups of this many layers behind "
+                         "one cross-stream wait (each wait costs the main queue a completion signal)")
+    ap.add_argument("--wgrad-tail", type=int, default=8,
+                    help="the last this many layers of the backward pass are enqueued one by one")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
     return ap.parse_args()
@@ -133,12 +138,14 @@ class Layer:
             done = torch.cuda.Event()
             done.record()
 
-            def wgrad():
-                side.wait_event(done)
+            def wgrad(wait=True):
+                if wait:
+                    side.wait_event(done)
                 with torch.cuda.stream(side):
                     nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws_side,
                                               ws_bytes=self.ws_len)
 
+            wgrad.done = done
             if defer:
                 return wgrad
             wgrad()
@@ -278,6 +285,7 @@ def main():
     two = args.streams == 2 and not args.serial
     side = torch.cuda.Stream() if two else None  # default priority
     defer = args.wgrad_order == "deferred"
+    GROUP, GTAIL = args.wgrad_group, args.wgrad_tail
     torch.cuda.synchronize()
     step_flops = sum(3 * l.flops for l in layers)
 
@@ -287,11 +295,22 @@ def main():
         sd = side if overlap else None
         for l in layers:
             l.fwd(ev)
-        pending = None
-        for l in reversed(layers):
-            pending = l.bwd(ev, sd, pending, defer)
-        if pending is not None:
-            pending()
+        queued = []  # weight gradients not yet enqueued; the last one's wait covers all
+
+        def flush():
+            if queued:
+                side.wait_event(queued[-1].done)
+            for f in queued:
+                f(wait=False)
+            queued.clear()
+
+        nl = len(layers)
+        for i, l in enumerate(reversed(layers)):
+            group = 1 if i >= nl - GTAIL else GROUP
+            r = l.bwd(ev, sd, flush if len(queued) >= group else None, defer)
+            if r is not None:
+                queued.append(r)
+        flush()
         if sd is not None:
             torch.cuda.current_stream().wait_stream(sd)
 
