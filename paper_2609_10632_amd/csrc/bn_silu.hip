@@ -380,9 +380,6 @@ int bn_reduce_blocks(int64_t m, int c) {
   int64_t rpi = cv > 0 ? kThreads / cv : 1;
   if (rpi < 1) rpi = 1;
   int64_t b = (m + rpi * vpt - 1) / (rpi * vpt);
-#ifdef NUMBAT_TUNING
-  if (getenv("NUMBAT_BN_OLD")) b = (m * (c / 8) + kThreads * vpt - 1) / (kThreads * vpt);
-#endif
   if (b > kMaxBlocks) b = kMaxBlocks;
   if (b < 1) b = 1;
   return (int)b;
