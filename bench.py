@@ -115,12 +115,14 @@ class Layer:
         weight gradient (which nothing later in the backward pass reads) runs there, on its
         own workspace, overlapping the data gradient and the following layers.
 
-        With a side stream this returns a callable that enqueues this layer's weight
-        gradient (waiting for its data gradient); `pending` is the previous layer's.  In
-        a captured graph the data gradient's first dependant is then the next main-stream
-        kernel, which keeps the main chain on one hardware queue (enqueued first, the weight
-        gradient took the data gradient's queue and moved the main chain to another, and
-        every such hop cost a cross-queue wait of several microseconds)."""
+        With a side stream and `defer`, this returns a callable that enqueues this layer's
+        weight gradient (by default after a wait for this layer's data gradient; `.done` is
+        that event), and `pending`, if given, runs between this layer's BN backward and its
+        data gradient to enqueue earlier layers' weight gradients.  In a captured graph a
+        data gradient's first dependant is then the next main-stream kernel, which keeps
+        the main chain on one hardware queue (enqueued first, the weight gradient kept the
+        data gradient's queue and the main chain moved to another at every layer, each hop
+        costing a cross-queue wait of several microseconds)."""
         nb = self.nb
         e = ev.get(self.name) if ev else None
         if e: e[3].record()
