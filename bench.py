@@ -287,7 +287,7 @@ def main():
     two = args.streams == 2 and not args.serial
     side = torch.cuda.Stream() if two else None  # default priority
     defer = args.wgrad_order == "deferred"
-    GROUP, GTAIL = args.wgrad_group, args.wgrad_tail
+    wg_group, wg_tail = args.wgrad_group, args.wgrad_tail
     torch.cuda.synchronize()
     step_flops = sum(3 * l.flops for l in layers)
 
@@ -308,7 +308,7 @@ def main():
 
         nl = len(layers)
         for i, l in enumerate(reversed(layers)):
-            group = 1 if i >= nl - GTAIL else GROUP
+            group = 1 if i >= nl - wg_tail else wg_group
             r = l.bwd(ev, sd, flush if len(queued) >= group else None, defer)
             if r is not None:
                 queued.append(r)
