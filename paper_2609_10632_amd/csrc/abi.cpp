@@ -34,7 +34,10 @@ hipEvent_t g_open[KC_COUNT];
 hipEvent_t pool_event() {
   if (g_pool_used == g_pool.size()) {
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreate(&e) != hipSuccess) {
+      (void)hipGetLastError();  // timing is best-effort; the launch status stays the kernel's
+      return nullptr;
+    }
     g_pool.push_back(e);
   }
   return g_pool[g_pool_used++];
@@ -53,8 +56,13 @@ void trace_begin(int cls, hipStream_t s) {
   if (!g_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
   hipEvent_t e = pool_event();
+  // a failed record drops this launch from the timing and clears its error, so that the
+  // launcher's own status check reports the kernel launch only
+  if (e && hipEventRecord(e, s) != hipSuccess) {
+    (void)hipGetLastError();
+    e = nullptr;
+  }
   g_open[cls] = e;
-  if (e) hipEventRecord(e, s);
 }
 
 void trace_end(int cls, hipStream_t s) {
@@ -62,8 +70,10 @@ void trace_end(int cls, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_tmu);
   hipEvent_t e = pool_event();
   if (e && g_open[cls]) {
-    hipEventRecord(e, s);
-    g_recs.push_back(TimingRec{cls, g_open[cls], e});
+    if (hipEventRecord(e, s) == hipSuccess)
+      g_recs.push_back(TimingRec{cls, g_open[cls], e});
+    else
+      (void)hipGetLastError();
   }
   g_open[cls] = nullptr;
 }
