@@ -15,7 +15,7 @@ graph (replays are checked bitwise against the eager step) and replayed K times.
 roofline = the dominant conv kernel's algorithmic FLOPs / its summed launch durations,
 from HIP events the library records around every kernel on its launch stream during K
 further (eager) steps.  cpu_baseline = the fp64 oracle on a bounded sample (all layers
-at batch 1), on this host's cores.
+at batch 2), on this host's cores.
 """
 from __future__ import annotations
 
@@ -58,104 +58,6 @@ def parse():
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
     return ap.parse_args()
-
-
-class Layer:
-    """Device buffers and problem descriptors of one layer."""
-
-    def __init__(self, idx, spec, n, cfg_index, eps):
-        import torch
-
-        from paper_2609_10632_amd import blocks, synth
-        from paper_2609_10632_amd import numbat as nb
-
-        self.spec = spec
-        self.name = spec.name
-        sid = lambda t: synth.stream_id(cfg_index, idx, t)
-        b = synth.kaiming_uniform_bound(spec.ci * spec.k * spec.k)
-        self.blk = blocks.ConvBlock(n, spec.h, spec.h, spec.ci, spec.co, spec.k, spec.s, eps=eps)
-        ho = self.blk.ho
-        self.x = blocks.dev_bf16(synth.bf16((n, spec.h, spec.h, spec.ci), sid(synth.T_X)))
-        self.w = blocks.dev_bf16(synth.bf16((spec.co, spec.k, spec.k, spec.ci), sid(synth.T_W), synth.UNIFORM, -b, b))
-        self.g = blocks.dev_bf16(synth.bf16((n, ho, ho, spec.co), sid(synth.T_G)))
-        dev = self.x.device
-        bf = torch.bfloat16
-        self.gamma = torch.ones(spec.co, device=dev)
-        self.beta = torch.zeros(spec.co, device=dev)
-        self.y = torch.empty((n, ho, ho, spec.co), dtype=bf, device=dev)
-        self.a = torch.empty_like(self.y)
-        self.dy = torch.empty_like(self.y)
-        self.dx = torch.empty((n, spec.h, spec.h, spec.ci), dtype=bf, device=dev)
-        self.dw = torch.empty((spec.co, spec.k, spec.k, spec.ci), dtype=torch.float32, device=dev)
-        f32 = lambda k: torch.empty(k, dtype=torch.float32, device=dev)
-        self.stats, self.smean, self.srstd, self.dgamma, self.dbeta = (f32(2 * spec.co), f32(spec.co),
-                                                                       f32(spec.co), f32(spec.co), f32(spec.co))
-        self.bnp = self.blk.bn()
-        self.ws_need = self.blk.ws_bytes()
-        self.nb = nb
-        self.flops = spec.gemm_flops(n)  # one pass
-        self.bn_elems = self.blk.m * spec.co
-
-    def bind_ws(self, ws, ws_side):
-        self.ws, self.ws_side = ws, ws_side
-        self.ws_len = ws.numel()
-
-    def fwd(self, ev=None):
-        nb = self.nb
-        e = ev.get(self.name) if ev else None
-        if e: e[0].record()
-        nb.numbat_conv_fwd(self.blk.prob, self.x, self.w, self.y, self.stats, self.ws, ws_bytes=self.ws_len)
-        if e: e[1].record()
-        nb.numbat_bn_silu_fwd(self.bnp, self.y, self.stats, self.gamma, self.beta, None, self.a, self.smean,
-                              self.srstd, ws=self.ws, ws_bytes=self.ws_len)
-        if e: e[2].record()
-
-    def bwd(self, ev=None, side=None, pending=None, defer=True):
-        """BN/SiLU backward, then the weight and data gradients.  With a side stream the
-        weight gradient (which nothing later in the backward pass reads) runs there, on its
-        own workspace, overlapping the data gradient and the following layers.
-
-        With a side stream and `defer`, this returns a callable that enqueues this layer's
-        weight gradient (by default after a wait for this layer's data gradient; `.done` is
-        that event), and `pending`, if given, runs between this layer's BN backward and its
-        data gradient to enqueue earlier layers' weight gradients.  In a captured graph a
-        data gradient's first dependant is then the next main-stream kernel, which keeps
-        the main chain on one hardware queue (enqueued first, the weight gradient kept the
-        data gradient's queue and the main chain moved to another at every layer, each hop
-        costing a cross-queue wait of several microseconds)."""
-        nb = self.nb
-        e = ev.get(self.name) if ev else None
-        if e: e[3].record()
-        nb.numbat_bn_silu_bwd(self.bnp, self.g, self.y, self.smean, self.srstd, self.gamma, self.beta, self.dy,
-                              self.dgamma, self.dbeta, None, ws=self.ws, ws_bytes=self.ws_len)
-        if e: e[4].record()
-        if side is not None:
-            import torch
-
-            if pending is not None:
-                pending()
-            # the data gradient first; the side stream's weight gradient then overlaps the
-            # next layer's BN backward instead of competing with this data gradient
-            nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
-            done = torch.cuda.Event()
-            done.record()
-
-            def wgrad(wait=True):
-                if wait:
-                    side.wait_event(done)
-                with torch.cuda.stream(side):
-                    nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws_side,
-                                              ws_bytes=self.ws_len)
-
-            wgrad.done = done
-            if defer:
-                return wgrad
-            wgrad()
-            return None
-        nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
-        if e: e[5].record()
-        nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
-        if e: e[6].record()
 
 
 PASSES = ("conv_fwd", "bn_silu_fwd", "bn_silu_bwd", "conv_bwd_weight", "conv_bwd_data")
@@ -269,6 +171,7 @@ def main():
     import torch
 
     from paper_2609_10632_amd import numbat as nb
+    from paper_2609_10632_amd.schedule import ConvSet
     from paper_2609_10632_amd.workloads import workload
 
     nb.load()
@@ -279,42 +182,16 @@ def main():
         want = set(args.layers.split(","))
         specs = [l for l in specs if l.name in want]
     print(f"# setting up {len(specs)} layers of configuration {wl.index} at batch {wl.n}", file=sys.stderr, flush=True)
-    layers = [Layer(i, l, wl.n, wl.index, wl.eps) for i, l in enumerate(specs)]
-    ws = torch.empty(max(l.ws_need for l in layers), dtype=torch.uint8, device="cuda")
-    ws_side = torch.empty_like(ws)
-    for l in layers:
-        l.bind_ws(ws, ws_side)
+    cs = ConvSet(specs, wl.n, wl.index, wl.eps, wl.g_std,
+                 [wl.layers.index(l) for l in specs])
+    layers = cs.layers
     two = args.streams == 2 and not args.serial
-    side = torch.cuda.Stream() if two else None  # default priority
     defer = args.wgrad_order == "deferred"
-    wg_group, wg_tail = args.wgrad_group, args.wgrad_tail
     torch.cuda.synchronize()
     step_flops = sum(3 * l.flops for l in layers)
 
     def step(ev=None, overlap=True):
-        """One training step of the conv set: every layer's forward, then the backward in
-        reverse order.  overlap=False keeps everything on one stream (per-kernel timing)."""
-        sd = side if overlap else None
-        for l in layers:
-            l.fwd(ev)
-        queued = []  # weight gradients not yet enqueued; the last one's wait covers all
-
-        def flush():
-            if queued:
-                side.wait_event(queued[-1].done)
-            for f in queued:
-                f(wait=False)
-            queued.clear()
-
-        nl = len(layers)
-        for i, l in enumerate(reversed(layers)):
-            group = 1 if i >= nl - wg_tail else wg_group
-            r = l.bwd(ev, sd, flush if len(queued) >= group else None, defer)
-            if r is not None:
-                queued.append(r)
-        flush()
-        if sd is not None:
-            torch.cuda.current_stream().wait_stream(sd)
+        cs.step(ev, overlap=overlap and two, defer=defer, group=args.wgrad_group, tail=args.wgrad_tail)
 
     print(f"# warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):

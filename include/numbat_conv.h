@@ -133,7 +133,10 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream);
 
-/* Data gradient of the forward convolution (its adjoint in x):
+/* Data gradient of the forward convolution (its adjoint in x): the backward of the
+ * detector's conv block (Sec. 6.1), whose training step runs a backward stage over every
+ * layer (Sec. 8.2 stage timings); the operator-level check of Sec. 6.3 compares this
+ * operator's CPU and GPU backward.  The sum is the transpose of the forward's:
  *   dx[n,h,w,c] = sum over (p,q,r,s,o) with p*stride_h - pad_h + r = h and
  *                 q*stride_w - pad_w + s = w of  w[o,r,s,c] * dy[n,p,q,o].
  * dy: bf16 NHWC [n,ho,wo,c_out] (y_pixel_stride); dx: bf16 NHWC [n,h,w,c_in] (x_pixel_stride).
@@ -171,7 +174,10 @@ numbat_status numbat_bn_silu_fwd(const numbat_bn_problem* p, const void* y, cons
                                  float* save_mean, float* save_rstd, float* running_mean, float* running_var,
                                  void* ws, size_t ws_bytes, void* stream);
 
-/* Backward of numbat_bn_silu_fwd with batch statistics, given g = dL/d(out):
+/* Backward of numbat_bn_silu_fwd with batch statistics, given g = dL/d(out): BN is trained
+ * in fp32 under mixed precision (Sec. 3.2, Table 1 precision row) with batch statistics in
+ * the training step, so its gradient flows through the statistics; SiLU is the detector's
+ * activation (Sec. 6.1).  The chain rule through those definitions gives:
  *   z = gamma * xhat + beta,  xhat = (y - save_mean) * save_rstd
  *   dz = g * sigmoid(z) * (1 + z * (1 - sigmoid(z)))
  *   dbeta = sum_rows dz,  dgamma = sum_rows dz * xhat                      (fp32 [c])

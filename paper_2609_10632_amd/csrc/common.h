@@ -74,7 +74,7 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const uint4& a, const uint4& b, f3
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, c, 0, 0, 0);
 }
 
-// sigmoid with the hardware exp2 and reciprocal (about 1 ulp each)
+// the same MFMA on native 16-byte vectors
 __device__ __forceinline__ f32x4 mfma16x16x32(const u32x4& a, const u32x4& b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
                                                  0, 0);
@@ -91,6 +91,7 @@ __device__ __forceinline__ f32x16 mfma32x32x16(const u32x4& a, const u32x4& b, f
                                                  0, 0);
 }
 
+// sigmoid with the hardware exp2 and reciprocal (about 1 ulp each)
 __device__ __forceinline__ float sigmoidf_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 // Workgroups are dealt round-robin to the 8 XCDs (linear id L runs on XCD L % 8), and

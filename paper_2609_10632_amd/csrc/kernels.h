@@ -31,8 +31,10 @@ enum KernelClass {
 void trace_begin(int cls, hipStream_t s);
 void trace_end(int cls, hipStream_t s);
 
-// conv GEMM kernel variants: generic (source channels a multiple of 8), and the two fast
-// paths for 16-multiple channel counts of at least 32 (LDS-staged, register-direct)
+// conv GEMM kernel variants: generic (source channels a multiple of 8; A fragments loaded
+// into registers), and the direct-to-LDS kernel for 16-multiple channel counts of at least
+// 32 in its stage configurations (three or two stages, 32- or 64-element steps, four or
+// eight waves)
 enum { kVariantGeneric = 0, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5, kVariantDma3W8 = 7 };
 struct TileCfg {
   int bm, bn;

@@ -19,3 +19,12 @@ def golden():
 
     with open(os.path.join(ROOT, "tests", "golden", "paper_values.json")) as f:
         return json.load(f)
+
+
+def pytest_terminal_summary(terminalreporter):
+    from parity import REPORT
+
+    if REPORT:
+        terminalreporter.section("parity coverage (complete / sampled per layer)")
+        for line in REPORT:
+            terminalreporter.write_line(line)

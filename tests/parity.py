@@ -11,6 +11,15 @@ from paper_2609_10632_amd import synth
 REL_TOL = 2e-2
 STAT_TOL = 1e-5
 
+# one line per compared layer or chain (what was compared completely, what was sampled);
+# printed in the session's terminal summary
+REPORT = []
+
+
+def report(line: str) -> None:
+    REPORT.append(line)
+    print(line, flush=True)
+
 
 def rel_inf(gpu, ref) -> float:
     gpu = np.asarray(gpu, np.float64)

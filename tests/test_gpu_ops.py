@@ -31,8 +31,9 @@ CONV_CASES = [
     (2, 15, 15, 3, 16, 3, 2),
     (1, 6, 6, 16, 16, 1, 2),
     (2, 12, 12, 1152, 64, 1, 1),
-    # more than 32768 GEMM rows with short reductions: the register-direct fast path
-    # (48 channels: two tap wraps per step; 32 -> 64 stride 2: 32-column data-gradient tiles)
+    # more than 32768 GEMM rows with short reductions: the direct-to-LDS kernel's
+    # three-stage 32-element variant (48 channels: two tap wraps per step; 32 -> 64 stride 2:
+    # 32-column data-gradient tiles)
     (2, 130, 129, 48, 48, 3, 1),
     (1, 364, 362, 32, 64, 3, 2),
     # narrow inputs (fewer than 8 channels: the image-input kernels) across channel
@@ -169,7 +170,47 @@ def test_conv_strided_views():
     assert_close(blocks.host_f64(dw), oracle.conv_wgrad(f64(big[..., 48:96]), f64(dyb[..., 40:88]), s), "dw views")
 
 
-BN_CASES = [(1000, 8), (4097, 48), (2048, 96), (777, 576), (300, 64)]
+def test_conv_strided_views_large():
+    """Channel slices at more than 32768 rows (batch 8 at 80x80: the large-tile kernel
+    variants): the forward with statistics into a 96-channel slice of a 384-wide buffer from
+    a slice of a 192-wide one, the data gradient accumulated into a slice, the weight
+    gradient from slices -- as in a C2f block at the detector's batch."""
+    n, h, c = 8, 80, 96
+    s = ConvShape(n, h, h, c, c, 3, 3, 1, 1, 1, 1)
+    inp = Inputs(108)
+    xbig = inp.normal((n, h, h, 192), synth.T_X)
+    wb = inp.weight(c, 3, c)
+    dybig = inp.normal((n, h, h, 384), synth.T_DY)
+    dx0 = inp.normal((n, h, h, 192), synth.T_RES)
+    blk = blocks.ConvBlock(n, h, h, c, c, 3, 1, x_pixel_stride=192, y_pixel_stride=384)
+    x, w = blocks.dev_bf16(xbig), blocks.dev_bf16(wb)
+    ybig = torch.zeros((n, h, h, 384), dtype=torch.bfloat16, device="cuda")
+    stats = torch.empty(2 * c, dtype=torch.float32, device="cuda")
+    ws = blocks.workspace(blk.ws_bytes())
+    nb.numbat_conv_fwd(blk.prob, x[..., 96:], w, ybig[..., 192:288], stats, ws)
+    dy = blocks.dev_bf16(dybig)
+    dxbig = blocks.dev_bf16(dx0)
+    nb.numbat_conv_bwd_data(blk.prob, dy[..., 288:], w, dxbig[..., 96:], True, ws)
+    dw = torch.empty((c, 3, 3, c), dtype=torch.float32, device="cuda")
+    nb.numbat_conv_bwd_weight(blk.prob, x[..., 96:], dy[..., 288:], dw, False, ws)
+    torch.cuda.synchronize()
+    xs = f64(xbig[..., 96:])
+    yref = oracle.conv_fwd(xs, f64(wb), s)
+    got = blocks.host_f64(ybig)
+    assert_close(got[..., 192:288], yref, "y view")
+    assert np.all(got[..., :192] == 0) and np.all(got[..., 288:] == 0)
+    mref, vref = oracle.bn_stats(yref)
+    st = blocks.host_f64(stats)
+    assert_stats(st[:c], st[c:], mref, vref, EPS, "batch stats of a view")
+    gx = blocks.host_f64(dxbig)
+    dxref = oracle.conv_dgrad(f64(dybig[..., 288:]), f64(wb), s) + f64(dx0[..., 96:])
+    assert_close(gx[..., 96:], dxref, "dx accumulated into a view")
+    assert np.array_equal(gx[..., :96], f64(dx0[..., :96]))
+    assert_close(blocks.host_f64(dw), oracle.conv_wgrad(xs, f64(dybig[..., 288:]), s), "dw from views")
+
+
+# the last three exceed 512 reduce blocks; (3000000, 48) and (250000, 576) meet the block cap
+BN_CASES = [(1000, 8), (4097, 48), (2048, 96), (777, 576), (300, 64), (400000, 48), (3000000, 48), (250000, 576)]
 
 
 @pytest.mark.parametrize("m,c", BN_CASES)
