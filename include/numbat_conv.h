@@ -133,6 +133,19 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream);
 
+/* numbat_conv_fwd without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same arguments, results and checks as numbat_conv_fwd; the per-tile statistics partials
+ * go to a static scratch array of 8 MiB that the library holds on every GPU it runs on
+ * until the process ends (the same kernels run, so results equal numbat_conv_fwd's bit
+ * for bit).  Calls no allocating routine.  A problem whose partials exceed 8 MiB returns
+ * NUMBAT_ERR_WORKSPACE before any launch (the detector's layers need at most 4.7 MiB at
+ * batch 32).  Uses the scratch of the current device; the stream must belong to it.  All
+ * calls on one GPU share that scratch: calls that may overlap in time on one GPU (several
+ * streams, several host threads) race and must be ordered by the caller. */
+numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* x, const void* w, void* y,
+                                      float* batch_stats, void* stream);
+
 /* Data gradient of the forward convolution (its adjoint in x): the backward of the
  * detector's conv block (Sec. 6.1), whose training step runs a backward stage over every
  * layer (Sec. 8.2 stage timings); the operator-level check of Sec. 6.3 compares this

@@ -277,6 +277,110 @@ numbat_status check_ws(void* ws, size_t have, size_t need) {
   return NUMBAT_OK;
 }
 
+// the checks of numbat_conv_fwd that do not involve the workspace
+numbat_status check_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, const void* y,
+                             const float* batch_stats, ConvDesc* dp) {
+  ConvDesc& d = *dp;
+  numbat_status st = check_conv(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (x == nullptr || w == nullptr || y == nullptr) return fail(NUMBAT_ERR_NULL, "x, w and y are required");
+  const bool vec_in = !narrow(d);
+  if ((vec_in && (!aligned16(x) || !aligned16(w))) || !aligned16(y))
+    return fail(NUMBAT_ERR_ALIGN, "x, w, y must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w)) & 1u)
+    return fail(NUMBAT_ERR_ALIGN, "x and w must be 2-byte aligned");
+  if (batch_stats != nullptr && (reinterpret_cast<uintptr_t>(batch_stats) & 3u))
+    return fail(NUMBAT_ERR_ALIGN, "batch_stats must be 4-byte aligned");
+  return NUMBAT_OK;
+}
+
+// the forward's launches, once every check has passed; ws holds at least fwd_stats_bytes(d)
+// bytes when batch_stats is given
+numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, void* y, float* batch_stats, void* ws,
+                              void* stream) {
+  const bool vec_in = !narrow(d);
+  const TileCfg t = fwd_tile(d);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  char* wsp = static_cast<char*>(ws);
+  float2* part = batch_stats ? reinterpret_cast<float2*>(wsp) : nullptr;
+  const bf16_t* src = static_cast<const bf16_t*>(x);
+  const bf16_t* wt = static_cast<const bf16_t*>(w);
+  const int64_t src_pix = d.x_pix;
+  const int cs = d.ci;
+  ConvGemmArgs g;
+  std::memset(&g, 0, sizeof g);
+  g.src = src;
+  g.src_pix = src_pix;
+  g.hs = d.h;
+  g.ws = d.w;
+  g.cs = cs;
+  g.nout = d.co;
+  g.nimg = d.n;
+  g.gstride_h = d.sh;
+  g.gstride_w = d.sw;
+  g.dst = static_cast<bf16_t*>(y);
+  g.dst_pix = d.y_pix;
+  g.hd = d.ho;
+  g.wd = d.wo;
+  g.dstep_h = g.dstep_w = 1;
+  g.stats_part = part;
+  g.nphase = 1;
+  GemmPhase& P = g.ph[0];
+  P.wt = wt;
+  P.taps = d.kh * d.kw;
+  P.ktot = P.taps * cs;
+  P.gh = d.ho;
+  P.gw = d.wo;
+  P.m = (int32_t)d.m;
+  P.div_gw = make_fastdiv((uint32_t)d.wo);
+  P.div_ghw = make_fastdiv((uint32_t)(d.ho * d.wo));
+  for (int r = 0; r < d.kh; ++r)
+    for (int q = 0; q < d.kw; ++q)
+      P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
+  e = vec_in ? convgemm_launch(g, t, s, KC_CONV_FWD) : convnarrow_launch(g, t, s);
+  if (e != hipSuccess) return hip_fail(e, "conv forward launch");
+  if (batch_stats) {
+    const int mt = (int)((d.m + t.bm - 1) / t.bm);
+    e = stats_merge_launch(part, mt, t.bm, d.m, d.co, batch_stats, s);
+    if (e != hipSuccess) return hip_fail(e, "batch statistics merge launch");
+  }
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch for numbat_conv_fwd_noalloc: a file-scope device array (each GPU holds its
+// own copy for the life of the process).  Its device address is looked up once per device
+// with that device current; host code uses only that address, never the array's name.
+constexpr size_t kScratchBytes = (size_t)8 << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+// (calls that use it on one GPU share it: overlapping calls race)
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+numbat_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(NUMBAT_ERR_DEVICE, "device index %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "static scratch address (hipGetSymbolAddress)");
+    if (ptr == nullptr) return fail(NUMBAT_ERR_DEVICE, "static scratch address (hipGetSymbolAddress) is NULL");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return NUMBAT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -373,67 +477,29 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream) {
   ConvDesc d;
-  numbat_status st = check_conv(p, &d);
+  numbat_status st = check_conv_fwd(p, x, w, y, batch_stats, &d);
   if (st != NUMBAT_OK) return st;
-  if (x == nullptr || w == nullptr || y == nullptr) return fail(NUMBAT_ERR_NULL, "x, w and y are required");
-  const bool vec_in = !narrow(d);
-  if ((vec_in && (!aligned16(x) || !aligned16(w))) || !aligned16(y))
-    return fail(NUMBAT_ERR_ALIGN, "x, w, y must be 16-byte aligned");
-  if ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(w)) & 1u)
-    return fail(NUMBAT_ERR_ALIGN, "x and w must be 2-byte aligned");
-  if (batch_stats != nullptr && (reinterpret_cast<uintptr_t>(batch_stats) & 3u))
-    return fail(NUMBAT_ERR_ALIGN, "batch_stats must be 4-byte aligned");
-  const size_t need = batch_stats ? fwd_stats_bytes(d) : 0;
-  st = check_ws(ws, ws_bytes, need);
+  st = check_ws(ws, ws_bytes, batch_stats ? fwd_stats_bytes(d) : 0);
   if (st != NUMBAT_OK) return st;
+  return conv_fwd_launch(d, x, w, y, batch_stats, ws, stream);
+}
 
-  const TileCfg t = fwd_tile(d);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e;
-  char* wsp = static_cast<char*>(ws);
-  float2* part = batch_stats ? reinterpret_cast<float2*>(wsp) : nullptr;
-  const bf16_t* src = static_cast<const bf16_t*>(x);
-  const bf16_t* wt = static_cast<const bf16_t*>(w);
-  const int64_t src_pix = d.x_pix;
-  const int cs = d.ci;
-  ConvGemmArgs g;
-  std::memset(&g, 0, sizeof g);
-  g.src = src;
-  g.src_pix = src_pix;
-  g.hs = d.h;
-  g.ws = d.w;
-  g.cs = cs;
-  g.nout = d.co;
-  g.nimg = d.n;
-  g.gstride_h = d.sh;
-  g.gstride_w = d.sw;
-  g.dst = static_cast<bf16_t*>(y);
-  g.dst_pix = d.y_pix;
-  g.hd = d.ho;
-  g.wd = d.wo;
-  g.dstep_h = g.dstep_w = 1;
-  g.stats_part = part;
-  g.nphase = 1;
-  GemmPhase& P = g.ph[0];
-  P.wt = wt;
-  P.taps = d.kh * d.kw;
-  P.ktot = P.taps * cs;
-  P.gh = d.ho;
-  P.gw = d.wo;
-  P.m = (int32_t)d.m;
-  P.div_gw = make_fastdiv((uint32_t)d.wo);
-  P.div_ghw = make_fastdiv((uint32_t)(d.ho * d.wo));
-  for (int r = 0; r < d.kh; ++r)
-    for (int q = 0; q < d.kw; ++q)
-      P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
-  e = vec_in ? convgemm_launch(g, t, s, KC_CONV_FWD) : convnarrow_launch(g, t, s);
-  if (e != hipSuccess) return hip_fail(e, "conv forward launch");
-  if (batch_stats) {
-    const int mt = (int)((d.m + t.bm - 1) / t.bm);
-    e = stats_merge_launch(part, mt, t.bm, d.m, d.co, batch_stats, s);
-    if (e != hipSuccess) return hip_fail(e, "batch statistics merge launch");
+numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* x, const void* w, void* y,
+                                      float* batch_stats, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv_fwd(p, x, w, y, batch_stats, &d);
+  if (st != NUMBAT_OK) return st;
+  const size_t need = batch_stats ? fwd_stats_bytes(d) : 0;
+  if (need > kScratchBytes)
+    return fail(NUMBAT_ERR_WORKSPACE,
+                "problem needs %zu bytes of scratch; the static scratch of numbat_conv_fwd_noalloc holds %zu "
+                "(use numbat_conv_fwd with a workspace)", need, kScratchBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    st = scratch_of_current_device(&ws);
+    if (st != NUMBAT_OK) return st;
   }
-  return ok();
+  return conv_fwd_launch(d, x, w, y, batch_stats, ws, stream);
 }
 
 numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,

@@ -24,7 +24,7 @@ EXPORTED = (
     "numbat_abi_version", "numbat_last_error", "numbat_status_string", "numbat_conv_output_shape",
     "numbat_workspace_size", "numbat_conv_fwd", "numbat_conv_bwd_data", "numbat_conv_bwd_weight",
     "numbat_bn_silu_fwd", "numbat_bn_silu_bwd", "numbat_kernel_class_count", "numbat_kernel_class_name",
-    "numbat_timing_enable", "numbat_timing_read",
+    "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc",
 )
 
 
@@ -71,6 +71,7 @@ def load() -> ctypes.CDLL:
                                                          ctypes.POINTER(ctypes.c_int32)]),
             "numbat_workspace_size": (ctypes.c_int, [ctypes.c_int, P, ctypes.POINTER(S)]),
             "numbat_conv_fwd": (ctypes.c_int, [CP, P, P, P, P, P, S, P]),
+            "numbat_conv_fwd_noalloc": (ctypes.c_int, [CP, P, P, P, P, P]),
             "numbat_conv_bwd_data": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
             "numbat_conv_bwd_weight": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
             "numbat_bn_silu_fwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
@@ -164,6 +165,12 @@ def numbat_conv_fwd(p, x, w, y, batch_stats=None, ws=None, stream=None, ws_bytes
     _check(load().numbat_conv_fwd(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(y), _ptr(batch_stats), _ptr(ws),
                                   _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
            "numbat_conv_fwd")
+
+
+def numbat_conv_fwd_noalloc(p, x, w, y, batch_stats=None, stream=None):
+    _check(load().numbat_conv_fwd_noalloc(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(y), _ptr(batch_stats),
+                                          _stream(stream)),
+           "numbat_conv_fwd_noalloc")
 
 
 def numbat_conv_bwd_data(p, dy, w, dx, accumulate=False, ws=None, stream=None, ws_bytes=None):

@@ -21,7 +21,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -134,3 +134,22 @@ def test_timing_facility_without_launches():
     assert nb.numbat_timing_read(0) == (0.0, 0)
     nb.numbat_timing_enable(False)
     assert status_of(nb.numbat_timing_read, n) == nb.ERR_BAD_DESC
+
+
+def test_noalloc_forward_refuses_before_any_launch():
+    """The static-scratch forward checks like numbat_conv_fwd and refuses a problem whose
+    statistics partials exceed its 8 MiB scratch, all before touching a GPU."""
+    fake = 1 << 20
+    p = nb.conv_problem(2, 8, 8, 16, 32, 3)
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_fwd_noalloc(p, None, fake, fake, fake)
+    assert ei.value.status == nb.ERR_NULL
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_fwd_noalloc(p, fake + 2, fake, fake, fake)
+    assert ei.value.status == nb.ERR_ALIGN
+    big = nb.conv_problem(64, 640, 640, 16, 576, 3)
+    assert nb.numbat_workspace_size(nb.OP_CONV_FWD, big) > 8 << 20
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_fwd_noalloc(big, fake, fake, fake, fake)
+    assert ei.value.status == nb.ERR_WORKSPACE
+    assert "static scratch" in nb.numbat_last_error()
