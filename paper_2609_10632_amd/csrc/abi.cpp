@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -178,8 +179,26 @@ numbat_status check_conv(const numbat_conv_problem* p, ConvDesc* d) {
 bool narrow(const ConvDesc& d) { return d.ci % 8 != 0; }
 size_t x8_bytes(const ConvDesc& d) { return round_up((size_t)d.n * d.h * d.w * 16, 256); }
 
+// 3x3, stride-1, padding-1 problems whose reduction channels (c_in for the forward, c_out
+// for the data gradient) are 16-multiples of at least 32 run the halo kernel: it stages each
+// tile's input halo once per 32-channel chunk instead of gathering every tap
+bool halo_geometry(const ConvDesc& d) {
+  bool on = d.kh == 3 && d.kw == 3 && d.sh == 1 && d.sw == 1 && d.ph == 1 && d.pw == 1;
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_HALO")) on = on && atoi(e) != 0;
+#endif
+  return on;
+}
+TileCfg halo_tile(const ConvDesc& d, int cs, int nout, bool bt) {
+  if (!halo_geometry(d) || cs % 16 != 0 || cs < 32 || (int64_t)nout * 9 * cs * 2 >= ((int64_t)1 << 31) - 16)
+    return TileCfg{0, 0, -1, kVariantGeneric};
+  return convhalo_pick(d.m, nout, d.w, bt);
+}
+
 TileCfg fwd_tile(const ConvDesc& d) {
   if (narrow(d)) return narrow_pick(d.co);
+  const TileCfg h = halo_tile(d, d.ci, d.co, false);
+  if (h.variant == kVariantHalo) return h;
   return convgemm_pick(d.m, d.co, d.ci, d.kh * d.kw * d.ci, 1, false);
 }
 
@@ -338,7 +357,10 @@ numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, v
   for (int r = 0; r < d.kh; ++r)
     for (int q = 0; q < d.kw; ++q)
       P.off[r * d.kw + q] = (int32_t)((uint32_t)(uint16_t)(int16_t)(r - d.ph) | ((uint32_t)(q - d.pw) << 16));
-  e = vec_in ? convgemm_launch(g, t, s, KC_CONV_FWD) : convnarrow_launch(g, t, s);
+  if (t.variant == kVariantHalo)
+    e = convhalo_launch(g, t, s, KC_CONV_FWD);
+  else
+    e = vec_in ? convgemm_launch(g, t, s, KC_CONV_FWD) : convnarrow_launch(g, t, s);
   if (e != hipSuccess) return hip_fail(e, "conv forward launch");
   if (batch_stats) {
     const int mt = (int)((d.m + t.bm - 1) / t.bm);
@@ -538,6 +560,42 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
     na.wo = d.wo;
     na.accumulate = accumulate ? 1 : 0;
     e = dgrad_narrow_launch(na, d.ci, static_cast<float*>(ws), s);
+    if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
+    return ok();
+  }
+
+  const TileCfg ht = halo_tile(d, d.co, d.ci, true);
+  if (ht.variant == kVariantHalo) {
+    // a 3x3 stride-1 data gradient is the forward convolution of dy with the flipped,
+    // transposed weights, which the halo kernel reads in place
+    ConvGemmArgs g;
+    std::memset(&g, 0, sizeof g);
+    g.src = static_cast<const bf16_t*>(dy);
+    g.src_pix = d.y_pix;
+    g.hs = d.ho;
+    g.ws = d.wo;
+    g.cs = d.co;
+    g.nout = d.ci;
+    g.nimg = d.n;
+    g.gstride_h = g.gstride_w = 1;
+    g.dst = static_cast<bf16_t*>(dx);
+    g.dst_pix = d.x_pix;
+    g.hd = d.h;
+    g.wd = d.w;
+    g.dstep_h = g.dstep_w = 1;
+    g.accumulate = accumulate ? 1 : 0;
+    g.nphase = 1;
+    g.bt = 1;
+    GemmPhase& P = g.ph[0];
+    P.wt = static_cast<const bf16_t*>(w);
+    P.taps = 9;
+    P.ktot = 9 * d.co;
+    P.gh = d.h;
+    P.gw = d.w;
+    P.m = (int32_t)((int64_t)d.n * d.h * d.w);
+    P.div_gw = make_fastdiv((uint32_t)d.w);
+    P.div_ghw = make_fastdiv((uint32_t)(d.h * d.w));
+    e = convhalo_launch(g, ht, s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
     return ok();
   }

@@ -1070,6 +1070,312 @@ __global__ __launch_bounds__(256) void convstem_kernel(ConvGemmArgs a) {
   gemm_epilogue<2, 2>(a, P, T, acc, m0, 0, smem, s_dst, s_red, s_mean);
 }
 
+// ---------------------------------------------------------------------------
+// 3x3, stride-1, padding-1 convolutions (the forward and, with the weights read in place
+// and flipped, the data gradient): the input halo of a tile is staged in LDS once per
+// 32-channel chunk and all nine taps are read out of it.  A tile is BM consecutive output
+// pixels (linear over image, row, column); the source pixels its taps reach are the
+// contiguous linear range [m0 - W - 1, m0 + BM + W + 1), because tap (r, s) of output
+// pixel m reads source pixel m + (r - 1) W + (s - 1) whenever that pixel is inside the
+// image (taps that leave the image read zeros instead: each lane keeps the LDS address of
+// every tap of its rows, pointing at a zero row for the taps outside the image).  Per
+// chunk the tile loads about BM + 2W pixels instead of 9 BM, so the loads are mostly the
+// weights.
+//
+// Pipeline: one step is KT taps (1, or a whole tap row of 3) of one chunk, 32 reduction
+// elements per tap: the weights of those taps (BN rows of 64 bytes per tap, or for the
+// data gradient 32 rows of BN columns read with transposing LDS reads) in one of SB
+// stages (prefetch distance SB - 1 steps), and the chunk's halo, two deep: the next
+// chunk's halo is issued at the first step of the current one.  The waits are exact: at
+// step s the loads issued after the weights of s are the later steps' weights, plus the
+// next halo on the steps right after a chunk's first.  Every step issues the same loads;
+// past the end of K they read zeros.  Halo buffers and weight stages are distinct LDS
+// objects selected at compile time (two chunks per loop trip), so the compiler can tell an
+// in-flight load's target from the buffer being read.
+template <int TM, int TN, int HI, int KT, int SB, bool BT>
+struct HaloShape {
+  using G = GemmShape<TM, TN, 4>;
+  static constexpr int NW = 4;
+  static constexpr int SPC = 9 / KT;                   // steps per chunk
+  static constexpr int HPAD = HI * NW * 16;            // halo pixels per buffer (16 per load instruction)
+  static constexpr int HBYTES = (HPAD + 1) * 64;       // + one zero row read by out-of-image taps
+  static constexpr int H0BYTES = HBYTES >= G::STAGE_BYTES ? HBYTES : G::STAGE_BYTES;  // buffer 0 stages the epilogue
+  static constexpr int TBYTES = G::BN * 64;            // the weights of one tap: BN x 32 elements
+  static constexpr int BI = KT * G::BN / 16;           // weight load instructions per step (all waves)
+  static constexpr int BI_MIN = BI / NW, BI_MAX = (BI + NW - 1) / NW;
+  static_assert(KT == 1 || KT == 3, "one tap or one tap row per step");
+  static_assert((2 * SPC) % SB == 0, "stage of a step known at compile time over two chunks");
+  static_assert(SB >= 2 && SB - 1 <= SPC, "prefetch within one chunk");
+};
+
+template <int TM, int TN, int HI, int KT, int SB, bool BT>
+__global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
+  using G = GemmShape<TM, TN, 4>;
+  using Sh = HaloShape<TM, TN, HI, KT, SB, BT>;
+  constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM, NW = 4, SPC = Sh::SPC, D = SB - 1;
+  constexpr int BI = Sh::BI, BI_MIN = Sh::BI_MIN, BI_MAX = Sh::BI_MAX, TBYTES = Sh::TBYTES;
+  static_assert((D - 1) * BI_MIN + HI <= 60, "load counter range");
+
+  __shared__ __attribute__((aligned(16))) unsigned char sH0[Sh::H0BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char sH1[Sh::HBYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char sB0[KT * TBYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char sB1[KT * TBYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char sB2[SB > 2 ? KT * TBYTES : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char sB3[SB > 3 ? KT * TBYTES : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char sB4[SB > 4 ? KT * TBYTES : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char sB5[SB > 5 ? KT * TBYTES : 16];
+  __shared__ int64_t s_dst[BM];
+  __shared__ float s_red[NW][BN];
+  __shared__ float s_mean[BN];
+  auto hbuf = [&](auto hc) __attribute__((always_inline)) -> unsigned char* {
+    if constexpr (decltype(hc)::value == 0) return sH0;
+    else return sH1;
+  };
+  auto bstage = [&](auto bc) __attribute__((always_inline)) -> unsigned char* {
+    constexpr int b = decltype(bc)::value;
+    if constexpr (b == 0) return sB0;
+    else if constexpr (b == 1) return sB1;
+    else if constexpr (b == 2) return sB2;
+    else if constexpr (b == 3) return sB3;
+    else if constexpr (b == 4) return sB4;
+    else return sB5;
+  };
+
+  const TileId T{(int)blockIdx.x, (int)blockIdx.y, 0};
+  const GemmPhase& P = a.ph[0];
+  const Geo Ge = load_geo(P);
+  const int m0 = T.mt * BM;
+  const int n0 = T.nt * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, half = lane >> 5;
+  const int W = a.ws, H = a.hs, cs = a.cs, nout = a.nout;
+  const int64_t pix2 = a.src_pix * 2;
+  const int64_t npix = (int64_t)a.nimg * H * W;
+
+  // zero rows read by out-of-image taps (never a load target)
+  if (tid < 4) {
+    *reinterpret_cast<u32x4*>(sH0 + Sh::HPAD * 64 + tid * 16) = u32x4{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4*>(sH1 + Sh::HPAD * 64 + tid * 16) = u32x4{0u, 0u, 0u, 0u};
+  }
+
+  // ---- halo loads: instruction q of this wave fills pixels (q*NW + wave)*16 .. +16; the
+  // lane's slot is lane % 4 of pixel lane / 4, holding chunk slot ^ ((pixel >> 2) & 3)
+  const int64_t hbase_px = (int64_t)m0 - W - 1;
+  const __amdgpu_buffer_rsrc_t rsA = buffer_rsrc(a.src + hbase_px * a.src_pix);
+  uint32_t hoff[HI];
+  int hc8[HI];  // channel of the lane's chunk within a 32-channel chunk
+#pragma unroll
+  for (int q = 0; q < HI; ++q) {
+    const int j = (q * NW + wave) * 16 + (lane >> 2);
+    const int lc = (lane & 3) ^ ((j >> 2) & 3);
+    const int64_t src_px = hbase_px + j;
+    const bool ok = src_px >= 0 && src_px < npix && j < BM + 2 * W + 2;
+    hoff[q] = ok ? (uint32_t)(j * pix2 + lc * 16) : kOob;
+    hc8[q] = ok ? lc * 8 : (1 << 20);
+  }
+  // ---- weight loads: instruction u of a step covers 1 KiB of tap u / (BI / KT)'s stage
+  const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
+  constexpr int BPT = BN / 16;  // load instructions per tap
+  uint32_t boff[BI_MAX];
+  int bch[BI_MAX];  // non-transposed: channel of the lane's chunk; transposed: o row of the stage
+  int btap[BI_MAX];  // tap of the step (0 .. KT-1) the instruction loads
+#pragma unroll
+  for (int j = 0; j < BI_MAX; ++j) {
+    const int u = j * NW + wave;     // instruction index within the step
+    const int tp = u / BPT, v = u % BPT;
+    btap[j] = tp;
+    if constexpr (!BT) {
+      // stage row = output channel n0 + row, 64 bytes = 32 channels of one tap
+      const int row = v * 16 + (lane >> 2), o = n0 + row;
+      const int lc = (lane & 3) ^ ((row >> 2) & 3);
+      const bool ok = u < BI && o < nout;
+      boff[j] = ok ? (uint32_t)(((int64_t)o * 9 * cs + tp * cs + lc * 8) * 2) : kOob;
+      bch[j] = ok ? lc * 8 : (1 << 20);
+    } else {
+      // stage row = reduction channel o (of the 32-channel chunk), 2*BN bytes = output
+      // channels n0 .. n0 + BN of one (flipped) tap
+      const int byte = v * 1024 + lane * 16;
+      const int row = byte / (2 * BN), slot = (byte % (2 * BN)) / 16;
+      const int ch = slot ^ bt_swizzle<BN>(row);
+      const bool ok = u < BI && n0 + ch * 8 < nout;
+      boff[j] = ok ? (uint32_t)(((int64_t)row * 9 * nout + n0 + ch * 8) * 2) : kOob;
+      bch[j] = ok ? row : (1 << 20);
+    }
+  }
+  const int nchunk = (cs + 31) / 32;
+  const int nsteps = SPC * nchunk;
+
+  auto issue_halo = [&](auto hc, int c) __attribute__((always_inline)) {
+    unsigned char* Hb = hbuf(hc);
+    const int cb = 32 * c;
+#pragma unroll
+    for (int q = 0; q < HI; ++q) {
+      const uint32_t v = cb + hc8[q] < cs ? hoff[q] : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void_t*)(Hb + (q * NW + wave) * 1024), 16, v,
+                                               (uint32_t)(cb * 2), 0, 0);
+    }
+  };
+  // weights of step s (chunk s / SPC, taps KT * (s % SPC) ..) into stage bc
+  auto issue_b = [&](auto bc, int s) __attribute__((always_inline)) {
+    unsigned char* Bb = bstage(bc);
+    const int c = s / SPC, t0 = KT * (s - SPC * c), cb = 32 * c;
+    const bool live = s < nsteps;
+    uint32_t so;
+    if constexpr (!BT) so = (uint32_t)((t0 * cs + cb) * 2);
+    else so = (uint32_t)(((int64_t)cb * 9 + 8 - t0) * nout * 2);  // the flipped tap 8 - t
+#pragma unroll
+    for (int j = 0; j < BI_MAX; ++j) {
+      if (j * NW + wave < BI) {  // wave-uniform
+        const uint32_t v = (live && cb + bch[j] < cs) ? boff[j] : kOob;
+        // (transposed: tap t0 + btap is 8 - t0 - btap, btap rows of weights lower)
+        const uint32_t sv = BT ? so - (uint32_t)(btap[j] * nout * 2) : so;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void_t*)(Bb + (j * NW + wave) * 1024), 16, v, sv, 0, 0);
+      }
+    }
+  };
+
+  // ---- this lane's A rows: the LDS address of every tap of its rows (zero row outside)
+  uint32_t aaddr[TM][9];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int prow = wave * WTM + i * 32 + l32;
+    const int m = m0 + prow;
+    uint32_t mask = 0;
+    if (m < Ge.m) {
+      uint32_t img, oh, ow;
+      geo_pos((uint32_t)m, Ge, img, oh, ow);
+#pragma unroll
+      for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+          const bool in = (unsigned)((int)oh + r - 1) < (unsigned)H && (unsigned)((int)ow + s - 1) < (unsigned)W;
+          mask |= (in ? 1u : 0u) << (3 * r + s);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        const int p = prow + r * W + s;
+        const uint32_t ad = (uint32_t)(p * 64 + (((half) ^ ((p >> 2) & 3)) << 4));
+        const uint32_t zr = (uint32_t)(Sh::HPAD * 64 + half * 16);
+        aaddr[i][3 * r + s] = ((mask >> (3 * r + s)) & 1u) ? ad : zr;
+      }
+  }
+  // transposed B reads (see convdma_kernel): lane l = 16 g + 4 e + q reads 4 columns of
+  // rows 8 (g / 2) + e and that + 4 of each 16-row slice
+  uint32_t btoff[BT ? TN : 1];
+  if constexpr (BT) {
+    const int g = lane >> 4, e = (lane & 15) >> 2, q = lane & 3;
+    const int r0 = 8 * (g >> 1) + e;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int c = 4 * j + 2 * (g & 1) + (q >> 1);
+      btoff[j] = (uint32_t)(r0 * 2 * BN + (c ^ bt_swizzle<BN>(r0)) * 16 + (q & 1) * 8);
+    }
+  }
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // multiply one tap (t, within the step's stage at tap slot tk) from halo buffer hc
+  auto compute_tap = [&](const unsigned char* Hb, const unsigned char* Bb, auto tc) __attribute__((always_inline)) {
+    constexpr int t = decltype(tc)::value;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      u32x4 af[TM], bf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const u32x4*>(Hb + (aaddr[i][t] ^ (uint32_t)(32 * ks)));
+      if constexpr (!BT) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int row = j * 32 + l32;
+          bf[j] = *reinterpret_cast<const u32x4*>(Bb + row * 64 + ((((2 * ks + half) ^ ((row >> 2) & 3))) << 4));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const unsigned char* pb = Bb + btoff[j] + ks * 16 * 2 * BN;
+          const v4s_t r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)pb);
+          const v4s_t r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(pb + 4 * 2 * BN));
+          const v2u_t lo = __builtin_bit_cast(v2u_t, r0), hi = __builtin_bit_cast(v2u_t, r1);
+          bf[j][0] = lo.x;
+          bf[j][1] = lo.y;
+          bf[j][2] = hi.x;
+          bf[j][3] = hi.y;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
+    }
+  };
+  // wait for this wave's loads of the step (N later loads stay in flight), then every wave's
+  auto sync = [&](auto nc) __attribute__((always_inline)) {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(decltype(nc)::value) : "memory");
+  };
+  // step k (0 .. SPC-1) of a chunk c of parity h (halo buffer h): wait, issue the next
+  // halo (k = 0) and the weights D steps ahead, multiply the step's KT taps
+  auto step = [&](auto hc, auto kc, int c) __attribute__((always_inline)) {
+    constexpr int h = decltype(hc)::value, k = decltype(kc)::value;
+    constexpr int sl = h * SPC + k;  // step index within the two-chunk trip
+    constexpr int waitn = (D - 1) * BI_MIN + ((k >= 1 && k <= D - 1) ? HI : 0);
+    sync(Ic<waitn>{});
+    if constexpr (k == 0) issue_halo(Ic<1 - h>{}, c + 1);
+    issue_b(Ic<(sl + D) % SB>{}, SPC * c + k + D);
+    const unsigned char* Hb = hbuf(hc);
+    const unsigned char* Bb = bstage(Ic<sl % SB>{});
+#pragma unroll
+    for (int tt = 0; tt < KT; ++tt) {
+      // (compile-time tap index: KT * k + tt)
+      if constexpr (KT == 1) compute_tap(Hb, Bb, Ic<k>{});
+      else {
+        if (tt == 0) compute_tap(Hb, Bb, Ic<3 * k + 0>{});
+        if (tt == 1) compute_tap(Hb, Bb + TBYTES, Ic<3 * k + 1>{});
+        if (tt == 2) compute_tap(Hb, Bb + 2 * TBYTES, Ic<3 * k + 2>{});
+      }
+    }
+  };
+  auto chunk = [&](auto hc, int c) __attribute__((always_inline)) {
+    step(hc, Ic<0>{}, c);
+    step(hc, Ic<1>{}, c);
+    step(hc, Ic<2>{}, c);
+    if constexpr (SPC == 9) {
+      step(hc, Ic<3>{}, c);
+      step(hc, Ic<4>{}, c);
+      step(hc, Ic<5>{}, c);
+      step(hc, Ic<6>{}, c);
+      step(hc, Ic<7>{}, c);
+      step(hc, Ic<8>{}, c);
+    }
+  };
+
+  issue_halo(Ic<0>{}, 0);
+  issue_b(Ic<0>{}, 0);
+  if constexpr (D >= 2) issue_b(Ic<1>{}, 1);
+  if constexpr (D >= 3) issue_b(Ic<2>{}, 2);
+  if constexpr (D >= 4) issue_b(Ic<3>{}, 3);
+  if constexpr (D >= 5) issue_b(Ic<4>{}, 4);
+  // destination offsets of the tile's rows (the epilogue's), under the first loads
+  for (int r = tid; r < BM; r += NW * 64) s_dst[r] = dst_offset(a, Ge, m0 + r);
+  int c = 0;
+  for (; c + 2 <= nchunk; c += 2) {
+    chunk(Ic<0>{}, c);
+    chunk(Ic<1>{}, c + 1);
+  }
+  if (c < nchunk) chunk(Ic<0>{}, c);
+  // the loads issued past the last step land before the halo buffer becomes staging space
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+  gemm_epilogue<TM, TN, NW>(a, P, T, acc, m0, n0, sH0, s_dst, s_red, s_mean);
+}
+
 template <int TN>
 hipError_t launch_narrow(const ConvGemmArgs& a, hipStream_t s) {
   using G = GemmShape<2, TN>;
@@ -1133,6 +1439,57 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
     hipLaunchKernelGGL((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
+}
+
+// halo kernel instantiations: (32-row tiles per wave, 32-column tiles, halo load
+// instructions per wave, taps per step, weight stages); a BM-row tile of a W-wide image
+// needs BM + 2 W + 2 halo pixels, 16 per instruction
+struct HInst {
+  int tm, tn, hi, kt, sb;
+};
+constexpr HInst kH[] = {
+    {1, 3, 4, 3, 2},  // 0: 128 x 96, W <= 63, a tap row per step, two weight stages
+    {2, 3, 7, 1, 3},  // 1: 256 x 96, W <= 95, one tap per step, three weight stages
+    {1, 2, 4, 3, 2},  // 2: 128 x 64, W <= 63
+    {2, 2, 7, 1, 3},  // 3: 256 x 64, W <= 95
+#ifdef NUMBAT_TUNING
+    {1, 3, 4, 1, 3},   // 4..
+    {1, 3, 5, 1, 3},
+    {2, 3, 6, 1, 3},
+    {1, 2, 8, 1, 3},
+    {2, 2, 10, 1, 3},
+    {1, 3, 4, 1, 6},
+    {1, 3, 4, 3, 3},
+    {2, 3, 6, 1, 6},
+    {2, 3, 6, 3, 2},
+    {1, 3, 5, 1, 6},
+    {1, 3, 5, 3, 2},
+    {2, 3, 7, 1, 6},
+    {2, 3, 7, 3, 2},
+#endif
+};
+constexpr int kNumH = sizeof(kH) / sizeof(kH[0]);
+
+template <int I>
+hipError_t launch_h(const ConvGemmArgs& a, hipStream_t s) {
+  if constexpr (I < kNumH) {
+    constexpr HInst c = kH[I];
+    using G = GemmShape<c.tm, c.tn, 4>;
+    dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
+    if (a.bt)
+      hipLaunchKernelGGL((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true>), grid, dim3(256), 0, s, a);
+    else
+      hipLaunchKernelGGL((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false>), grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  } else {
+    return hipErrorInvalidValue;
+  }
+}
+
+template <int I>
+hipError_t launch_h_id(int id, const ConvGemmArgs& a, hipStream_t s) {
+  if constexpr (I >= kNumH) return hipErrorInvalidValue;
+  else return id == I ? launch_h<I>(a, s) : launch_h_id<I + 1>(id, a, s);
 }
 
 int tap_dh(int32_t off) { return (int)(int16_t)(off & 0xffff); }
@@ -1339,6 +1696,61 @@ hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int 
     case 6: e = launch_g<6>(a, variant, s); break;
     default: e = launch_g<7>(a, variant, s); break;
   }
+  trace_end(cls, s);
+  return e;
+}
+
+// 3x3, stride 1, padding 1, 16-multiple source channels (at least 32), one phase
+bool convhalo_shape(const ConvGemmArgs& a) {
+  const GemmPhase& P = a.ph[0];
+  if (a.nphase != 1 || a.cs % 16 != 0 || a.cs < 32 || P.taps != 9 || a.gstride_h != 1 || a.gstride_w != 1 ||
+      a.dstep_h != 1 || a.dstep_w != 1 || P.gh != a.hs || P.gw != a.ws || a.hd != a.hs || a.wd != a.ws)
+    return false;
+  if (!a.bt)
+    for (int r = 0; r < 3; ++r)
+      for (int q = 0; q < 3; ++q)
+        if (P.off[r * 3 + q] != (int32_t)((uint32_t)(uint16_t)(int16_t)(r - 1) | ((uint32_t)(q - 1) << 16)))
+          return false;
+  // weight offsets of one step are 32-bit
+  return (int64_t)a.nout * 9 * a.cs * 2 < (int64_t)kRecords;
+}
+
+// Halo kernel tile, from a sweep of the instantiations over the detector's 3x3 stride-1
+// layers at batch 16 (each layer alone): 96 columns when 96 divides the channel count, else
+// 64; images up to 63 pixels wide on 128-row tiles with a whole tap row (three taps) per
+// step and two weight stages (40 x 40, 192 channels: forward 33.6 -> 29.6 us, data
+// gradient 29.4 -> 24.0), up to 95 wide on 256-row tiles with one tap per step and three
+// stages (80 x 80, 96 channels: 35.4 -> 28.3 and 28.9 -> 22.6 us); wider images (the
+// 160-wide, 48-channel layers measured 30-80% slower on every instantiation) and forward
+// grids of fewer than 256 tiles (20 x 20, 288 channels: 23.6 -> 26.1 us) keep the
+// direct-to-LDS kernel.  Returns variant kVariantGeneric when the halo kernel is not used.
+TileCfg convhalo_pick(int64_t m, int nout, int w, bool bt) {
+  const int tn = nout % 96 == 0 ? 3 : 2;
+  int tm = w <= 63 ? 1 : 2, kt = w <= 63 ? 3 : 1, sb = w <= 63 ? 2 : 3;
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_HALO_TM")) tm = atoi(e);
+  if (const char* e = getenv("NUMBAT_HALO_KT")) kt = atoi(e);
+  if (const char* e = getenv("NUMBAT_HALO_SB")) sb = atoi(e);
+#endif
+  const TileCfg none{0, 0, -1, kVariantGeneric};
+  const int64_t tiles = ((m + 128 * tm - 1) / (128 * tm)) * ((nout + 32 * tn - 1) / (32 * tn));
+  if (!bt && tiles < 256) return none;
+  int best = -1;
+  for (int i = 0; i < kNumH; ++i) {
+    const HInst& c = kH[i];
+    if (c.tm != tm || c.tn != tn || c.kt != kt || c.sb != sb) continue;
+    if (c.hi * 64 < 128 * tm + 2 * w + 2) continue;
+    if (best < 0 || c.hi < kH[best].hi) best = i;
+  }
+  if (best < 0) return none;
+  return TileCfg{128 * kH[best].tm, 32 * kH[best].tn, best, kVariantHalo};
+}
+
+hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
+  if (t.variant != kVariantHalo || t.id < 0 || t.id >= kNumH || !convhalo_shape(a)) return hipErrorInvalidValue;
+  if (kH[t.id].hi * 64 < t.bm + 2 * a.ws + 2) return hipErrorInvalidValue;
+  trace_begin(cls, s);
+  const hipError_t e = launch_h_id<0>(t.id, a, s);
   trace_end(cls, s);
   return e;
 }

@@ -35,7 +35,7 @@ void trace_end(int cls, hipStream_t s);
 // into registers), and the direct-to-LDS kernel for 16-multiple channel counts of at least
 // 32 in its stage configurations (three or two stages, 32- or 64-element steps, four or
 // eight waves)
-enum { kVariantGeneric = 0, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5, kVariantDma3W8 = 7 };
+enum { kVariantGeneric = 0, kVariantDma3 = 3, kVariantDma2 = 4, kVariantDma32 = 5, kVariantDma3W8 = 7, kVariantHalo = 11 };
 struct TileCfg {
   int bm, bn;
   int id;       // instantiation id
@@ -101,6 +101,15 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot, int nphase, boo
 hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int cls);
 // whether the direct-to-LDS kernel takes the problem on tile t (it can read B in place)
 bool convgemm_direct(ConvGemmArgs a, const TileCfg& t);
+// 3x3, stride-1, padding-1 convolutions whose input halo is staged in LDS once per
+// 32-channel chunk (conv_gemm.hip, convhalo_kernel): the forward (K-major weights, taps in
+// off[]) and the data gradient (bt: the OHWI weights read in place, flipped; off[] unused).
+// convhalo_shape: whether the kernel takes the problem; convhalo_pick: its tile for m rows,
+// nout columns and a w-wide image, bt for the data gradient (variant kVariantGeneric when
+// the halo kernel is not the one to use).
+bool convhalo_shape(const ConvGemmArgs& a);
+TileCfg convhalo_pick(int64_t m, int nout, int w, bool bt);
+hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
 // forward convolution of a narrow input (cs = ci < 8, one phase, wt = OHWI weights with
 // K = taps * ci packed densely); rows per tile and columns per tile of narrow_pick
 TileCfg narrow_pick(int nout);

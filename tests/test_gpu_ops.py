@@ -64,6 +64,21 @@ CONV_CASES = [
     (2, 10, 12, 64, 192, 3, 1),
     (1, 9, 11, 200, 576, 3, 2),
     (2, 9, 7, 576, 192, 1, 1),
+    # 3x3 stride-1 halo kernel.  Data gradients always take it (up to 95-wide images);
+    # forwards from 256 tiles up.  The detector's 80/40-wide shapes, tiny images (a tile
+    # spans many images), chunk tails (48, 80), the widest image each tile height takes
+    # (63 on 128 rows, 95 on 256) with forward grids over 256 tiles, 64-column tiles on
+    # both heights; the 160- and 191-wide cases stay on the direct-to-LDS kernel
+    (1, 160, 160, 48, 48, 3, 1),
+    (1, 80, 80, 96, 96, 3, 1),
+    (2, 40, 40, 192, 192, 3, 1),
+    (3, 5, 3, 32, 64, 3, 1),
+    (1, 23, 191, 64, 32, 3, 1),
+    (2, 21, 19, 80, 48, 3, 1),
+    (8, 66, 63, 32, 96, 3, 1),
+    (6, 120, 95, 48, 96, 3, 1),
+    (9, 90, 90, 32, 64, 3, 1),
+    (10, 64, 60, 32, 64, 3, 1),
 ]
 
 
