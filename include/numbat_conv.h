@@ -71,7 +71,8 @@ typedef enum {
   NUMBAT_OP_CONV_BWD_DATA = 1,
   NUMBAT_OP_CONV_BWD_WEIGHT = 2,
   NUMBAT_OP_BN_SILU_FWD = 3,
-  NUMBAT_OP_BN_SILU_BWD = 4
+  NUMBAT_OP_BN_SILU_BWD = 4,
+  NUMBAT_OP_CLIP_SGD_NESTEROV = 5 /* problem ignored (may be NULL) */
 } numbat_op;
 
 /* One 2-D convolution (dilation 1, one group).  Output size
@@ -201,6 +202,43 @@ numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, cons
                                  const float* save_mean, const float* save_rstd, const float* gamma,
                                  const float* beta, void* dy, float* dgamma, float* dbeta, void* residual_grad,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/* One fp32 parameter tensor of the optimiser step: its values, gradient and momentum
+ * buffer (device pointers, n elements each) and its parameter group. */
+typedef struct {
+  float* w;           /* parameters, updated in place */
+  const float* grad;  /* gradient of the loss */
+  float* momentum;    /* momentum buffer, updated in place; zeros before the first step */
+  int64_t n;          /* elements */
+  int32_t group;      /* parameter group, 0 .. ngroups-1 (a tensor outside them is left unchanged) */
+  int32_t reserved;   /* 0 */
+} numbat_param_tensor;
+
+/* Learning rate and weight decay of one parameter group. */
+typedef struct {
+  float lr;
+  float weight_decay;
+} numbat_sgd_group;
+
+/* The optimiser step after the weight gradients (Sec. 3.2 optimisation; Table 1 optimisation
+ * row): global-norm gradient clipping as one squared-norm accumulation over every gradient
+ * (Table 2 #7: clip at 10.0 every step), then SGD with Nesterov momentum in parameter groups
+ * (three in the case study: decayed weights, undecayed normalisation gains, undecayed biases),
+ * with the reference-default semantics:
+ *   total = sqrt(sum over every tensor and element of grad^2)
+ *   c     = min(1, max_norm / (total + 1e-6))
+ *   d     = c * grad + weight_decay[group] * w
+ *   momentum = momentum_factor * momentum + d            (no dampening)
+ *   w     = w - lr[group] * (d + momentum_factor * momentum)
+ * tensors: DEVICE array of `count` numbat_param_tensor (1 .. 1024), read by the kernels (the
+ * caller keeps it for the life of the call); all pointers in it are device pointers, 16-byte
+ * aligned ones take the vector path.  groups: HOST array of ngroups (1 .. 8) entries.
+ * total_norm: NULL, or a device float receiving `total`.  No host synchronisation: the norm
+ * stays on the device.  The sum is taken in fp64 in a fixed order, so results are bitwise
+ * reproducible.  ws: numbat_workspace_size(NUMBAT_OP_CLIP_SGD_NESTEROV) bytes (8 KiB). */
+numbat_status numbat_clip_sgd_nesterov(const numbat_param_tensor* tensors, int32_t count,
+                                       const numbat_sgd_group* groups, int32_t ngroups, float momentum_factor,
+                                       float max_norm, float* total_norm, void* ws, size_t ws_bytes, void* stream);
 
 /* Launch timing, for measurement (the paper times its training step phase by phase,
  * Sec. 8): while enabled, every kernel the library launches is bracketed by two HIP

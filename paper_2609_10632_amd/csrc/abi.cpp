@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
+#include <cstddef>
 #include <cstdlib>
 #include <cstdio>
 #include <cstring>
@@ -47,7 +48,7 @@ hipEvent_t pool_event() {
 const char* const kClassNames[KC_COUNT] = {
     "conv_fwd_igemm", "stats_merge", "dgrad_weight_relayout", "conv_dgrad_igemm", "wgrad_igemm",
     "wgrad_splitk_reduce", "bn_stats", "bn_silu_fwd_apply", "bn_silu_bwd_reduce", "bn_silu_bwd_finalize",
-    "bn_silu_bwd_apply", "narrow_input_pack"};
+    "bn_silu_bwd_apply", "narrow_input_pack", "opt_sumsq", "opt_update"};
 
 }  // namespace
 
@@ -484,6 +485,9 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
                                                                                     : bwd_weight_ws(d, nullptr, nullptr);
       return ok();
     }
+    case NUMBAT_OP_CLIP_SGD_NESTEROV:
+      *bytes = round_up((size_t)kOptBlocks * sizeof(double), 256);
+      return ok();
     case NUMBAT_OP_BN_SILU_FWD:
     case NUMBAT_OP_BN_SILU_BWD: {
       BnDesc d;
@@ -884,6 +888,42 @@ numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, cons
                                gamma, beta, static_cast<bf16_t*>(dy), dgamma, dbeta, static_cast<bf16_t*>(residual_grad),
                                part, nb, coef, s);
   if (e != hipSuccess) return hip_fail(e, "BN+SiLU backward launch");
+  return ok();
+}
+
+static_assert(sizeof(numbat_param_tensor) == sizeof(OptTensor) && offsetof(numbat_param_tensor, n) == offsetof(OptTensor, n) &&
+                  offsetof(numbat_param_tensor, group) == offsetof(OptTensor, group),
+              "numbat_param_tensor and OptTensor share one layout");
+
+numbat_status numbat_clip_sgd_nesterov(const numbat_param_tensor* tensors, int32_t count,
+                                       const numbat_sgd_group* groups, int32_t ngroups, float momentum_factor,
+                                       float max_norm, float* total_norm, void* ws, size_t ws_bytes, void* stream) {
+  if (tensors == nullptr || groups == nullptr) return fail(NUMBAT_ERR_NULL, "tensors and groups are required");
+  if (reinterpret_cast<uintptr_t>(tensors) & 7u) return fail(NUMBAT_ERR_ALIGN, "tensors must be 8-byte aligned");
+  if (total_norm != nullptr && (reinterpret_cast<uintptr_t>(total_norm) & 3u))
+    return fail(NUMBAT_ERR_ALIGN, "total_norm must be 4-byte aligned");
+  if (count < 1 || count > kOptMaxTensors)
+    return fail(NUMBAT_ERR_BAD_DESC, "count = %d: 1 .. %d tensors", count, kOptMaxTensors);
+  if (ngroups < 1 || ngroups > kOptMaxGroups)
+    return fail(NUMBAT_ERR_BAD_DESC, "ngroups = %d: 1 .. %d groups", ngroups, kOptMaxGroups);
+  if (!(momentum_factor >= 0.0f && momentum_factor < 1.0f))
+    return fail(NUMBAT_ERR_BAD_DESC, "momentum_factor must be in [0, 1)");
+  if (!(max_norm > 0.0f && max_norm < 3.0e38f)) return fail(NUMBAT_ERR_BAD_DESC, "max_norm must be positive and finite");
+  OptGroups g;
+  std::memset(&g, 0, sizeof g);
+  g.count = ngroups;
+  for (int i = 0; i < ngroups; ++i) {
+    const float lr = groups[i].lr, wd = groups[i].weight_decay;
+    if (!(lr >= 0.0f && lr < 3.0e38f) || !(wd >= 0.0f && wd < 3.0e38f))
+      return fail(NUMBAT_ERR_BAD_DESC, "group %d: lr and weight_decay must be finite and >= 0", i);
+    g.lr[i] = lr;
+    g.wd[i] = wd;
+  }
+  numbat_status st = check_ws(ws, ws_bytes, round_up((size_t)kOptBlocks * sizeof(double), 256));
+  if (st != NUMBAT_OK) return st;
+  const hipError_t e = opt_clip_sgd_launch(reinterpret_cast<const OptTensor*>(tensors), count, g, momentum_factor, max_norm,
+                                           total_norm, static_cast<double*>(ws), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "optimiser step launch");
   return ok();
 }
 

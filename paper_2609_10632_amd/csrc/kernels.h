@@ -26,6 +26,8 @@ enum KernelClass {
   KC_BN_BWD_FINALIZE,   // BN + SiLU backward finalize
   KC_BN_BWD_APPLY,      // BN + SiLU backward apply
   KC_PACK,              // 8-channel repacking of a 3-channel image input
+  KC_OPT_SUMSQ,         // optimiser step: squared-norm partials of the gradients
+  KC_OPT_UPDATE,        // optimiser step: clipped SGD-Nesterov update
   KC_COUNT
 };
 void trace_begin(int cls, hipStream_t s);
@@ -189,5 +191,25 @@ hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var
 hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,
                          const float* save_rstd, const float* gamma, const float* beta, bf16_t* dy, float* dgamma,
                          float* dbeta, bf16_t* res_grad, float* part2, int nblocks, float* coef, hipStream_t s);
+
+// Optimiser step (optim.hip): global-norm clip + SGD-Nesterov over a device table of fp32
+// tensors.  OptTensor has the layout of numbat_param_tensor.
+struct OptTensor {
+  float* w;
+  const float* g;
+  float* mom;
+  int64_t n;
+  int32_t group;
+  int32_t reserved;
+};
+constexpr int kOptMaxGroups = 8;
+constexpr int kOptMaxTensors = 1024;  // the table is staged in LDS (40 bytes each)
+constexpr int kOptBlocks = 1024;      // blocks of both launches; part holds kOptBlocks doubles
+struct OptGroups {
+  int32_t count;
+  float lr[kOptMaxGroups], wd[kOptMaxGroups];
+};
+hipError_t opt_clip_sgd_launch(const OptTensor* tab, int count, const OptGroups& grp, float momentum, float max_norm,
+                               float* total_norm, double* part, hipStream_t s);
 
 }  // namespace numbat

@@ -18,13 +18,13 @@ LIB_PATH = os.path.join(HERE, "libnumbat_conv.so")
 NUMBAT_ABI_VERSION = 1
 
 OK, ERR_NULL, ERR_BAD_DESC, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE, ERR_DEVICE, ERR_VERSION = range(8)
-OP_CONV_FWD, OP_CONV_BWD_DATA, OP_CONV_BWD_WEIGHT, OP_BN_SILU_FWD, OP_BN_SILU_BWD = range(5)
+OP_CONV_FWD, OP_CONV_BWD_DATA, OP_CONV_BWD_WEIGHT, OP_BN_SILU_FWD, OP_BN_SILU_BWD, OP_CLIP_SGD_NESTEROV = range(6)
 
 EXPORTED = (
     "numbat_abi_version", "numbat_last_error", "numbat_status_string", "numbat_conv_output_shape",
     "numbat_workspace_size", "numbat_conv_fwd", "numbat_conv_bwd_data", "numbat_conv_bwd_weight",
     "numbat_bn_silu_fwd", "numbat_bn_silu_bwd", "numbat_kernel_class_count", "numbat_kernel_class_name",
-    "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc",
+    "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc", "numbat_clip_sgd_nesterov",
 )
 
 
@@ -41,6 +41,15 @@ class numbat_bn_problem(ctypes.Structure):
         ("momentum", ctypes.c_float), ("y_pixel_stride", ctypes.c_int64), ("a_pixel_stride", ctypes.c_int64),
         ("r_pixel_stride", ctypes.c_int64), ("dy_pixel_stride", ctypes.c_int64),
     ]
+
+
+class numbat_param_tensor(ctypes.Structure):
+    _fields_ = [("w", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("momentum", ctypes.c_void_p),
+                ("n", ctypes.c_int64), ("group", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class numbat_sgd_group(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("weight_decay", ctypes.c_float)]
 
 
 class NumbatError(RuntimeError):
@@ -72,6 +81,8 @@ def load() -> ctypes.CDLL:
             "numbat_workspace_size": (ctypes.c_int, [ctypes.c_int, P, ctypes.POINTER(S)]),
             "numbat_conv_fwd": (ctypes.c_int, [CP, P, P, P, P, P, S, P]),
             "numbat_conv_fwd_noalloc": (ctypes.c_int, [CP, P, P, P, P, P]),
+            "numbat_clip_sgd_nesterov": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(numbat_sgd_group),
+                                                         ctypes.c_int32, ctypes.c_float, ctypes.c_float, P, P, S, P]),
             "numbat_conv_bwd_data": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
             "numbat_conv_bwd_weight": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
             "numbat_bn_silu_fwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
@@ -200,6 +211,26 @@ def numbat_bn_silu_bwd(p, g, y, save_mean, save_rstd, gamma, beta, dy, dgamma, d
                                      _ptr(beta), _ptr(dy), _ptr(dgamma), _ptr(dbeta), _ptr(residual_grad), _ptr(ws),
                                      _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
            "numbat_bn_silu_bwd")
+
+
+def param_table(entries):
+    """numbat_param_tensor entries for (w, grad, momentum, group) tensor tuples, as bytes
+    laid out like the C array (upload them to the device to pass as `tensors`)."""
+    arr = (numbat_param_tensor * len(entries))()
+    for e, (w, g, m, grp) in zip(arr, entries):
+        e.w, e.grad, e.momentum, e.n, e.group, e.reserved = _ptr(w), _ptr(g), _ptr(m), w.numel(), grp, 0
+    return bytes(arr)
+
+
+def numbat_clip_sgd_nesterov(tensors, count, groups, momentum_factor, max_norm, total_norm=None, ws=None,
+                             stream=None, ws_bytes=None):
+    """tensors: device buffer holding `count` numbat_param_tensor entries; groups: list of
+    (lr, weight_decay) pairs."""
+    g = (numbat_sgd_group * len(groups))(*[numbat_sgd_group(lr, wd) for lr, wd in groups])
+    _check(load().numbat_clip_sgd_nesterov(_ptr(tensors), count, g, len(groups), momentum_factor, max_norm,
+                                           _ptr(total_norm), _ptr(ws), _nbytes(ws) if ws_bytes is None else ws_bytes,
+                                           _stream(stream)),
+           "numbat_clip_sgd_nesterov")
 
 
 def numbat_kernel_class_count() -> int:

@@ -21,7 +21,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -126,7 +126,7 @@ def test_entry_points_refuse_before_launch():
 
 def test_timing_facility_without_launches():
     n = nb.numbat_kernel_class_count()
-    assert n == 12
+    assert n == 14
     names = [nb.numbat_kernel_class_name(i) for i in range(n)]
     assert len(set(names)) == n and all(names)
     assert nb.numbat_kernel_class_name(n) == ""
@@ -153,3 +153,30 @@ def test_noalloc_forward_refuses_before_any_launch():
         nb.numbat_conv_fwd_noalloc(big, fake, fake, fake, fake)
     assert ei.value.status == nb.ERR_WORKSPACE
     assert "static scratch" in nb.numbat_last_error()
+
+
+def test_optimiser_step_refuses_before_any_launch():
+    fake = 1 << 20
+    ws_need = nb.numbat_workspace_size(nb.OP_CLIP_SGD_NESTEROV, nb.bn_problem(2, 8))
+    assert ws_need >= 1024 * 8
+    cases = [
+        (dict(tensors=None, count=3, groups=[(0.01, 0.0)]), nb.ERR_NULL),
+        (dict(tensors=fake + 4, count=3, groups=[(0.01, 0.0)]), nb.ERR_ALIGN),
+        (dict(tensors=fake, count=0, groups=[(0.01, 0.0)]), nb.ERR_BAD_DESC),
+        (dict(tensors=fake, count=2000, groups=[(0.01, 0.0)]), nb.ERR_BAD_DESC),
+        (dict(tensors=fake, count=3, groups=[(0.01, 0.0)] * 9), nb.ERR_BAD_DESC),
+        (dict(tensors=fake, count=3, groups=[(float("nan"), 0.0)]), nb.ERR_BAD_DESC),
+        (dict(tensors=fake, count=3, groups=[(0.01, -1.0)]), nb.ERR_BAD_DESC),
+    ]
+    for kw, code in cases:
+        with pytest.raises(nb.NumbatError) as ei:
+            nb.numbat_clip_sgd_nesterov(kw["tensors"], kw["count"], kw["groups"], 0.937, 10.0, ws=fake,
+                                        ws_bytes=ws_need)
+        assert ei.value.status == code, kw
+    for mom, mx in ((1.0, 10.0), (-0.1, 10.0), (0.9, 0.0), (0.9, float("inf"))):
+        with pytest.raises(nb.NumbatError) as ei:
+            nb.numbat_clip_sgd_nesterov(fake, 3, [(0.01, 0.0)], mom, mx, ws=fake, ws_bytes=ws_need)
+        assert ei.value.status == nb.ERR_BAD_DESC
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_clip_sgd_nesterov(fake, 3, [(0.01, 0.0)], 0.9, 10.0, ws=fake, ws_bytes=ws_need - 1)
+    assert ei.value.status == nb.ERR_WORKSPACE
