@@ -265,3 +265,20 @@ def block_bwd(g, x, w, s: ConvShape, fwd, gamma, beta, eps):
     dx = conv_dgrad(dy, w, s)
     dw = conv_wgrad(x, dy, s)
     return {"dy": dy, "dgamma": dgamma, "dbeta": dbeta, "dx": dx, "dw": dw}
+
+
+# ---------------------------------------------------------------------------
+# Inference (evaluation) mode: BN with running statistics (Table 2 divergence #9: eval-mode
+# BN for validation), and the bias of the detect head's 1x1 prediction convolutions
+# (Sec. 6.1 decoupled head).
+
+
+def conv_fwd_bias(x, w, bias, s: ConvShape) -> np.ndarray:
+    """y = conv(x, w) + bias[o] on every output pixel."""
+    return conv_fwd(x, w, s) + np.asarray(bias, np.float64)
+
+
+def bn_silu_eval(y, running_mean, running_var, gamma, beta, eps, residual=None):
+    """a = SiLU(gamma * (y - running_mean) / sqrt(running_var + eps) + beta) [+ residual]: the
+    training-mode formula with the running statistics in place of the batch's."""
+    return bn_silu_fwd(y, running_mean, running_var, gamma, beta, eps, residual)
