@@ -134,6 +134,21 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream);
 
+/* Forward convolution plus a per-channel bias, y = conv(x, w) + bias[o]: the detect head's
+ * 1x1 prediction convolutions, which carry a bias and no BN (Sec. 6.1 decoupled head).  Same
+ * layouts and checks as numbat_conv_fwd; bias: fp32 [c_out]; no statistics, no workspace. */
+numbat_status numbat_conv_fwd_bias(const numbat_conv_problem* p, const void* x, const void* w, const float* bias,
+                                   void* y, void* stream);
+
+/* Inference-mode Conv -> BN -> SiLU in one pass: BN with running statistics (evaluation
+ * mode, Table 2 #9), folded into the convolution's output stage:
+ *   y = SiLU(gamma * (conv(x, w) - running_mean) / sqrt(running_var + eps) + beta)
+ * computed from the fp32 accumulators, rounded once to bf16.  Same layouts and checks as
+ * numbat_conv_fwd; gamma, beta, running_mean, running_var: fp32 [c_out]; no workspace. */
+numbat_status numbat_conv_bn_silu_infer(const numbat_conv_problem* p, const void* x, const void* w,
+                                        const float* gamma, const float* beta, const float* running_mean,
+                                        const float* running_var, float eps, void* y, void* stream);
+
 /* numbat_conv_fwd without a workspace, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
  * Same arguments, results and checks as numbat_conv_fwd; the per-tile statistics partials
@@ -187,6 +202,14 @@ numbat_status numbat_bn_silu_fwd(const numbat_bn_problem* p, const void* y, cons
                                  const float* gamma, const float* beta, const void* residual, void* out,
                                  float* save_mean, float* save_rstd, float* running_mean, float* running_var,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/* BN (evaluation mode, running statistics; Table 2 #9) + SiLU on a stored conv output:
+ *   out = SiLU(gamma * (y - running_mean) / sqrt(running_var + eps) + beta) [+ residual]
+ * with eps = p->eps (p->momentum unused); layouts and pixel strides as numbat_bn_silu_fwd;
+ * nothing is saved or updated; no workspace. */
+numbat_status numbat_bn_silu_infer(const numbat_bn_problem* p, const void* y, const float* running_mean,
+                                   const float* running_var, const float* gamma, const float* beta,
+                                   const void* residual, void* out, void* stream);
 
 /* Backward of numbat_bn_silu_fwd with batch statistics, given g = dL/d(out): BN is trained
  * in fp32 under mixed precision (Sec. 3.2, Table 1 precision row) with batch statistics in

@@ -179,3 +179,37 @@ class C2fBlock:
         grads[0] = self.cv1.backward(dcat[..., :self.c2], st["x"], w, g, b, st["cv1"], ws=self.ws,
                                      g_pixel_stride=self.catc)
         return grads, grads[0]["dx"]
+
+
+class DetectHeadInfer:
+    """One scale of the architecture-faithful decoupled detect head (Sec. 6.1) in inference
+    mode on the C ABI: a box branch (3x3 c -> 64, 3x3 64 -> 64, 1x1 64 -> 64 + bias) and a
+    class branch (3x3 c -> 192, 3x3 192 -> 192, 1x1 192 -> 80 + bias).  Each 3x3 layer is one
+    numbat_conv_bn_silu_infer call (BN with running statistics folded into the conv's output
+    stage); the two 1x1 prediction convs write channel slices 0..63 and 64..143 of one
+    [n, h, w, 144] output (zero-copy concatenation)."""
+
+    BOX, CLS, NCLS, REG = 64, 192, 80, 64
+
+    def __init__(self, n, h, c, eps=1e-3):
+        self.n, self.h, self.c, self.eps = n, h, c, eps
+        self.out_c = self.REG + self.NCLS
+        self.p3 = {co_ci: nb.conv_problem(n, h, h, co_ci[1], co_ci[0], 3) for co_ci in
+                   ((self.BOX, c), (self.BOX, self.BOX), (self.CLS, c), (self.CLS, self.CLS))}
+        self.p_box = nb.conv_problem(n, h, h, self.BOX, self.REG, 1, y_pixel_stride=self.out_c)
+        self.p_cls = nb.conv_problem(n, h, h, self.CLS, self.NCLS, 1, y_pixel_stride=self.out_c)
+
+    def forward(self, x, box, cls, stream=None):
+        """box / cls: [(w, gamma, beta, mean, var), (w, gamma, beta, mean, var), (w, bias)]."""
+        dev = x.device
+        out = torch.empty((self.n, self.h, self.h, self.out_c), dtype=torch.bfloat16, device=dev)
+        for layers, width, dst, p1 in ((box, self.BOX, out[..., :self.REG], self.p_box),
+                                       (cls, self.CLS, out[..., self.REG:], self.p_cls)):
+            a = x
+            for (w, g, b, m, v), ci in zip(layers[:2], (self.c, width)):
+                y = torch.empty((self.n, self.h, self.h, width), dtype=torch.bfloat16, device=dev)
+                nb.numbat_conv_bn_silu_infer(self.p3[(width, ci)], a, w, g, b, m, v, self.eps, y, stream=stream)
+                a = y
+            w, bias = layers[2]
+            nb.numbat_conv_fwd_bias(p1, a, w, bias, dst, stream=stream)
+        return out

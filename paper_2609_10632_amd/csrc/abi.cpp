@@ -316,8 +316,15 @@ numbat_status check_conv_fwd(const numbat_conv_problem* p, const void* x, const 
 
 // the forward's launches, once every check has passed; ws holds at least fwd_stats_bytes(d)
 // bytes when batch_stats is given
+// epilogue operation of the inference entry points (none for the training forward)
+struct PostOp {
+  int32_t kind = kPostNone;
+  float eps = 0.f;
+  const float *bias = nullptr, *gamma = nullptr, *beta = nullptr, *mean = nullptr, *var = nullptr;
+};
+
 numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, void* y, float* batch_stats, void* ws,
-                              void* stream) {
+                              void* stream, const PostOp& post = PostOp()) {
   const bool vec_in = !narrow(d);
   const TileCfg t = fwd_tile(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -345,6 +352,13 @@ numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, v
   g.wd = d.wo;
   g.dstep_h = g.dstep_w = 1;
   g.stats_part = part;
+  g.post = post.kind;
+  g.post_eps = post.eps;
+  g.post_bias = post.bias;
+  g.post_gamma = post.gamma;
+  g.post_beta = post.beta;
+  g.post_mean = post.mean;
+  g.post_var = post.var;
   g.nphase = 1;
   GemmPhase& P = g.ph[0];
   P.wt = wt;
@@ -526,6 +540,41 @@ numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* 
     if (st != NUMBAT_OK) return st;
   }
   return conv_fwd_launch(d, x, w, y, batch_stats, ws, stream);
+}
+
+numbat_status numbat_conv_fwd_bias(const numbat_conv_problem* p, const void* x, const void* w, const float* bias,
+                                   void* y, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv_fwd(p, x, w, y, nullptr, &d);
+  if (st != NUMBAT_OK) return st;
+  if (bias == nullptr) return fail(NUMBAT_ERR_NULL, "bias is required");
+  if (reinterpret_cast<uintptr_t>(bias) & 3u) return fail(NUMBAT_ERR_ALIGN, "bias must be 4-byte aligned");
+  PostOp op;
+  op.kind = kPostBias;
+  op.bias = bias;
+  return conv_fwd_launch(d, x, w, y, nullptr, nullptr, stream, op);
+}
+
+numbat_status numbat_conv_bn_silu_infer(const numbat_conv_problem* p, const void* x, const void* w,
+                                        const float* gamma, const float* beta, const float* running_mean,
+                                        const float* running_var, float eps, void* y, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv_fwd(p, x, w, y, nullptr, &d);
+  if (st != NUMBAT_OK) return st;
+  if (gamma == nullptr || beta == nullptr || running_mean == nullptr || running_var == nullptr)
+    return fail(NUMBAT_ERR_NULL, "gamma, beta, running_mean and running_var are required");
+  if ((reinterpret_cast<uintptr_t>(gamma) | reinterpret_cast<uintptr_t>(beta) |
+       reinterpret_cast<uintptr_t>(running_mean) | reinterpret_cast<uintptr_t>(running_var)) & 3u)
+    return fail(NUMBAT_ERR_ALIGN, "gamma, beta, running_mean and running_var must be 4-byte aligned");
+  if (!(eps >= 0.0f)) return fail(NUMBAT_ERR_BAD_DESC, "eps must be >= 0");
+  PostOp op;
+  op.kind = kPostBnSilu;
+  op.eps = eps;
+  op.gamma = gamma;
+  op.beta = beta;
+  op.mean = running_mean;
+  op.var = running_var;
+  return conv_fwd_launch(d, x, w, y, nullptr, nullptr, stream, op);
 }
 
 numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
@@ -860,9 +909,28 @@ numbat_status numbat_bn_silu_fwd(const numbat_bn_problem* p, const void* y, cons
     if (e != hipSuccess) return hip_fail(e, "batch statistics launch");
     mv = mean_var;
   }
-  hipError_t e = bn_fwd_launch(d.a, static_cast<const bf16_t*>(y), mv, gamma, beta, static_cast<const bf16_t*>(residual),
-                               static_cast<bf16_t*>(out), save_mean, save_rstd, running_mean, running_var, s);
+  hipError_t e = bn_fwd_launch(d.a, static_cast<const bf16_t*>(y), mv, mv + d.a.c, gamma, beta,
+                               static_cast<const bf16_t*>(residual), static_cast<bf16_t*>(out), save_mean, save_rstd,
+                               running_mean, running_var, s);
   if (e != hipSuccess) return hip_fail(e, "BN+SiLU forward launch");
+  return ok();
+}
+
+numbat_status numbat_bn_silu_infer(const numbat_bn_problem* p, const void* y, const float* running_mean,
+                                   const float* running_var, const float* gamma, const float* beta,
+                                   const void* residual, void* out, void* stream) {
+  BnDesc d;
+  numbat_status st = check_bn(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (y == nullptr || running_mean == nullptr || running_var == nullptr || gamma == nullptr || beta == nullptr ||
+      out == nullptr)
+    return fail(NUMBAT_ERR_NULL, "y, running_mean, running_var, gamma, beta and out are required");
+  if (!aligned16(y) || !aligned16(out) || (residual && !aligned16(residual)))
+    return fail(NUMBAT_ERR_ALIGN, "y, out and residual must be 16-byte aligned");
+  hipError_t e = bn_fwd_launch(d.a, static_cast<const bf16_t*>(y), running_mean, running_var, gamma, beta,
+                               static_cast<const bf16_t*>(residual), static_cast<bf16_t*>(out), nullptr, nullptr,
+                               nullptr, nullptr, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "BN+SiLU inference launch");
   return ok();
 }
 

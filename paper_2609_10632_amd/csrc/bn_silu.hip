@@ -97,17 +97,18 @@ __global__ __launch_bounds__(kThreads) void bn_stats_kernel(const bf16_t* y, int
 // --- forward apply: out = SiLU((y - mean) * gamma * rstd + beta) [+ residual].
 // Thread t always handles channel vector t % cv, so its per-channel constants sit in
 // registers; rows advance by rows_per_iter, four rows in flight.
-__global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t* y, const float* mean_var,
-                                                          const float* gamma, const float* beta, const bf16_t* res,
-                                                          bf16_t* out, float* save_mean, float* save_rstd,
-                                                          float* run_mean, float* run_var, int64_t rows_per_block) {
+__global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t* y, const float* mean,
+                                                          const float* var_in, const float* gamma, const float* beta,
+                                                          const bf16_t* res, bf16_t* out, float* save_mean,
+                                                          float* save_rstd, float* run_mean, float* run_var,
+                                                          int64_t rows_per_block, int stat_block) {
   const int t = threadIdx.x;
-  // the last block only publishes the saved statistics and updates the running ones, in
-  // parallel with the row blocks (done by a row block, it would lengthen that block by a
-  // round trip to memory)
-  if (blockIdx.x == gridDim.x - 1) {
+  // the last block (when save_mean is given) only publishes the saved statistics and
+  // updates the running ones, in parallel with the row blocks (done by a row block, it
+  // would lengthen that block by a round trip to memory)
+  if (stat_block && blockIdx.x == gridDim.x - 1) {
     for (int ch = t; ch < a.c; ch += kThreads) {
-      const float mu = mean_var[ch], var = mean_var[a.c + ch];
+      const float mu = mean[ch], var = var_in[ch];
       save_mean[ch] = mu;
       save_rstd[ch] = 1.0f / sqrtf(var + a.eps);
       if (run_mean != nullptr) {
@@ -125,8 +126,8 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
   float sc[8], bz[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    sc[e] = gamma[cb + e] * (1.0f / sqrtf(mean_var[a.c + cb + e] + a.eps));
-    bz[e] = beta[cb + e] - mean_var[cb + e] * sc[e];
+    sc[e] = gamma[cb + e] * (1.0f / sqrtf(var_in[cb + e] + a.eps));
+    bz[e] = beta[cb + e] - mean[cb + e] * sc[e];
   }
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
@@ -420,14 +421,15 @@ static int apply_blocks(int64_t m, int c, int64_t* rows_per_block) {
   return (int)((m + *rows_per_block - 1) / *rows_per_block);
 }
 
-hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var, const float* gamma,
+hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, const float* var, const float* gamma,
                          const float* beta, const bf16_t* res, bf16_t* out, float* save_mean, float* save_rstd,
                          float* run_mean, float* run_var, hipStream_t s) {
   int64_t rpb = 0;
   const int nb = apply_blocks(a.m, a.c, &rpb);
+  const int stat = save_mean != nullptr ? 1 : 0;
   trace_begin(KC_BN_FWD, s);
-  hipLaunchKernelGGL(bn_fwd_kernel, dim3(nb + 1), dim3(kThreads), 0, s, a, y, mean_var, gamma, beta, res, out, save_mean,
-                     save_rstd, run_mean, run_var, rpb);
+  hipLaunchKernelGGL(bn_fwd_kernel, dim3(nb + stat), dim3(kThreads), 0, s, a, y, mean, var, gamma, beta, res, out,
+                     save_mean, save_rstd, run_mean, run_var, rpb, stat);
   trace_end(KC_BN_FWD, s);
   return hipGetLastError();
 }

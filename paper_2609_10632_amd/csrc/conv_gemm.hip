@@ -206,6 +206,36 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
     }
   }
 
+  // ---- inference epilogue constants: per column a scale and a shift (bias: 1, bias[n];
+  // eval-mode BN: gamma rstd, beta - mean gamma rstd), in s_red rows 0 and 1 (the
+  // statistics, which share that space, are never asked for with them)
+  const int post = a.post;
+  if (post != kPostNone) {
+    __syncthreads();
+    if (tid < BN) {
+      const int col = n0 + tid;
+      float sc = 1.f, sh = 0.f;
+      if (col < a.nout) {
+        if (post == kPostBias) {
+          sh = a.post_bias[col];
+        } else {
+          sc = a.post_gamma[col] * (1.0f / sqrtf(a.post_var[col] + a.post_eps));
+          sh = a.post_beta[col] - a.post_mean[col] * sc;
+        }
+      }
+      s_red[0][tid] = sc;
+      s_red[1][tid] = sh;
+    }
+    __syncthreads();
+  }
+  auto post_op = [&](float (&f)[8], int c0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = __builtin_fmaf(f[e], s_red[0][c0 + e], s_red[1][c0 + e]);
+      f[e] = post == kPostBnSilu ? z * sigmoidf_fast(z) : z;
+    }
+  };
+
   // ---- output
   if ((a.nout & 7) == 0) {
     // stage 8 rows per wave in LDS as fp32 (register group g = r/4 of every 32-row block),
@@ -232,6 +262,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
             const float4 hi = *reinterpret_cast<const float4*>(&st[r * S::STAGE_LD + c8 * 8 + 4]);
             float f[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
             uint4* p = reinterpret_cast<uint4*>(a.dst + d + col);
+            if (post != kPostNone) post_op(f, c8 * 8);
             if (a.accumulate) {
               float o[8];
               unpack8(*p, o);
@@ -258,6 +289,10 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
           const int col = n0 + j * 32 + l32;
           if (col < a.nout) {
             float v = acc[i][j][r];
+            if (post != kPostNone) {
+              v = __builtin_fmaf(v, s_red[0][j * 32 + l32], s_red[1][j * 32 + l32]);
+              if (post == kPostBnSilu) v = v * sigmoidf_fast(v);
+            }
             if (a.accumulate) v += bf2f(a.dst[d + col]);
             a.dst[d + col] = (bf16_t)f2bf(v);
           }

@@ -93,8 +93,16 @@ struct ConvGemmArgs {
   int32_t halo_px;     // set by convgemm_launch: pixels the fast path's gather base sits before an image
   int32_t remap;       // set by convgemm_launch: XCD-aware tile order (see xcd_remap)
   int32_t bt;          // B is the OHWI weight tensor read in place (direct-to-LDS kernel only)
+  // epilogue operation on each fp32 result before rounding (inference paths; never with
+  // accumulate or statistics): kPostNone, kPostBias (+ bias[n]) or kPostBnSilu
+  // (SiLU(gamma (v - mean) / sqrt(var + eps) + beta) with running statistics)
+  int32_t post;
+  float post_eps;
+  const float* post_bias;
+  const float *post_gamma, *post_beta, *post_mean, *post_var;
   GemmPhase ph[kMaxPhases];
 };
+enum { kPostNone = 0, kPostBias = 1, kPostBnSilu = 2 };
 // tile and kernel for a problem with at most m_max rows per phase, nout columns, cs
 // source channels, reduction length ktot and nphase phases; bt: the weights are read in
 // place (transposed B) if the direct-to-LDS kernel takes the problem
@@ -185,7 +193,8 @@ struct BnArgs {
 int bn_reduce_blocks(int64_t m, int c);
 hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int nblocks, float* mean_var,
                            hipStream_t s);
-hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean_var, const float* gamma,
+// save_mean == nullptr: no saved or running statistics (inference with running statistics)
+hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, const float* var, const float* gamma,
                          const float* beta, const bf16_t* res, bf16_t* out, float* save_mean, float* save_rstd,
                          float* run_mean, float* run_var, hipStream_t s);
 hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,

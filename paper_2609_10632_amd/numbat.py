@@ -25,6 +25,7 @@ EXPORTED = (
     "numbat_workspace_size", "numbat_conv_fwd", "numbat_conv_bwd_data", "numbat_conv_bwd_weight",
     "numbat_bn_silu_fwd", "numbat_bn_silu_bwd", "numbat_kernel_class_count", "numbat_kernel_class_name",
     "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc", "numbat_clip_sgd_nesterov",
+    "numbat_conv_fwd_bias", "numbat_conv_bn_silu_infer", "numbat_bn_silu_infer",
 )
 
 
@@ -81,6 +82,9 @@ def load() -> ctypes.CDLL:
             "numbat_workspace_size": (ctypes.c_int, [ctypes.c_int, P, ctypes.POINTER(S)]),
             "numbat_conv_fwd": (ctypes.c_int, [CP, P, P, P, P, P, S, P]),
             "numbat_conv_fwd_noalloc": (ctypes.c_int, [CP, P, P, P, P, P]),
+            "numbat_conv_fwd_bias": (ctypes.c_int, [CP, P, P, P, P, P]),
+            "numbat_conv_bn_silu_infer": (ctypes.c_int, [CP, P, P, P, P, P, P, ctypes.c_float, P, P]),
+            "numbat_bn_silu_infer": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P]),
             "numbat_clip_sgd_nesterov": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(numbat_sgd_group),
                                                          ctypes.c_int32, ctypes.c_float, ctypes.c_float, P, P, S, P]),
             "numbat_conv_bwd_data": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
@@ -182,6 +186,23 @@ def numbat_conv_fwd_noalloc(p, x, w, y, batch_stats=None, stream=None):
     _check(load().numbat_conv_fwd_noalloc(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(y), _ptr(batch_stats),
                                           _stream(stream)),
            "numbat_conv_fwd_noalloc")
+
+
+def numbat_conv_fwd_bias(p, x, w, bias, y, stream=None):
+    _check(load().numbat_conv_fwd_bias(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(bias), _ptr(y), _stream(stream)),
+           "numbat_conv_fwd_bias")
+
+
+def numbat_conv_bn_silu_infer(p, x, w, gamma, beta, running_mean, running_var, eps, y, stream=None):
+    _check(load().numbat_conv_bn_silu_infer(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(gamma), _ptr(beta),
+                                            _ptr(running_mean), _ptr(running_var), eps, _ptr(y), _stream(stream)),
+           "numbat_conv_bn_silu_infer")
+
+
+def numbat_bn_silu_infer(p, y, running_mean, running_var, gamma, beta, residual, out, stream=None):
+    _check(load().numbat_bn_silu_infer(ctypes.byref(p), _ptr(y), _ptr(running_mean), _ptr(running_var), _ptr(gamma),
+                                       _ptr(beta), _ptr(residual), _ptr(out), _stream(stream)),
+           "numbat_bn_silu_infer")
 
 
 def numbat_conv_bwd_data(p, dy, w, dx, accumulate=False, ws=None, stream=None, ws_bytes=None):

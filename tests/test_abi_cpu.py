@@ -21,7 +21,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 19
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -180,3 +180,26 @@ def test_optimiser_step_refuses_before_any_launch():
     with pytest.raises(nb.NumbatError) as ei:
         nb.numbat_clip_sgd_nesterov(fake, 3, [(0.01, 0.0)], 0.9, 10.0, ws=fake, ws_bytes=ws_need - 1)
     assert ei.value.status == nb.ERR_WORKSPACE
+
+
+def test_inference_entry_points_refuse_before_any_launch():
+    fake = 1 << 20
+    p = nb.conv_problem(2, 8, 8, 16, 32, 3)
+    for args, code in (((p, fake, fake, None, fake), nb.ERR_NULL), ((p, fake, fake, fake + 2, fake), nb.ERR_ALIGN),
+                       ((p, fake + 2, fake, fake, fake), nb.ERR_ALIGN)):
+        with pytest.raises(nb.NumbatError) as ei:
+            nb.numbat_conv_fwd_bias(*args)
+        assert ei.value.status == code
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_bn_silu_infer(p, fake, fake, fake, None, fake, fake, 1e-3, fake)
+    assert ei.value.status == nb.ERR_NULL
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_bn_silu_infer(p, fake, fake, fake, fake, fake, fake, -1.0, fake)
+    assert ei.value.status == nb.ERR_BAD_DESC
+    b = nb.bn_problem(100, 48)
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_bn_silu_infer(b, fake, None, fake, fake, fake, None, fake)
+    assert ei.value.status == nb.ERR_NULL
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_bn_silu_infer(b, fake + 8, fake, fake, fake, fake, None, fake)
+    assert ei.value.status == nb.ERR_ALIGN
