@@ -263,6 +263,40 @@ numbat_status numbat_clip_sgd_nesterov(const numbat_param_tensor* tensors, int32
                                        const numbat_sgd_group* groups, int32_t ngroups, float momentum_factor,
                                        float max_norm, float* total_norm, void* ws, size_t ws_bytes, void* stream);
 
+/* A pooled or upsampled NHWC bf16 tensor: n images of h x w pixels, c channels (a multiple
+ * of 8).  For the max pool x / dx and y / dy are all n x h x w; for the upsampling x / dx
+ * are n x h x w and y / dy are n x 2h x 2w.  Pixel strides as in the other descriptors
+ * (0 means c), so operands can be channel slices of concatenation buffers. */
+typedef struct {
+  uint32_t struct_size;    /* = sizeof(numbat_pool_problem) */
+  int32_t n, h, w, c;
+  int64_t x_pixel_stride;  /* pixels of x and dx */
+  int64_t y_pixel_stride;  /* pixels of y and dy */
+} numbat_pool_problem;
+
+/* The SPPF block's max pool (Sec. 6.1 backbone; applied three times in a row): 5 x 5 window,
+ * stride 1, padding 2 that never wins:
+ *   y[n,p,q,c] = max over in-image (i, j) with |i - p| <= 2, |j - q| <= 2 of x[n,i,j,c]
+ * idx: NULL, or uint8 [n][h][w][c] (dense, 8-byte aligned) receiving the row-major window
+ * position r * 5 + s (0 .. 24) of each window's FIRST maximum (a later equal value does not
+ * replace it), the position the backward sends the gradient to. */
+numbat_status numbat_maxpool5_fwd(const numbat_pool_problem* p, const void* x, void* y, uint8_t* idx, void* stream);
+
+/* Backward of numbat_maxpool5_fwd: dx[n,i,j,c] = sum of dy over the windows whose stored
+ * first-maximum position is (i, j) (summed in fp32 in a fixed order, rounded once);
+ * accumulate != 0: dx += that sum. */
+numbat_status numbat_maxpool5_bwd(const numbat_pool_problem* p, const void* dy, const uint8_t* idx, void* dx,
+                                  int accumulate, void* stream);
+
+/* The neck's nearest-neighbour 2x upsampling (Sec. 6.1 PAN-FPN neck):
+ *   y[n, 2i + a, 2j + b, c] = x[n, i, j, c]   for a, b in {0, 1}. */
+numbat_status numbat_upsample2x_fwd(const numbat_pool_problem* p, const void* x, void* y, void* stream);
+
+/* Backward: dx[n,i,j,c] = sum over a, b of dy[n, 2i + a, 2j + b, c] (fp32, rounded once);
+ * accumulate != 0: dx += that sum. */
+numbat_status numbat_upsample2x_bwd(const numbat_pool_problem* p, const void* dy, void* dx, int accumulate,
+                                    void* stream);
+
 /* Launch timing, for measurement (the paper times its training step phase by phase,
  * Sec. 8): while enabled, every kernel the library launches is bracketed by two HIP
  * events recorded on its launch stream, and numbat_timing_read sums their elapsed times

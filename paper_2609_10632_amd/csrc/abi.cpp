@@ -48,7 +48,7 @@ hipEvent_t pool_event() {
 const char* const kClassNames[KC_COUNT] = {
     "conv_fwd_igemm", "stats_merge", "dgrad_weight_relayout", "conv_dgrad_igemm", "wgrad_igemm",
     "wgrad_splitk_reduce", "bn_stats", "bn_silu_fwd_apply", "bn_silu_bwd_reduce", "bn_silu_bwd_finalize",
-    "bn_silu_bwd_apply", "narrow_input_pack", "opt_sumsq", "opt_update"};
+    "bn_silu_bwd_apply", "narrow_input_pack", "opt_sumsq", "opt_update", "pool_upsample"};
 
 }  // namespace
 
@@ -992,6 +992,82 @@ numbat_status numbat_clip_sgd_nesterov(const numbat_param_tensor* tensors, int32
   const hipError_t e = opt_clip_sgd_launch(reinterpret_cast<const OptTensor*>(tensors), count, g, momentum_factor, max_norm,
                                            total_norm, static_cast<double*>(ws), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "optimiser step launch");
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// SPPF max pool and neck upsampling
+namespace {
+numbat_status check_pool(const numbat_pool_problem* p, PoolArgs* a) {
+  if (p == nullptr) return fail(NUMBAT_ERR_NULL, "problem descriptor is NULL");
+  if (p->struct_size != sizeof(numbat_pool_problem))
+    return fail(NUMBAT_ERR_VERSION, "numbat_pool_problem.struct_size is %u, this library expects %zu", p->struct_size,
+                sizeof(numbat_pool_problem));
+  if (p->n < 1 || p->h < 1 || p->w < 1 || p->c < 1)
+    return fail(NUMBAT_ERR_BAD_DESC, "sizes must be >= 1 (n=%d h=%d w=%d c=%d)", p->n, p->h, p->w, p->c);
+  if (p->c % 8 != 0) return fail(NUMBAT_ERR_UNSUPPORTED, "c = %d is not a multiple of 8", p->c);
+  a->n = p->n;
+  a->h = p->h;
+  a->w = p->w;
+  a->c = p->c;
+  a->x_pix = p->x_pixel_stride ? p->x_pixel_stride : p->c;
+  a->y_pix = p->y_pixel_stride ? p->y_pixel_stride : p->c;
+  if (a->x_pix < a->c || a->y_pix < a->c) return fail(NUMBAT_ERR_BAD_DESC, "a pixel stride is smaller than c");
+  if (a->x_pix % 8 != 0 || a->y_pix % 8 != 0) return fail(NUMBAT_ERR_ALIGN, "pixel strides must be multiples of 8");
+  if ((int64_t)p->n * p->h * p->w * 4 > kMaxIndex) return fail(NUMBAT_ERR_UNSUPPORTED, "more than 2^29 pixels");
+  return NUMBAT_OK;
+}
+}  // namespace
+
+numbat_status numbat_maxpool5_fwd(const numbat_pool_problem* p, const void* x, void* y, uint8_t* idx, void* stream) {
+  PoolArgs a;
+  numbat_status st = check_pool(p, &a);
+  if (st != NUMBAT_OK) return st;
+  if (x == nullptr || y == nullptr) return fail(NUMBAT_ERR_NULL, "x and y are required");
+  if (!aligned16(x) || !aligned16(y)) return fail(NUMBAT_ERR_ALIGN, "x and y must be 16-byte aligned");
+  if (idx != nullptr && (reinterpret_cast<uintptr_t>(idx) & 7u)) return fail(NUMBAT_ERR_ALIGN, "idx must be 8-byte aligned");
+  const hipError_t e = maxpool5_fwd_launch(a, static_cast<const bf16_t*>(x), static_cast<bf16_t*>(y), idx,
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "max pool launch");
+  return ok();
+}
+
+numbat_status numbat_maxpool5_bwd(const numbat_pool_problem* p, const void* dy, const uint8_t* idx, void* dx,
+                                  int accumulate, void* stream) {
+  PoolArgs a;
+  numbat_status st = check_pool(p, &a);
+  if (st != NUMBAT_OK) return st;
+  if (dy == nullptr || idx == nullptr || dx == nullptr) return fail(NUMBAT_ERR_NULL, "dy, idx and dx are required");
+  if (!aligned16(dy) || !aligned16(dx) || (reinterpret_cast<uintptr_t>(idx) & 7u))
+    return fail(NUMBAT_ERR_ALIGN, "dy and dx must be 16-byte and idx 8-byte aligned");
+  const hipError_t e = maxpool5_bwd_launch(a, static_cast<const bf16_t*>(dy), idx, static_cast<bf16_t*>(dx),
+                                           accumulate ? 1 : 0, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "max pool backward launch");
+  return ok();
+}
+
+numbat_status numbat_upsample2x_fwd(const numbat_pool_problem* p, const void* x, void* y, void* stream) {
+  PoolArgs a;
+  numbat_status st = check_pool(p, &a);
+  if (st != NUMBAT_OK) return st;
+  if (x == nullptr || y == nullptr) return fail(NUMBAT_ERR_NULL, "x and y are required");
+  if (!aligned16(x) || !aligned16(y)) return fail(NUMBAT_ERR_ALIGN, "x and y must be 16-byte aligned");
+  const hipError_t e = upsample2x_fwd_launch(a, static_cast<const bf16_t*>(x), static_cast<bf16_t*>(y),
+                                             static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "upsample launch");
+  return ok();
+}
+
+numbat_status numbat_upsample2x_bwd(const numbat_pool_problem* p, const void* dy, void* dx, int accumulate,
+                                    void* stream) {
+  PoolArgs a;
+  numbat_status st = check_pool(p, &a);
+  if (st != NUMBAT_OK) return st;
+  if (dy == nullptr || dx == nullptr) return fail(NUMBAT_ERR_NULL, "dy and dx are required");
+  if (!aligned16(dy) || !aligned16(dx)) return fail(NUMBAT_ERR_ALIGN, "dy and dx must be 16-byte aligned");
+  const hipError_t e = upsample2x_bwd_launch(a, static_cast<const bf16_t*>(dy), static_cast<bf16_t*>(dx),
+                                             accumulate ? 1 : 0, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "upsample backward launch");
   return ok();
 }
 

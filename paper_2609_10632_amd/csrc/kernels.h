@@ -28,6 +28,7 @@ enum KernelClass {
   KC_PACK,              // 8-channel repacking of a 3-channel image input
   KC_OPT_SUMSQ,         // optimiser step: squared-norm partials of the gradients
   KC_OPT_UPDATE,        // optimiser step: clipped SGD-Nesterov update
+  KC_POOL,              // SPPF max pool and neck upsampling, forward and backward
   KC_COUNT
 };
 void trace_begin(int cls, hipStream_t s);
@@ -200,6 +201,19 @@ hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, co
 hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,
                          const float* save_rstd, const float* gamma, const float* beta, bf16_t* dy, float* dgamma,
                          float* dbeta, bf16_t* res_grad, float* part2, int nblocks, float* coef, hipStream_t s);
+
+// SPPF max pool (5x5, stride 1, padding 2) and nearest 2x upsampling (pool.hip): n, h, w
+// of the pooled / low-resolution tensor, c channels (a multiple of 8), pixel strides of x
+// (and dx) and y (and dy); idx: one byte per element of y, dense [n][h][w][c]
+struct PoolArgs {
+  int32_t n, h, w, c;
+  int64_t x_pix, y_pix;
+};
+hipError_t maxpool5_fwd_launch(const PoolArgs& a, const bf16_t* x, bf16_t* y, uint8_t* idx, hipStream_t s);
+hipError_t maxpool5_bwd_launch(const PoolArgs& a, const bf16_t* dy, const uint8_t* idx, bf16_t* dx, int accumulate,
+                               hipStream_t s);
+hipError_t upsample2x_fwd_launch(const PoolArgs& a, const bf16_t* x, bf16_t* y, hipStream_t s);
+hipError_t upsample2x_bwd_launch(const PoolArgs& a, const bf16_t* dy, bf16_t* dx, int accumulate, hipStream_t s);
 
 // Optimiser step (optim.hip): global-norm clip + SGD-Nesterov over a device table of fp32
 // tensors.  OptTensor has the layout of numbat_param_tensor.

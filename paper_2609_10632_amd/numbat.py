@@ -26,6 +26,7 @@ EXPORTED = (
     "numbat_bn_silu_fwd", "numbat_bn_silu_bwd", "numbat_kernel_class_count", "numbat_kernel_class_name",
     "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc", "numbat_clip_sgd_nesterov",
     "numbat_conv_fwd_bias", "numbat_conv_bn_silu_infer", "numbat_bn_silu_infer",
+    "numbat_maxpool5_fwd", "numbat_maxpool5_bwd", "numbat_upsample2x_fwd", "numbat_upsample2x_bwd",
 )
 
 
@@ -42,6 +43,12 @@ class numbat_bn_problem(ctypes.Structure):
         ("momentum", ctypes.c_float), ("y_pixel_stride", ctypes.c_int64), ("a_pixel_stride", ctypes.c_int64),
         ("r_pixel_stride", ctypes.c_int64), ("dy_pixel_stride", ctypes.c_int64),
     ]
+
+
+class numbat_pool_problem(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("n", ctypes.c_int32), ("h", ctypes.c_int32),
+                ("w", ctypes.c_int32), ("c", ctypes.c_int32), ("x_pixel_stride", ctypes.c_int64),
+                ("y_pixel_stride", ctypes.c_int64)]
 
 
 class numbat_param_tensor(ctypes.Structure):
@@ -73,6 +80,7 @@ def load() -> ctypes.CDLL:
         lib = ctypes.CDLL(LIB_PATH)
         P, S = ctypes.c_void_p, ctypes.c_size_t
         CP, BP = ctypes.POINTER(numbat_conv_problem), ctypes.POINTER(numbat_bn_problem)
+        PP = ctypes.POINTER(numbat_pool_problem)
         sig = {
             "numbat_abi_version": (ctypes.c_uint32, []),
             "numbat_last_error": (ctypes.c_char_p, []),
@@ -85,6 +93,10 @@ def load() -> ctypes.CDLL:
             "numbat_conv_fwd_bias": (ctypes.c_int, [CP, P, P, P, P, P]),
             "numbat_conv_bn_silu_infer": (ctypes.c_int, [CP, P, P, P, P, P, P, ctypes.c_float, P, P]),
             "numbat_bn_silu_infer": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P]),
+            "numbat_maxpool5_fwd": (ctypes.c_int, [PP, P, P, P, P]),
+            "numbat_maxpool5_bwd": (ctypes.c_int, [PP, P, P, P, ctypes.c_int, P]),
+            "numbat_upsample2x_fwd": (ctypes.c_int, [PP, P, P, P]),
+            "numbat_upsample2x_bwd": (ctypes.c_int, [PP, P, P, ctypes.c_int, P]),
             "numbat_clip_sgd_nesterov": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(numbat_sgd_group),
                                                          ctypes.c_int32, ctypes.c_float, ctypes.c_float, P, P, S, P]),
             "numbat_conv_bwd_data": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
@@ -148,6 +160,30 @@ def bn_problem(m, c, eps=1e-3, momentum=0.03, y_pixel_stride=0, a_pixel_stride=0
                dy_pixel_stride=0):
     return numbat_bn_problem(ctypes.sizeof(numbat_bn_problem), c, m, eps, momentum, y_pixel_stride, a_pixel_stride,
                              r_pixel_stride, dy_pixel_stride)
+
+
+def pool_problem(n, h, w, c, x_pixel_stride=0, y_pixel_stride=0):
+    return numbat_pool_problem(ctypes.sizeof(numbat_pool_problem), n, h, w, c, x_pixel_stride, y_pixel_stride)
+
+
+def numbat_maxpool5_fwd(p, x, y, idx=None, stream=None):
+    _check(load().numbat_maxpool5_fwd(ctypes.byref(p), _ptr(x), _ptr(y), _ptr(idx), _stream(stream)),
+           "numbat_maxpool5_fwd")
+
+
+def numbat_maxpool5_bwd(p, dy, idx, dx, accumulate=False, stream=None):
+    _check(load().numbat_maxpool5_bwd(ctypes.byref(p), _ptr(dy), _ptr(idx), _ptr(dx), int(bool(accumulate)),
+                                      _stream(stream)),
+           "numbat_maxpool5_bwd")
+
+
+def numbat_upsample2x_fwd(p, x, y, stream=None):
+    _check(load().numbat_upsample2x_fwd(ctypes.byref(p), _ptr(x), _ptr(y), _stream(stream)), "numbat_upsample2x_fwd")
+
+
+def numbat_upsample2x_bwd(p, dy, dx, accumulate=False, stream=None):
+    _check(load().numbat_upsample2x_bwd(ctypes.byref(p), _ptr(dy), _ptr(dx), int(bool(accumulate)), _stream(stream)),
+           "numbat_upsample2x_bwd")
 
 
 def numbat_abi_version() -> int:

@@ -15,13 +15,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions():
     text = open(os.path.join(ROOT, "include", "numbat_conv.h")).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(numbat_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(numbat_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 23
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -126,7 +126,7 @@ def test_entry_points_refuse_before_launch():
 
 def test_timing_facility_without_launches():
     n = nb.numbat_kernel_class_count()
-    assert n == 14
+    assert n == 15
     names = [nb.numbat_kernel_class_name(i) for i in range(n)]
     assert len(set(names)) == n and all(names)
     assert nb.numbat_kernel_class_name(n) == ""
@@ -203,3 +203,20 @@ def test_inference_entry_points_refuse_before_any_launch():
     with pytest.raises(nb.NumbatError) as ei:
         nb.numbat_bn_silu_infer(b, fake + 8, fake, fake, fake, fake, None, fake)
     assert ei.value.status == nb.ERR_ALIGN
+
+
+def test_pool_entry_points_refuse_before_any_launch():
+    fake = 1 << 20
+    good = nb.pool_problem(2, 20, 20, 288)
+    assert ctypes.sizeof(nb.numbat_pool_problem) == 40
+    bad_c = nb.pool_problem(2, 20, 20, 12)
+    bad_stride = nb.pool_problem(2, 20, 20, 16, x_pixel_stride=8)
+    bad_ver = nb.pool_problem(2, 20, 20, 16)
+    bad_ver.struct_size = 8
+    for p, code in ((bad_c, nb.ERR_UNSUPPORTED), (bad_stride, nb.ERR_BAD_DESC), (bad_ver, nb.ERR_VERSION)):
+        assert status_of(nb.numbat_maxpool5_fwd, p, fake, fake) == code
+    assert status_of(nb.numbat_maxpool5_fwd, good, None, fake) == nb.ERR_NULL
+    assert status_of(nb.numbat_maxpool5_fwd, good, fake, fake, fake + 4) == nb.ERR_ALIGN
+    assert status_of(nb.numbat_maxpool5_bwd, good, fake, None, fake) == nb.ERR_NULL
+    assert status_of(nb.numbat_upsample2x_fwd, good, fake + 2, fake) == nb.ERR_ALIGN
+    assert status_of(nb.numbat_upsample2x_bwd, good, fake, None) == nb.ERR_NULL
