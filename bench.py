@@ -56,11 +56,256 @@ def parse():
     ap.add_argument("--wgrad-tail", type=int, default=8,
                     help="the last this many layers of the backward pass are enqueued one by one")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
-    ap.add_argument("--detail", type=str, default=None, help="write per-layer timings (JSON) to this file")
+    ap.add_argument("--detail", type=str, default=None,
+                    help="write per-layer x pass timings (JSON) to this file, and a markdown table beside it")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the extra measurements (chain mode, optimiser step, configuration 5, cold-cache "
+                         "steps, copy bandwidth)")
     return ap.parse_args()
 
 
+class SclkSampler:
+    """Samples the GPU's current shader clock (the starred level of pp_dpm_sclk) every 20 ms on
+    a host thread while active; mean / min / max in MHz."""
+
+    def __init__(self):
+        import glob
+        import threading
+
+        paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = paths[0] if paths else None
+        self.samples = []
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True) if self.path else None
+
+    def _read(self):
+        try:
+            for line in open(self.path):
+                if line.strip().endswith("*"):
+                    return float(line.split(":")[1].strip().split("Mhz")[0].split("MHz")[0])
+        except (OSError, ValueError, IndexError):
+            return None
+        return None
+
+    def _run(self):
+        while not self._stop.wait(0.02):
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+
+    def __enter__(self):
+        if self._t:
+            self._t.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._t:
+            self._t.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        v = self.samples
+        return {"mean_mhz": round(sum(v) / len(v), 1), "min_mhz": min(v), "max_mhz": max(v), "samples": len(v)}
+
+
+def hbm_copy_gbs(torch, nbytes=1 << 30, reps=10):
+    """Device-to-device copy of nbytes (read + write counted), GB/s: the achievable HBM figure."""
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del a, b
+    return round(gbs, 1)
+
+
+def graph_of(torch, step):
+    """Capture one step (after a side-stream warm-up) into a HIP graph."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_replays(torch, graph, steps):
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def cold_cache_ms(torch, graph, steps, evict_bytes=1 << 30):
+    """Median step time with the caches cold: before every timed replay a 1 GiB buffer is
+    written (more than the 256 MB Infinity Cache and the L2s hold), outside the events."""
+    buf = torch.empty(evict_bytes // 4, dtype=torch.float32, device="cuda")
+    times = []
+    for i in range(steps):
+        buf.fill_(float(i))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del buf
+    times.sort()
+    return round(times[len(times) // 2], 3)
+
+
+def chain_mode(torch, steps, warmup):
+    """The 65 layers as one network (real dataflow, SPPF pools, upsampling, concatenations) at
+    batch 16, 640 x 640, on one stream, graph-replayed."""
+    from paper_2609_10632_amd.detector import Detector
+
+    det = Detector(16, 640)
+    det.seeded(4)
+    for _ in range(warmup):
+        det.step()
+    g = graph_of(torch, det.step)
+    ms = time_replays(torch, g, steps)
+    out = {"ms_per_step": round(ms, 3), "tflops": round(det.flops / (ms / 1e3) / 1e12, 2),
+           "pct_mfma_peak": round(100 * det.flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+           "step_gflop": round(det.flops / 1e9, 2), "launch": "hip graph replay", "streams": 1,
+           "batch": 16, "input": "640x640"}
+    del g, det
+    torch.cuda.empty_cache()
+    return out
+
+
+def optimizer_step(torch, steps):
+    """The fused global-norm clip + SGD-Nesterov step over the detector's 243 parameter tensors
+    (25.9M fp32 parameters, three groups)."""
+    from paper_2609_10632_amd import numbat as nb
+    from paper_2609_10632_amd import workloads
+
+    shapes = []
+    for l, bn, bias in [(l, True, False) for l in workloads.backbone_neck_layers()] + \
+            workloads.faithful_head_param_tensors():
+        shapes.append((l.co * l.k * l.k * l.ci, 0))
+        if bn:
+            shapes += [(l.co, 1), (l.co, 2)]
+        if bias:
+            shapes.append((l.co, 2))
+    total = sum(n for n, _ in shapes)
+    w = torch.randn(total, device="cuda") * 0.05
+    g = torch.randn(total, device="cuda") * 1e-3
+    m = torch.zeros(total, device="cuda")
+    ents, pos = [], 0
+    for n, grp in shapes:
+        pad = (-pos) % 4  # 16-byte aligned tensors
+        pos += pad
+        ents.append((w[pos:pos + n], g[pos:pos + n], m[pos:pos + n], grp))
+        pos += n
+    table = torch.frombuffer(bytearray(nb.param_table(ents)), dtype=torch.uint8).cuda()
+    ws = torch.zeros(nb.numbat_workspace_size(nb.OP_CLIP_SGD_NESTEROV, nb.bn_problem(2, 8)), dtype=torch.uint8,
+                     device="cuda")
+    hp = [(0.01, 3.75e-4), (0.01, 0.0), (0.1, 0.0)]
+    fn = lambda: nb.numbat_clip_sgd_nesterov(table, len(ents), hp, 0.937, 10.0, None, ws)
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nbytes = sum(n for n, _ in shapes) * (4 + 20)  # squared-norm pass reads g; the update reads w, g, buf, writes w, buf
+    gbs = nbytes / (ms / 1e3) / 1e9
+    return {"tensors": len(shapes), "parameters": sum(n for n, _ in shapes), "ms": round(ms, 4),
+            "bytes": nbytes, "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 3)}
+
+
+def config_set(torch, cfg, batch, steps, warmup, two=True):
+    """Set-mode step of a configuration at a batch (two streams, graph-replayed)."""
+    from paper_2609_10632_amd.schedule import ConvSet
+    from paper_2609_10632_amd.workloads import workload
+
+    wl = workload(cfg, batch)
+    cs = ConvSet(wl.layers, wl.n, wl.index, wl.eps, wl.g_std)
+    for _ in range(warmup):
+        cs.step(overlap=two)
+    g = graph_of(torch, lambda: cs.step(overlap=two))
+    ms = time_replays(torch, g, steps)
+    flops = sum(3 * l.flops for l in cs.layers)
+    out = {"layers": len(cs.layers), "batch": wl.n, "ms_per_step": round(ms, 3),
+           "tflops": round(flops / (ms / 1e3) / 1e12, 2),
+           "pct_mfma_peak": round(100 * flops / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+           "step_gflop": round(flops / 1e9, 2)}
+    del g, cs
+    torch.cuda.empty_cache()
+    return out
+
+
 PASSES = ("conv_fwd", "bn_silu_fwd", "bn_silu_bwd", "conv_bwd_weight", "conv_bwd_data")
+
+
+def write_detail(torch, args, step, layers, wl):
+    """Per layer x pass: median of five serial steps' HIP-event times (launch gaps included),
+    with each pass's algorithmic work against the roofline that binds it: conv passes 2 M N K
+    FLOPs and their operand bytes (fwd x + W + y, dgrad dy + W + dx in bf16, wgrad x + dy in
+    bf16 + dW in fp32); BN passes 4 (fwd) and 10 (bwd) bytes per element.  JSON to
+    args.detail, a markdown table beside it."""
+    reps = []
+    for _ in range(5):
+        ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
+        step(ev, overlap=False)
+        torch.cuda.synchronize()
+        reps.append({l.name: [ev[l.name][a].elapsed_time(ev[l.name][b]) for a, b in ((0, 1), (1, 2), (3, 4), (4, 5),
+                                                                                      (5, 6))] for l in layers})
+    per_layer = {l.name: [sorted(r[l.name][k] for r in reps)[2] for k in range(5)] for l in layers}
+    rows, tot = [], {p: 0.0 for p in PASSES}
+    for l in layers:
+        sp, blk = l.spec, l.blk
+        n = blk.n
+        xb = n * sp.h * sp.h * sp.ci * 2
+        yb = blk.m * sp.co * 2
+        wb = sp.co * sp.k * sp.k * sp.ci * 2
+        work = {"conv_fwd": (l.flops, xb + wb + yb), "bn_silu_fwd": (0, 4 * l.bn_elems),
+                "bn_silu_bwd": (0, 10 * l.bn_elems), "conv_bwd_weight": (l.flops, xb + yb + 2 * wb),
+                "conv_bwd_data": (l.flops, yb + wb + xb)}
+        for k, pname in enumerate(PASSES):
+            ms = per_layer[l.name][k]
+            tot[pname] += ms
+            fl, by = work[pname]
+            tf = fl / (ms / 1e3) / 1e12 if fl else 0.0
+            gbs = by / (ms / 1e3) / 1e9
+            t_mfma, t_hbm = fl / (PEAK_BF16_TFLOPS * 1e12), by / (PEAK_HBM_GBS * 1e9)
+            bound = "mfma" if t_mfma >= t_hbm else "hbm"
+            frac = max(t_mfma, t_hbm) / (ms / 1e3)
+            rows.append((l.name, pname, ms * 1e3, tf, 100 * tf / PEAK_BF16_TFLOPS, gbs, 100 * gbs / PEAK_HBM_GBS, bound,
+                         100 * frac))
+    with open(args.detail, "w") as f:
+        json.dump({"per_layer_ms": per_layer, "passes": PASSES, "flops": {l.name: l.flops for l in layers}}, f,
+                  indent=1)
+    md = os.path.splitext(args.detail)[0] + ".md"
+    with open(md, "w") as f:
+        f.write(f"# Per layer x pass, configuration {wl.index}, batch {wl.n} (serial step, median of 5, HIP events)\n\n")
+        f.write("| layer | pass | us | TFLOP/s | % MFMA peak | GB/s | % HBM peak | binding roofline | % of it |\n")
+        f.write("|---|---|---|---|---|---|---|---|---|\n")
+        for r in rows:
+            f.write(f"| {r[0]} | {r[1]} | {r[2]:.1f} | {r[3]:.1f} | {r[4]:.1f} | {r[5]:.0f} | {r[6]:.1f} | {r[7]} | "
+                    f"{r[8]:.1f} |\n")
+        f.write("\n| pass | ms per step |\n|---|---|\n")
+        for pname in PASSES:
+            f.write(f"| {pname} | {tot[pname]:.3f} |\n")
 
 
 # HBM traffic per launch measured with rocprofv3 counters (FETCH_SIZE, WRITE_SIZE, each
@@ -209,15 +454,20 @@ def main():
     # ---- timed region: K steps, nothing else on the stream
     print(f"# timing {args.steps} steps ({'graph replay' if graph else 'eager launches'})", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        if graph is not None:
-            graph.replay()
-        else:
-            step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    with SclkSampler() as sclk:
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            if graph is not None:
+                graph.replay()
+            else:
+                step()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
+    cold = None
+    if graph is not None and not args.no_extras:
+        print("# cold-cache steps (1 GiB written between replays)", file=sys.stderr, flush=True)
+        cold = cold_cache_ms(torch, graph, max(5, args.steps // 2))
 
     # ---- instrumented region: the same K steps, eager, every kernel bracketed by HIP events on
     # its launch stream (library timing), for the per-kernel roofline
@@ -276,7 +526,10 @@ def main():
                    "streams": 2 if two else 1},
         "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": roofline,
+        "sclk": sclk.summary(),
     }
+    if cold is not None:
+        out["ms_per_step_cold_cache"] = cold
     if per_cls:
         out["kernel_ms_per_step"] = {c: round(v[0], 4) for c, v in per_cls.items()}
         out["conv_kernel_ms"] = round(conv_ms, 3)
@@ -284,17 +537,16 @@ def main():
         out["bn_silu_kernel_ms"] = round(bn_ms, 3)
         out["instrumented_ms_per_step"] = round(ms_instr, 3)
     if args.detail:
-        ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
-        step(ev, overlap=False)
-        torch.cuda.synchronize()
-        per_layer = {}
-        for l in layers:
-            e = ev[l.name]
-            per_layer[l.name] = [e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[3].elapsed_time(e[4]),
-                                 e[4].elapsed_time(e[5]), e[5].elapsed_time(e[6])]
-        with open(args.detail, "w") as f:
-            json.dump({"per_layer_ms": per_layer, "passes": PASSES, "flops": {l.name: l.flops for l in layers}}, f,
-                      indent=1)
+        write_detail(torch, args, step, layers, wl)
+    if not args.no_extras and not args.layers and wl.index == 4:
+        print("# extras: copy bandwidth, chain mode, optimiser step, configuration 5", file=sys.stderr, flush=True)
+        out["hbm_copy_gbs"] = hbm_copy_gbs(torch)
+        out["chain_mode"] = chain_mode(torch, args.steps, args.warmup)
+        out["optimizer_step"] = optimizer_step(torch, args.steps)
+        del graph
+        torch.cuda.empty_cache()
+        out["config5_batch32"] = config_set(torch, 5, 32, max(5, args.steps // 2), 2)
+        out["config5_layers_batch16"] = config_set(torch, 5, 16, max(5, args.steps // 2), 2)
     if not args.no_cpu_baseline:
         print("# cpu baseline (fp64 oracle, bounded sample)", file=sys.stderr, flush=True)
         import oracle

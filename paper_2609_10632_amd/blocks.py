@@ -33,9 +33,10 @@ def host_f64(t: torch.Tensor) -> np.ndarray:
 
 
 def workspace(nbytes: int, device=DEV) -> Optional[torch.Tensor]:
+    """A workspace for the C ABI: zero-filled (its leading counter header must start at zero)."""
     if nbytes == 0:
         return None
-    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
 
 
 @dataclass

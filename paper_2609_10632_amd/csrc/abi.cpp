@@ -109,6 +109,13 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// Every non-empty workspace begins with a 256-byte header of counters for the kernels'
+// grid-wide synchronisation (zero before a workspace's first use; every call leaves it
+// zero); the op's own data follows.
+constexpr size_t kWsHeader = 256;
+size_t with_header(size_t body) { return body ? body + kWsHeader : 0; }
+void* ws_body(void* ws) { return ws ? static_cast<char*>(ws) + kWsHeader : nullptr; }
+
 constexpr int64_t kMaxIndex = (1ll << 31) - 1;
 
 // ---------------------------------------------------------------------------
@@ -495,19 +502,20 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
       ConvDesc d;
       numbat_status st = check_conv(static_cast<const numbat_conv_problem*>(problem), &d);
       if (st != NUMBAT_OK) return st;
-      *bytes = op == NUMBAT_OP_CONV_FWD ? fwd_ws(d) : op == NUMBAT_OP_CONV_BWD_DATA ? bwd_data_ws(d)
-                                                                                    : bwd_weight_ws(d, nullptr, nullptr);
+      *bytes = with_header(op == NUMBAT_OP_CONV_FWD        ? fwd_ws(d)
+                           : op == NUMBAT_OP_CONV_BWD_DATA ? bwd_data_ws(d)
+                                                           : bwd_weight_ws(d, nullptr, nullptr));
       return ok();
     }
     case NUMBAT_OP_CLIP_SGD_NESTEROV:
-      *bytes = round_up((size_t)kOptBlocks * sizeof(double), 256);
+      *bytes = with_header(round_up((size_t)kOptBlocks * sizeof(double), 256));
       return ok();
     case NUMBAT_OP_BN_SILU_FWD:
     case NUMBAT_OP_BN_SILU_BWD: {
       BnDesc d;
       numbat_status st = check_bn(static_cast<const numbat_bn_problem*>(problem), &d);
       if (st != NUMBAT_OK) return st;
-      *bytes = op == NUMBAT_OP_BN_SILU_FWD ? bn_fwd_ws(d) : bn_bwd_ws(d);
+      *bytes = with_header(op == NUMBAT_OP_BN_SILU_FWD ? bn_fwd_ws(d) : bn_bwd_ws(d));
       return ok();
     }
   }
@@ -519,9 +527,9 @@ numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const
   ConvDesc d;
   numbat_status st = check_conv_fwd(p, x, w, y, batch_stats, &d);
   if (st != NUMBAT_OK) return st;
-  st = check_ws(ws, ws_bytes, batch_stats ? fwd_stats_bytes(d) : 0);
+  st = check_ws(ws, ws_bytes, with_header(batch_stats ? fwd_stats_bytes(d) : 0));
   if (st != NUMBAT_OK) return st;
-  return conv_fwd_launch(d, x, w, y, batch_stats, ws, stream);
+  return conv_fwd_launch(d, x, w, y, batch_stats, batch_stats ? ws_body(ws) : nullptr, stream);
 }
 
 numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* x, const void* w, void* y,
@@ -529,7 +537,7 @@ numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* 
   ConvDesc d;
   numbat_status st = check_conv_fwd(p, x, w, y, batch_stats, &d);
   if (st != NUMBAT_OK) return st;
-  const size_t need = batch_stats ? fwd_stats_bytes(d) : 0;
+  const size_t need = with_header(batch_stats ? fwd_stats_bytes(d) : 0);
   if (need > kScratchBytes)
     return fail(NUMBAT_ERR_WORKSPACE,
                 "problem needs %zu bytes of scratch; the static scratch of numbat_conv_fwd_noalloc holds %zu "
@@ -539,7 +547,7 @@ numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* 
     st = scratch_of_current_device(&ws);
     if (st != NUMBAT_OK) return st;
   }
-  return conv_fwd_launch(d, x, w, y, batch_stats, ws, stream);
+  return conv_fwd_launch(d, x, w, y, batch_stats, ws_body(ws), stream);
 }
 
 numbat_status numbat_conv_fwd_bias(const numbat_conv_problem* p, const void* x, const void* w, const float* bias,
@@ -587,8 +595,9 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
   if ((reinterpret_cast<uintptr_t>(w) | reinterpret_cast<uintptr_t>(dx)) & 1u)
     return fail(NUMBAT_ERR_ALIGN, "w and dx must be 2-byte aligned");
   if (d.ci % 8 == 0 && !aligned16(dx)) return fail(NUMBAT_ERR_ALIGN, "dx must be 16-byte aligned");
-  st = check_ws(ws, ws_bytes, bwd_data_ws(d));
+  st = check_ws(ws, ws_bytes, with_header(bwd_data_ws(d)));
   if (st != NUMBAT_OK) return st;
+  ws = ws_body(ws);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
@@ -795,8 +804,9 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   int splits = 1;
   int64_t rps = 0;
   const size_t need = bwd_weight_ws(d, &splits, &rps);
-  st = check_ws(ws, ws_bytes, need);
+  st = check_ws(ws, ws_bytes, with_header(need));
   if (st != NUMBAT_OK) return st;
+  ws = ws_body(ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (stem_wgrad(d)) {
@@ -897,8 +907,9 @@ numbat_status numbat_bn_silu_fwd(const numbat_bn_problem* p, const void* y, cons
   if (!aligned16(y) || !aligned16(out) || (residual && !aligned16(residual)))
     return fail(NUMBAT_ERR_ALIGN, "y, out and residual must be 16-byte aligned");
   const size_t need = batch_stats ? 0 : bn_fwd_ws(d);
-  st = check_ws(ws, ws_bytes, need);
+  st = check_ws(ws, ws_bytes, with_header(need));
   if (st != NUMBAT_OK) return st;
+  ws = ws_body(ws);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const float* mv = batch_stats;
   if (mv == nullptr) {
@@ -946,8 +957,9 @@ numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, cons
     return fail(NUMBAT_ERR_NULL, "g, y, save_mean, save_rstd, gamma, beta, dy, dgamma and dbeta are required");
   if (!aligned16(g) || !aligned16(y) || !aligned16(dy) || (residual_grad && !aligned16(residual_grad)))
     return fail(NUMBAT_ERR_ALIGN, "g, y, dy and residual_grad must be 16-byte aligned");
-  st = check_ws(ws, ws_bytes, bn_bwd_ws(d));
+  st = check_ws(ws, ws_bytes, with_header(bn_bwd_ws(d)));
   if (st != NUMBAT_OK) return st;
+  ws = ws_body(ws);
   const int nb = bn_reduce_blocks(d.a.m, d.a.c);
   float* part = static_cast<float*>(ws);
   float* coef = reinterpret_cast<float*>(static_cast<char*>(ws) + round_up((size_t)nb * d.a.c * sizeof(float2), 256));
@@ -987,8 +999,9 @@ numbat_status numbat_clip_sgd_nesterov(const numbat_param_tensor* tensors, int32
     g.lr[i] = lr;
     g.wd[i] = wd;
   }
-  numbat_status st = check_ws(ws, ws_bytes, round_up((size_t)kOptBlocks * sizeof(double), 256));
+  numbat_status st = check_ws(ws, ws_bytes, with_header(round_up((size_t)kOptBlocks * sizeof(double), 256)));
   if (st != NUMBAT_OK) return st;
+  ws = ws_body(ws);
   const hipError_t e = opt_clip_sgd_launch(reinterpret_cast<const OptTensor*>(tensors), count, g, momentum_factor, max_norm,
                                            total_norm, static_cast<double*>(ws), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "optimiser step launch");

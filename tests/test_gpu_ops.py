@@ -224,8 +224,10 @@ def test_conv_strided_views_large():
     assert_close(blocks.host_f64(dw), oracle.conv_wgrad(xs, f64(dybig[..., 288:]), s), "dw from views")
 
 
-# the last three exceed 512 reduce blocks; (3000000, 48) and (250000, 576) meet the block cap
-BN_CASES = [(1000, 8), (4097, 48), (2048, 96), (777, 576), (300, 64), (400000, 48), (3000000, 48), (250000, 576)]
+# (400000, 48) and the next two exceed 512 reduce blocks; (3000000, 48) and (250000, 576) meet the
+# block cap; then the detector's 20/40/80-wide shapes, the smallest m and the widest c
+BN_CASES = [(1000, 8), (4097, 48), (2048, 96), (777, 576), (300, 64), (400000, 48), (3000000, 48), (250000, 576),
+            (6400, 576), (25600, 192), (102400, 96), (2, 8), (4, 2048)]
 
 
 @pytest.mark.parametrize("m,c", BN_CASES)
@@ -316,6 +318,13 @@ def test_bn_silu_bwd(m, c):
     assert_close(blocks.host_f64(dg), dgr, "dgamma")
     assert_close(blocks.host_f64(db), dbr, "dbeta")
     assert_close(blocks.host_f64(rg), f64(r0) + f64(gb), "residual grad")
+    # the workspace's counter header is left zero
+    assert int(ws[:256].count_nonzero()) == 0
+    # bitwise reproducible (whichever path the layer takes)
+    dy2, dg2, db2 = torch.empty_like(dy), torch.empty_like(dg), torch.empty_like(db)
+    nb.numbat_bn_silu_bwd(p, blocks.dev_bf16(gb), y, sm, sr, ga, be, dy2, dg2, db2, None, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(dy, dy2) and torch.equal(dg, dg2) and torch.equal(db, db2)
 
 
 def test_bitwise_determinism():
