@@ -318,6 +318,9 @@ TRAFFIC_PROFILES = {
     ("conv_fwd_igemm", 4, 16): ("profiles/conv_fwd_igemm_c4_b16_traffic.md",
                                 ("paper_2609_10632_amd/csrc/conv_gemm.hip", "paper_2609_10632_amd/csrc/common.h",
                                  "paper_2609_10632_amd/csrc/kernels.h")),
+    ("conv_dgrad_igemm", 4, 16): ("profiles/conv_dgrad_igemm_c4_b16_traffic.md",
+                                  ("paper_2609_10632_amd/csrc/conv_gemm.hip", "paper_2609_10632_amd/csrc/conv_aux.hip",
+                                   "paper_2609_10632_amd/csrc/common.h", "paper_2609_10632_amd/csrc/kernels.h")),
 }
 
 
@@ -538,9 +541,21 @@ def main():
         out["instrumented_ms_per_step"] = round(ms_instr, 3)
     if args.detail:
         write_detail(torch, args, step, layers, wl)
+    copy_gbs = hbm_copy_gbs(torch)
+    out["hbm_copy_gbs"] = copy_gbs
+    if per_cls:
+        # BN + SiLU kernels: algorithmic bytes (bf16) per element of the step's activations --
+        # forward apply reads y and writes a (4), backward reduce reads g and y (4), backward
+        # apply reads g and y and writes dy (6) -- over their summed kernel time
+        elems = sum(l.bn_elems for l in layers)
+        out["bn_silu_gbs"] = {}
+        for c, b in (("bn_silu_fwd_apply", 4), ("bn_silu_bwd_reduce", 4), ("bn_silu_bwd_apply", 6)):
+            if c in per_cls:
+                gbs = b * elems / (per_cls[c][0] / 1e3) / 1e9
+                out["bn_silu_gbs"][c] = {"gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
+                                         "frac_copy": round(gbs / copy_gbs, 4)}
     if not args.no_extras and not args.layers and wl.index == 4:
-        print("# extras: copy bandwidth, chain mode, optimiser step, configuration 5", file=sys.stderr, flush=True)
-        out["hbm_copy_gbs"] = hbm_copy_gbs(torch)
+        print("# extras: chain mode, optimiser step, configuration 5", file=sys.stderr, flush=True)
         out["chain_mode"] = chain_mode(torch, args.steps, args.warmup)
         out["optimizer_step"] = optimizer_step(torch, args.steps)
         del graph

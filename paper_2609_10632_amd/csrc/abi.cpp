@@ -18,7 +18,8 @@
 using namespace numbat;
 
 // ---------------------------------------------------------------------------
-// Optional launch timing: HIP events bracket each kernel on its launch stream.
+// Optional launch timing: each kernel launch carries a start / stop event pair that takes
+// the dispatch's own begin and end timestamps.
 namespace {
 
 struct TimingRec {
@@ -31,7 +32,7 @@ bool g_timing = false;
 std::vector<TimingRec> g_recs;
 std::vector<hipEvent_t> g_pool;
 size_t g_pool_used = 0;
-hipEvent_t g_open[KC_COUNT];
+thread_local int g_cls = -1;  // the class of the launches in progress on this thread
 
 hipEvent_t pool_event() {
   if (g_pool_used == g_pool.size()) {
@@ -54,30 +55,19 @@ const char* const kClassNames[KC_COUNT] = {
 
 namespace numbat {
 
-void trace_begin(int cls, hipStream_t s) {
-  if (!g_timing) return;
-  std::lock_guard<std::mutex> lk(g_tmu);
-  hipEvent_t e = pool_event();
-  // a failed record drops this launch from the timing and clears its error, so that the
-  // launcher's own status check reports the kernel launch only
-  if (e && hipEventRecord(e, s) != hipSuccess) {
-    (void)hipGetLastError();
-    e = nullptr;
-  }
-  g_open[cls] = e;
-}
+void trace_begin(int cls) { g_cls = cls; }
 
-void trace_end(int cls, hipStream_t s) {
-  if (!g_timing) return;
+void trace_end(int) { g_cls = -1; }
+
+bool timing_events(hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_timing || g_cls < 0) return false;
   std::lock_guard<std::mutex> lk(g_tmu);
-  hipEvent_t e = pool_event();
-  if (e && g_open[cls]) {
-    if (hipEventRecord(e, s) == hipSuccess)
-      g_recs.push_back(TimingRec{cls, g_open[cls], e});
-    else
-      (void)hipGetLastError();
-  }
-  g_open[cls] = nullptr;
+  hipEvent_t e0 = pool_event(), e1 = pool_event();
+  if (e0 == nullptr || e1 == nullptr) return false;  // timing is best-effort: launch untimed
+  g_recs.push_back(TimingRec{g_cls, e0, e1});
+  *start = e0;
+  *stop = e1;
+  return true;
 }
 
 }  // namespace numbat
@@ -442,7 +432,6 @@ numbat_status numbat_timing_enable(int enable) {
   g_timing = enable != 0;
   g_recs.clear();
   g_pool_used = 0;
-  for (int i = 0; i < KC_COUNT; ++i) g_open[i] = nullptr;
   return ok();
 }
 

@@ -393,10 +393,10 @@ hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int n
   const int64_t rpb = rows_per_block(a.m, nblocks);
   const int nb = (int)((a.m + rpb - 1) / rpb);
   float2* part = reinterpret_cast<float2*>(part3);
-  trace_begin(KC_BN_STATS, s);
-  hipLaunchKernelGGL(bn_stats_kernel, dim3(nb), dim3(kThreads), reduce_smem(a.c), s, y, a.y_pix, a.m, a.c, rpb,
+  trace_begin(KC_BN_STATS);
+  NUMBAT_LAUNCH(bn_stats_kernel, dim3(nb), dim3(kThreads), reduce_smem(a.c), s, y, a.y_pix, a.m, a.c, rpb,
                      part);
-  trace_end(KC_BN_STATS, s);
+  trace_end(KC_BN_STATS);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return stats_merge_launch(part, nb, (int)rpb, a.m, a.c, mean_var, s);
@@ -427,10 +427,10 @@ hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, co
   int64_t rpb = 0;
   const int nb = apply_blocks(a.m, a.c, &rpb);
   const int stat = save_mean != nullptr ? 1 : 0;
-  trace_begin(KC_BN_FWD, s);
-  hipLaunchKernelGGL(bn_fwd_kernel, dim3(nb + stat), dim3(kThreads), 0, s, a, y, mean, var, gamma, beta, res, out,
+  trace_begin(KC_BN_FWD);
+  NUMBAT_LAUNCH(bn_fwd_kernel, dim3(nb + stat), dim3(kThreads), 0, s, a, y, mean, var, gamma, beta, res, out,
                      save_mean, save_rstd, run_mean, run_var, rpb, stat);
-  trace_end(KC_BN_FWD, s);
+  trace_end(KC_BN_FWD);
   return hipGetLastError();
 }
 
@@ -440,13 +440,13 @@ hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, cons
   const int64_t rpb = rows_per_block(a.m, nblocks);
   const int nb = (int)((a.m + rpb - 1) / rpb);
   float2* part = reinterpret_cast<float2*>(part2);
-  trace_begin(KC_BN_BWD_REDUCE, s);
-  hipLaunchKernelGGL(bn_bwd_reduce_kernel, dim3(nb), dim3(kThreads), reduce_smem(a.c), s, a, g, y, save_mean,
+  trace_begin(KC_BN_BWD_REDUCE);
+  NUMBAT_LAUNCH(bn_bwd_reduce_kernel, dim3(nb), dim3(kThreads), reduce_smem(a.c), s, a, g, y, save_mean,
                      save_rstd, gamma, beta, rpb, part);
-  trace_end(KC_BN_BWD_REDUCE, s);
+  trace_end(KC_BN_BWD_REDUCE);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  trace_begin(KC_BN_BWD_FINALIZE, s);
+  trace_begin(KC_BN_BWD_FINALIZE);
   // about eight partial rows per lane
   const dim3 fgrid((a.c + kFinCh - 1) / kFinCh);
   int fg = nb <= 256 ? 32 : nb <= 512 ? 64 : 128;
@@ -454,23 +454,23 @@ hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, cons
   if (const char* e = getenv("NUMBAT_BN_FING")) fg = atoi(e);
 #endif
   if (fg == 128)
-    hipLaunchKernelGGL(bn_bwd_finalize_kernel<128>, fgrid, dim3(kFinCh * 128), 0, s, part, nb, a.c, a.m, save_rstd,
+    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<128>, fgrid, dim3(kFinCh * 128), 0, s, part, nb, a.c, a.m, save_rstd,
                        gamma, dgamma, dbeta, coef);
   else if (fg == 64)
-    hipLaunchKernelGGL(bn_bwd_finalize_kernel<64>, fgrid, dim3(kFinCh * 64), 0, s, part, nb, a.c, a.m, save_rstd,
+    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<64>, fgrid, dim3(kFinCh * 64), 0, s, part, nb, a.c, a.m, save_rstd,
                        gamma, dgamma, dbeta, coef);
   else
-    hipLaunchKernelGGL(bn_bwd_finalize_kernel<32>, fgrid, dim3(kFinCh * 32), 0, s, part, nb, a.c, a.m, save_rstd,
+    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<32>, fgrid, dim3(kFinCh * 32), 0, s, part, nb, a.c, a.m, save_rstd,
                        gamma, dgamma, dbeta, coef);
-  trace_end(KC_BN_BWD_FINALIZE, s);
+  trace_end(KC_BN_BWD_FINALIZE);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   int64_t arpb = 0;
   const int anb = apply_blocks(a.m, a.c, &arpb);
-  trace_begin(KC_BN_BWD_APPLY, s);
-  hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(anb), dim3(kThreads), 0, s, a, g, y, save_mean, save_rstd, gamma, beta,
+  trace_begin(KC_BN_BWD_APPLY);
+  NUMBAT_LAUNCH(bn_bwd_apply_kernel, dim3(anb), dim3(kThreads), 0, s, a, g, y, save_mean, save_rstd, gamma, beta,
                      coef, dy, res_grad, arpb);
-  trace_end(KC_BN_BWD_APPLY, s);
+  trace_end(KC_BN_BWD_APPLY);
   return hipGetLastError();
 }
 

@@ -103,10 +103,10 @@ __global__ __launch_bounds__(kMergeCh * kMergeGroups) void stats_merge_kernel(co
 
 hipError_t stats_merge_launch(const float2* part, int mtiles, int tile_rows, int64_t m, int c, float* mean_var,
                               hipStream_t s) {
-  trace_begin(KC_STATS_MERGE, s);
-  hipLaunchKernelGGL(stats_merge_kernel, dim3((c + kMergeCh - 1) / kMergeCh), dim3(kMergeCh * kMergeGroups), 0, s,
+  trace_begin(KC_STATS_MERGE);
+  NUMBAT_LAUNCH(stats_merge_kernel, dim3((c + kMergeCh - 1) / kMergeCh), dim3(kMergeCh * kMergeGroups), 0, s,
                      part, mtiles, tile_rows, m, c, mean_var);
-  trace_end(KC_STATS_MERGE, s);
+  trace_end(KC_STATS_MERGE);
   return hipGetLastError();
 }
 
@@ -175,10 +175,10 @@ hipError_t dgrad_weights_launch(const bf16_t* w, bf16_t* wt, int co, int kh, int
   int blocks = (nitems + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (blocks < 1) blocks = 1;
-  trace_begin(KC_DGRAD_WEIGHTS, s);
-  hipLaunchKernelGGL(dgrad_weights_kernel, dim3(blocks), dim3(256), 0, s, w, reinterpret_cast<uint4*>(wt), co, kh, kw,
+  trace_begin(KC_DGRAD_WEIGHTS);
+  NUMBAT_LAUNCH(dgrad_weights_kernel, dim3(blocks), dim3(256), 0, s, w, reinterpret_cast<uint4*>(wt), co, kh, kw,
                      ci, cpad, nitems, tab);
-  trace_end(KC_DGRAD_WEIGHTS, s);
+  trace_end(KC_DGRAD_WEIGHTS);
   return hipGetLastError();
 }
 
@@ -218,16 +218,16 @@ int blocks_for(int64_t n) {
 }  // namespace
 
 hipError_t pack8_launch(const bf16_t* src, int64_t src_pix, int ci, int64_t n, bf16_t* dst, hipStream_t s) {
-  trace_begin(KC_PACK, s);
-  hipLaunchKernelGGL(pack8_kernel, dim3(blocks_for(n)), dim3(256), 0, s, src, src_pix, ci, n, reinterpret_cast<uint4*>(dst));
-  trace_end(KC_PACK, s);
+  trace_begin(KC_PACK);
+  NUMBAT_LAUNCH(pack8_kernel, dim3(blocks_for(n)), dim3(256), 0, s, src, src_pix, ci, n, reinterpret_cast<uint4*>(dst));
+  trace_end(KC_PACK);
   return hipGetLastError();
 }
 
 hipError_t unpack_dw_launch(const float* dw8, float* dw, int64_t rows, int ci, int accumulate, hipStream_t s) {
-  trace_begin(KC_PACK, s);
-  hipLaunchKernelGGL(unpack_dw_kernel, dim3(blocks_for(rows * ci)), dim3(256), 0, s, dw8, dw, rows, ci, accumulate);
-  trace_end(KC_PACK, s);
+  trace_begin(KC_PACK);
+  NUMBAT_LAUNCH(unpack_dw_kernel, dim3(blocks_for(rows * ci)), dim3(256), 0, s, dw8, dw, rows, ci, accumulate);
+  trace_end(KC_PACK);
   return hipGetLastError();
 }
 
@@ -640,23 +640,23 @@ hipError_t dgrad_narrow_launch(const NarrowDgradArgs& a, int ci, float* wf, hipS
     const int64_t npatch = (int64_t)ntw * nth * a.n;
     if (npatch > 0 && npatch < 0x7fffffff) {
       dim3 grid((unsigned)(npatch < 1280 ? npatch : 1280));  // five blocks per CU
-      trace_begin(KC_CONV_DGRAD, s);
+      trace_begin(KC_CONV_DGRAD);
       const int np = (int)npatch;
       if (ci == 3 && a.kh == 3 && a.kw == 3 && a.sh == 2 && a.sw == 2 && a.co == 48 && th == 8 && lgtw == 6) {
-        hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<3, 3, 2, 8, 6, 48>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np);
+        NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<3, 3, 2, 8, 6, 48>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np);
       } else {
         switch (ci) {
-          case 1: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<1, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          case 2: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<2, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          case 3: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<3, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          case 4: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<4, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          case 5: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<5, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          case 6: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<6, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          case 7: hipLaunchKernelGGL((dgrad_narrow_mfma_kernel<7, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
-          default: trace_end(KC_CONV_DGRAD, s); return hipErrorInvalidValue;
+          case 1: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<1, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 2: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<2, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 3: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<3, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 4: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<4, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 5: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<5, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 6: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<6, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          case 7: NUMBAT_LAUNCH((dgrad_narrow_mfma_kernel<7, 0, 0, 0, 0, 0>), grid, dim3(256), 0, s, a, th, lgtw, ntw, nth, np); break;
+          default: trace_end(KC_CONV_DGRAD); return hipErrorInvalidValue;
         }
       }
-      trace_end(KC_CONV_DGRAD, s);
+      trace_end(KC_CONV_DGRAD);
       return hipGetLastError();
     }
   }
@@ -664,25 +664,25 @@ hipError_t dgrad_narrow_launch(const NarrowDgradArgs& a, int ci, float* wf, hipS
   const int64_t blocks = ((int64_t)a.n * ghm * ((gwm + 63) / 64) + 3) / 4;  // 4 waves of 64 pixels
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   const int64_t wn = (int64_t)a.kh * a.kw * a.co * ci;
-  trace_begin(KC_DGRAD_WEIGHTS, s);
-  hipLaunchKernelGGL(narrow_weights_kernel, dim3((unsigned)((wn + 255) / 256)), dim3(256), 0, s, a.wt, wf, a.co, a.kh,
+  trace_begin(KC_DGRAD_WEIGHTS);
+  NUMBAT_LAUNCH(narrow_weights_kernel, dim3((unsigned)((wn + 255) / 256)), dim3(256), 0, s, a.wt, wf, a.co, a.kh,
                      a.kw, ci);
-  trace_end(KC_DGRAD_WEIGHTS, s);
+  trace_end(KC_DGRAD_WEIGHTS);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 grid((unsigned)blocks, (unsigned)(a.sh * a.sw), 1);
-  trace_begin(KC_CONV_DGRAD, s);
+  trace_begin(KC_CONV_DGRAD);
   switch (ci) {
-    case 1: hipLaunchKernelGGL(dgrad_narrow_kernel<1>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    case 2: hipLaunchKernelGGL(dgrad_narrow_kernel<2>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    case 3: hipLaunchKernelGGL(dgrad_narrow_kernel<3>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    case 4: hipLaunchKernelGGL(dgrad_narrow_kernel<4>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    case 5: hipLaunchKernelGGL(dgrad_narrow_kernel<5>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    case 6: hipLaunchKernelGGL(dgrad_narrow_kernel<6>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    case 7: hipLaunchKernelGGL(dgrad_narrow_kernel<7>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
-    default: trace_end(KC_CONV_DGRAD, s); return hipErrorInvalidValue;
+    case 1: NUMBAT_LAUNCH(dgrad_narrow_kernel<1>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    case 2: NUMBAT_LAUNCH(dgrad_narrow_kernel<2>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    case 3: NUMBAT_LAUNCH(dgrad_narrow_kernel<3>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    case 4: NUMBAT_LAUNCH(dgrad_narrow_kernel<4>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    case 5: NUMBAT_LAUNCH(dgrad_narrow_kernel<5>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    case 6: NUMBAT_LAUNCH(dgrad_narrow_kernel<6>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    case 7: NUMBAT_LAUNCH(dgrad_narrow_kernel<7>, grid, dim3(256), 0, s, a, a.dy, wf, a.dx); break;
+    default: trace_end(KC_CONV_DGRAD); return hipErrorInvalidValue;
   }
-  trace_end(KC_CONV_DGRAD, s);
+  trace_end(KC_CONV_DGRAD);
   return hipGetLastError();
 }
 

@@ -1415,7 +1415,7 @@ template <int TN>
 hipError_t launch_narrow(const ConvGemmArgs& a, hipStream_t s) {
   using G = GemmShape<2, TN>;
   dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
-  hipLaunchKernelGGL((convnarrow_kernel<2, TN>), grid, dim3(256), 0, s, a);
+  NUMBAT_LAUNCH((convnarrow_kernel<2, TN>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1439,9 +1439,9 @@ void launch_dma(const ConvGemmArgs& a, int mmax, hipStream_t s) {
   using Sh = GemmShape<TM, TN, NW>;
   dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN), (unsigned)a.nphase);
   if (a.bt)
-    hipLaunchKernelGGL((convdma_kernel<TM, TN, S, BK, NW, true>), grid, dim3(NW * 64), 0, s, a);
+    NUMBAT_LAUNCH((convdma_kernel<TM, TN, S, BK, NW, true>), grid, dim3(NW * 64), 0, s, a);
   else
-    hipLaunchKernelGGL((convdma_kernel<TM, TN, S, BK, NW, false>), grid, dim3(NW * 64), 0, s, a);
+    NUMBAT_LAUNCH((convdma_kernel<TM, TN, S, BK, NW, false>), grid, dim3(NW * 64), 0, s, a);
 }
 
 template <int I>
@@ -1471,7 +1471,7 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
   else {
     dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN),
               (unsigned)a.nphase);
-    hipLaunchKernelGGL((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
+    NUMBAT_LAUNCH((convgemm_kernel<c.tm, c.tn, c.d>), grid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
@@ -1512,9 +1512,9 @@ hipError_t launch_h(const ConvGemmArgs& a, hipStream_t s) {
     using G = GemmShape<c.tm, c.tn, 4>;
     dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
     if (a.bt)
-      hipLaunchKernelGGL((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true>), grid, dim3(256), 0, s, a);
     else
-      hipLaunchKernelGGL((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -1695,15 +1695,15 @@ hipError_t convnarrow_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_
   if (a.nphase != 1 || a.ph[0].ktot > NarrowShape<2, 2>::KMAX || a.ph[0].taps > kMaxTaps)
     return hipErrorInvalidValue;
   if (stem_shape(a, t)) {
-    trace_begin(KC_CONV_FWD, s);
+    trace_begin(KC_CONV_FWD);
     dim3 grid((unsigned)(a.ph[0].gw / 64), (unsigned)(a.ph[0].gh / 4), (unsigned)a.nimg);
-    hipLaunchKernelGGL(convstem_kernel, grid, dim3(256), 0, s, a);
-    trace_end(KC_CONV_FWD, s);
+    NUMBAT_LAUNCH(convstem_kernel, grid, dim3(256), 0, s, a);
+    trace_end(KC_CONV_FWD);
     return hipGetLastError();
   }
-  trace_begin(KC_CONV_FWD, s);
+  trace_begin(KC_CONV_FWD);
   const hipError_t e = t.bn == 32 ? launch_narrow<1>(a, s) : launch_narrow<2>(a, s);
-  trace_end(KC_CONV_FWD, s);
+  trace_end(KC_CONV_FWD);
   return e;
 }
 
@@ -1719,7 +1719,7 @@ hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int 
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_REMAP_CONV")) a.remap = atoi(e);
 #endif
-  trace_begin(cls, s);
+  trace_begin(cls);
   hipError_t e;
   switch (t.id) {
     case 0: e = launch_g<0>(a, variant, s); break;
@@ -1731,7 +1731,7 @@ hipError_t convgemm_launch(ConvGemmArgs a, const TileCfg& t, hipStream_t s, int 
     case 6: e = launch_g<6>(a, variant, s); break;
     default: e = launch_g<7>(a, variant, s); break;
   }
-  trace_end(cls, s);
+  trace_end(cls);
   return e;
 }
 
@@ -1784,9 +1784,9 @@ TileCfg convhalo_pick(int64_t m, int nout, int w, bool bt) {
 hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
   if (t.variant != kVariantHalo || t.id < 0 || t.id >= kNumH || !convhalo_shape(a)) return hipErrorInvalidValue;
   if (kH[t.id].hi * 64 < t.bm + 2 * a.ws + 2) return hipErrorInvalidValue;
-  trace_begin(cls, s);
+  trace_begin(cls);
   const hipError_t e = launch_h_id<0>(t.id, a, s);
-  trace_end(cls, s);
+  trace_end(cls);
   return e;
 }
 

@@ -418,7 +418,7 @@ hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
   constexpr int BMO = 64 * TMO;
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
-  hipLaunchKernelGGL((wgrad_dma_kernel<TMO, S, BR>), grid, dim3(256), 0, s, a, dwo, dhw);
+  NUMBAT_LAUNCH((wgrad_dma_kernel<TMO, S, BR>), grid, dim3(256), 0, s, a, dwo, dhw);
   return hipGetLastError();
 }
 template <int TMO>
@@ -437,12 +437,12 @@ hipError_t wgrad_launch(const WgradArgs& args, hipStream_t s) {
   if (const char* e = getenv("NUMBAT_REMAP_WG")) a.remap = atoi(e);
 #endif
   const WgCfg c = wgrad_cfg(a.co);
-  trace_begin(KC_WGRAD, s);
+  trace_begin(KC_WGRAD);
   hipError_t e;
   if (c.tmo == 1) e = launch_w_tmo<1>(a, c, s);
   else if (c.tmo == 3) e = launch_w_tmo<3>(a, c, s);
   else e = launch_w_tmo<2>(a, c, s);
-  trace_end(KC_WGRAD, s);
+  trace_end(KC_WGRAD);
   return e;
 }
 
@@ -458,17 +458,17 @@ hipError_t splitk_reduce_launch(const float* part, int splits, int64_t count, fl
   const float4* p4 = reinterpret_cast<const float4*>(part);
   const int opb = 256 / G;
   const unsigned blocks = (unsigned)((count4 + opb - 1) / opb);
-  trace_begin(KC_SPLITK_REDUCE, s);
+  trace_begin(KC_SPLITK_REDUCE);
   switch (G) {
-    case 1: hipLaunchKernelGGL(splitk_reduce_kernel<1>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
-    case 2: hipLaunchKernelGGL(splitk_reduce_kernel<2>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
-    case 4: hipLaunchKernelGGL(splitk_reduce_kernel<4>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
-    case 8: hipLaunchKernelGGL(splitk_reduce_kernel<8>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
-    case 16: hipLaunchKernelGGL(splitk_reduce_kernel<16>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
-    case 32: hipLaunchKernelGGL(splitk_reduce_kernel<32>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
-    default: hipLaunchKernelGGL(splitk_reduce_kernel<64>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 1: NUMBAT_LAUNCH(splitk_reduce_kernel<1>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 2: NUMBAT_LAUNCH(splitk_reduce_kernel<2>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 4: NUMBAT_LAUNCH(splitk_reduce_kernel<4>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 8: NUMBAT_LAUNCH(splitk_reduce_kernel<8>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 16: NUMBAT_LAUNCH(splitk_reduce_kernel<16>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    case 32: NUMBAT_LAUNCH(splitk_reduce_kernel<32>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
+    default: NUMBAT_LAUNCH(splitk_reduce_kernel<64>, dim3(blocks), dim3(256), 0, s, p4, splits, count4, dw, accumulate); break;
   }
-  trace_end(KC_SPLITK_REDUCE, s);
+  trace_end(KC_SPLITK_REDUCE);
   return hipGetLastError();
 }
 
@@ -644,9 +644,9 @@ hipError_t wgrad_stem_launch(const WgradArgs& a, float* part, hipStream_t s) {
   const int64_t npatch = (int64_t)a.n * (a.ho / 4) * (a.wo / 64);
   if (!wgrad_stem_shape(a) || npatch <= 0 || npatch >= 0x7fffffff) return hipErrorInvalidValue;
   const int nb = wgrad_stem_blocks(a);
-  trace_begin(KC_WGRAD, s);
-  hipLaunchKernelGGL(wgrad_stem_kernel, dim3((unsigned)nb), dim3(256), 0, s, a, (int)npatch, part);
-  trace_end(KC_WGRAD, s);
+  trace_begin(KC_WGRAD);
+  NUMBAT_LAUNCH(wgrad_stem_kernel, dim3((unsigned)nb), dim3(256), 0, s, a, (int)npatch, part);
+  trace_end(KC_WGRAD);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return splitk_reduce_launch(part, nb, (int64_t)a.co * 27, a.out, a.accumulate, s);

@@ -1,6 +1,7 @@
 // Host-side launch interface between the C ABI layer and the gfx950 kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -10,9 +11,12 @@ namespace numbat {
 
 constexpr int kMaxTaps = 25;
 
-// Kernel classes for the optional launch timing (numbat_timing_*).  Each launcher
-// brackets its kernel with trace_begin / trace_end, which record HIP events on the
-// launch stream when timing is enabled and do nothing otherwise.
+// Kernel classes for the optional launch timing (numbat_timing_*).  A launcher names the
+// class of its kernels with trace_begin / trace_end around their launches.  While timing
+// is enabled, every launch made through NUMBAT_LAUNCH carries a start and a stop event
+// that take the dispatch's own begin and end timestamps (hipExtLaunchKernelGGL), so a
+// class's time is its kernels' execution time alone, without launch gaps or the time an
+// event marker of its own would add; with timing off it is a plain hipLaunchKernelGGL.
 enum KernelClass {
   KC_CONV_FWD = 0,      // implicit GEMM, forward
   KC_STATS_MERGE,       // batch statistics merge
@@ -31,8 +35,20 @@ enum KernelClass {
   KC_POOL,              // SPPF max pool and neck upsampling, forward and backward
   KC_COUNT
 };
-void trace_begin(int cls, hipStream_t s);
-void trace_end(int cls, hipStream_t s);
+void trace_begin(int cls);
+void trace_end(int cls);
+// a start / stop event pair for the next launch, recorded under the current class; false
+// when timing is off (or no class is open, or no event could be created)
+bool timing_events(hipEvent_t* start, hipEvent_t* stop);
+
+#define NUMBAT_LAUNCH(kernel, grid, block, smem, stream, ...)                                        \
+  do {                                                                                               \
+    hipEvent_t numbat_ev0_, numbat_ev1_;                                                             \
+    if (::numbat::timing_events(&numbat_ev0_, &numbat_ev1_))                                         \
+      hipExtLaunchKernelGGL(kernel, grid, block, smem, stream, numbat_ev0_, numbat_ev1_, 0, __VA_ARGS__); \
+    else                                                                                             \
+      hipLaunchKernelGGL(kernel, grid, block, smem, stream, __VA_ARGS__);                           \
+  } while (0)
 
 // conv GEMM kernel variants: generic (source channels a multiple of 8; A fragments loaded
 // into registers), and the direct-to-LDS kernel for 16-multiple channel counts of at least

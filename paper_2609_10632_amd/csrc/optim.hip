@@ -122,15 +122,15 @@ __global__ __launch_bounds__(kOptThreads) void opt_update_kernel(const OptTensor
 hipError_t opt_clip_sgd_launch(const OptTensor* tab, int count, const OptGroups& grp, float momentum, float max_norm,
                                float* total_norm, double* part, hipStream_t s) {
   const size_t smem = (size_t)count * sizeof(OptTensor);
-  trace_begin(KC_OPT_SUMSQ, s);
-  hipLaunchKernelGGL(opt_sumsq_kernel, dim3(kOptBlocks), dim3(kOptThreads), smem, s, tab, count, part);
-  trace_end(KC_OPT_SUMSQ, s);
+  trace_begin(KC_OPT_SUMSQ);
+  NUMBAT_LAUNCH(opt_sumsq_kernel, dim3(kOptBlocks), dim3(kOptThreads), smem, s, tab, count, part);
+  trace_end(KC_OPT_SUMSQ);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  trace_begin(KC_OPT_UPDATE, s);
-  hipLaunchKernelGGL(opt_update_kernel, dim3(kOptBlocks), dim3(kOptThreads), smem, s, tab, count, grp, momentum,
+  trace_begin(KC_OPT_UPDATE);
+  NUMBAT_LAUNCH(opt_update_kernel, dim3(kOptBlocks), dim3(kOptThreads), smem, s, tab, count, grp, momentum,
                      max_norm, (const double*)part, total_norm);
-  trace_end(KC_OPT_UPDATE, s);
+  trace_end(KC_OPT_UPDATE);
   return hipGetLastError();
 }
 

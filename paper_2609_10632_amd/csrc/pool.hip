@@ -167,31 +167,31 @@ int pool_blocks(const PoolArgs& a) {
 }  // namespace
 
 hipError_t maxpool5_fwd_launch(const PoolArgs& a, const bf16_t* x, bf16_t* y, uint8_t* idx, hipStream_t s) {
-  trace_begin(KC_POOL, s);
-  hipLaunchKernelGGL(maxpool5_fwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, x, y, idx);
-  trace_end(KC_POOL, s);
+  trace_begin(KC_POOL);
+  NUMBAT_LAUNCH(maxpool5_fwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, x, y, idx);
+  trace_end(KC_POOL);
   return hipGetLastError();
 }
 
 hipError_t maxpool5_bwd_launch(const PoolArgs& a, const bf16_t* dy, const uint8_t* idx, bf16_t* dx, int accumulate,
                                hipStream_t s) {
-  trace_begin(KC_POOL, s);
-  hipLaunchKernelGGL(maxpool5_bwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, dy, idx, dx, accumulate);
-  trace_end(KC_POOL, s);
+  trace_begin(KC_POOL);
+  NUMBAT_LAUNCH(maxpool5_bwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, dy, idx, dx, accumulate);
+  trace_end(KC_POOL);
   return hipGetLastError();
 }
 
 hipError_t upsample2x_fwd_launch(const PoolArgs& a, const bf16_t* x, bf16_t* y, hipStream_t s) {
-  trace_begin(KC_POOL, s);
-  hipLaunchKernelGGL(upsample2x_fwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, x, y);
-  trace_end(KC_POOL, s);
+  trace_begin(KC_POOL);
+  NUMBAT_LAUNCH(upsample2x_fwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, x, y);
+  trace_end(KC_POOL);
   return hipGetLastError();
 }
 
 hipError_t upsample2x_bwd_launch(const PoolArgs& a, const bf16_t* dy, bf16_t* dx, int accumulate, hipStream_t s) {
-  trace_begin(KC_POOL, s);
-  hipLaunchKernelGGL(upsample2x_bwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, dy, dx, accumulate);
-  trace_end(KC_POOL, s);
+  trace_begin(KC_POOL);
+  NUMBAT_LAUNCH(upsample2x_bwd_kernel, dim3(pool_blocks(a)), dim3(kPoolThreads), 0, s, a, dy, dx, accumulate);
+  trace_end(KC_POOL);
   return hipGetLastError();
 }
 
