@@ -79,6 +79,11 @@ CONV_CASES = [
     (6, 120, 95, 48, 96, 3, 1),
     (9, 90, 90, 32, 64, 3, 1),
     (10, 64, 60, 32, 64, 3, 1),
+    # long reductions on small grids with ragged row and column tiles: 36 and 39 steps of
+    # 64 (the reduction ends mid-step), stride 1 and 2
+    (2, 20, 20, 256, 96, 3, 1),
+    (1, 21, 19, 272, 80, 3, 1),
+    (2, 41, 41, 256, 64, 3, 2),
 ]
 
 
@@ -327,15 +332,16 @@ def test_bn_silu_bwd(m, c):
     assert torch.equal(dy, dy2) and torch.equal(dg, dg2) and torch.equal(db, db2)
 
 
-def test_bitwise_determinism():
-    c = (4, 20, 20, 96, 96, 3, 1)
+@pytest.mark.parametrize("c", [(4, 20, 20, 96, 96, 3, 1), (4, 20, 20, 288, 288, 3, 1)])
+def test_bitwise_determinism(c):
+    """Two runs of a block's forward and backward are bit for bit equal."""
     s = shape_of(c)
     inp = Inputs(107)
-    xb, wb, gb = inp.normal(s.x_shape, synth.T_X), inp.weight(96, 3, 96), inp.normal(s.y_shape, synth.T_G)
+    xb, wb, gb = inp.normal(s.x_shape, synth.T_X), inp.weight(s.co, 3, s.ci), inp.normal(s.y_shape, synth.T_G)
     blk = blocks.ConvBlock(s.n, s.h, s.w, s.ci, s.co, 3, 1)
     x, w, g = blocks.dev_bf16(xb), blocks.dev_bf16(wb), blocks.dev_bf16(gb)
-    ga = torch.ones(96, device="cuda")
-    be = torch.zeros(96, device="cuda")
+    ga = torch.ones(s.co, device="cuda")
+    be = torch.zeros(s.co, device="cuda")
     runs = []
     for _ in range(2):
         f = blk.forward(x, w, ga, be)
