@@ -1,7 +1,9 @@
 """The detector's backbone and neck as one network on the C ABI (chain mode): the 65
 Conv+BN+SiLU layers of the workload table connected as the case study's network (Sec. 6.1:
 CSP backbone of C2f blocks and an SPPF block, PAN-FPN neck with nearest upsampling and
-concatenations), forward and backward, on one stream.
+concatenations), forward and backward.  The backward runs each layer's weight gradient on
+a second stream (nothing later in the backward reads it), enqueued in small groups behind
+one wait for the last data gradient of the group, as the conv-set schedule does.
 
 Every concatenation is a buffer whose channel slices the producers write and the consumers
 read through pixel strides (no copies): a C2f block's halves live in its own concat buffer,
@@ -51,12 +53,33 @@ class Conv:
         nb.numbat_conv_fwd(self.blk.prob, self.x, w, self.y, self.stats, ws)
         nb.numbat_bn_silu_fwd(self.bnp, self.y, self.stats, g, b, self.res, self.out, self.smean, self.srstd, ws=ws)
 
-    def bwd(self, w, g, b, ws, want_dx=True):
+    def bwd(self, w, g, b, ws, want_dx=True, side=None, ws_side=None, pending=None):
+        """BN/SiLU backward, then the data and weight gradients.  With a side stream, returns
+        a callable that enqueues the weight gradient there (on ws_side) after a wait for this
+        layer's data gradient (`.done`); `pending`, if given, runs between the BN backward and
+        the data gradient to enqueue earlier layers' weight gradients."""
         nb.numbat_bn_silu_bwd(self.bnp, self.dout, self.y, self.smean, self.srstd, g, b, self.dy, self.dgamma,
                               self.dbeta, self.dres, ws=ws)
-        nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, ws)
+        if side is None:
+            nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, ws)
+            if want_dx:
+                nb.numbat_conv_bwd_data(self.blk.prob, self.dy, w, self.dx, self.acc_dx, ws)
+            return None
+        if pending is not None:
+            pending()
         if want_dx:
             nb.numbat_conv_bwd_data(self.blk.prob, self.dy, w, self.dx, self.acc_dx, ws)
+        done = torch.cuda.Event()
+        done.record()
+
+        def wgrad(wait=True):
+            if wait:
+                side.wait_event(done)
+            with torch.cuda.stream(side):
+                nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, ws_side)
+
+        wgrad.done = done
+        return wgrad
 
 
 class Detector:
@@ -146,6 +169,8 @@ class Detector:
         c2f("n21", S[5], n20, dn20, self.p5, self.g5)
         self.L = L
         self.ws = torch.zeros(max(c.blk.ws_bytes() for c in self.layers), dtype=torch.uint8, device=dev)
+        self.ws_side = torch.zeros_like(self.ws)
+        self.side = torch.cuda.Stream()  # default priority
         self.flops = 3 * sum(self.specs[c.name].gemm_flops(n) * (hin / 640.0) ** 2 for c in self.layers)
 
     # ---- parameters and inputs
@@ -191,21 +216,47 @@ class Detector:
                 _, pp, src, dst, _, _ = op
                 nb.numbat_upsample2x_fwd(pp, src, dst)
 
-    def backward(self):
+    def backward(self, overlap=True, group=2, tail=8):
+        """The backward in reverse program order.  overlap=False keeps everything on the
+        current stream; otherwise the weight gradients run on the side stream in groups of
+        `group` layers behind one wait (the last `tail` convs of the backward one by one)."""
         # the outputs' upstream gradients (P3 and P4 also receive the stride-2 convs' dx)
         for t, g in zip((self.g3, self.g4, self.g5), self.g_init):
             t.copy_(g)
+        sd = self.side if overlap else None
+        if sd is not None:
+            sd.wait_stream(torch.cuda.current_stream())
+        queued = []
+
+        def flush():
+            if queued:
+                sd.wait_event(queued[-1].done)
+            for f in queued:
+                f(wait=False)
+            queued.clear()
+
+        nconv = len(self.layers)
+        i = 0
         for op in reversed(self.ops):
             if op[0] == "conv":
                 c = op[1]
-                c.bwd(*self.params[c.name], self.ws, want_dx=True)
+                gsz = 1 if i >= nconv - tail else group
+                i += 1
+                r = c.bwd(*self.params[c.name], self.ws, want_dx=True, side=sd, ws_side=self.ws_side,
+                          pending=flush if len(queued) >= gsz else None)
+                if r is not None:
+                    queued.append(r)
             elif op[0] == "pool":
                 _, pp, _, _, idx, ddst, dsrc = op
                 nb.numbat_maxpool5_bwd(pp, ddst, idx, dsrc, True)
             else:
                 _, pp, _, _, ddst, dsrc = op
                 nb.numbat_upsample2x_bwd(pp, ddst, dsrc, True)
+        if sd is not None:
+            flush()
+            # the next forward overwrites the activations the weight gradients read
+            torch.cuda.current_stream().wait_stream(sd)
 
-    def step(self):
+    def step(self, overlap=True):
         self.forward()
-        self.backward()
+        self.backward(overlap)

@@ -7,6 +7,10 @@ max-pool backwards, the outputs' upstream gradients).  That checks every connect
 network -- views, concat offsets, accumulation flags -- while bf16 rounding of intermediate
 activations cannot accumulate over the network's depth.
 
+The benchmarked step runs the weight gradients on a second stream; it is first checked bit
+for bit against the same step on one stream (every layer's dw, dgamma, dbeta, y and the
+image gradient), then the two-stream step's results are compared with the oracle.
+
 Tolerances: rel_inf <= 2e-2 for every bf16 output and gradient; batch statistics 1e-5;
 pooled values, first-maximum positions and upsampled copies bit for bit.  The end-to-end
 distance of the three outputs from the oracle's (run from the same seeded input, so bf16
@@ -43,9 +47,18 @@ def test_chain_network_stage_isolated(affine):
     n, hin = 1, 320
     det = Detector(n, hin, EPS)
     host, xb, gs = det.seeded(40, affine=affine)
-    print(f"chain network n={n} input {hin}: GPU step", flush=True)
+    print(f"chain network n={n} input {hin}: GPU step on one stream", flush=True)
+    det.step(overlap=False)
+    torch.cuda.synchronize()
+    keys = lambda: {**{(c.name, k): getattr(c, k).clone() for c in det.layers for k in ("dw", "dgamma", "dbeta", "y")},
+                    ("image", "dx"): det.dx.clone()}
+    serial = keys()
+    print("GPU step, weight gradients on the side stream", flush=True)
     det.step()
     torch.cuda.synchronize()
+    now = keys()
+    bad = [k for k in serial if not torch.equal(serial[k], now[k])]
+    assert not bad, f"two-stream step differs from the serial one: {bad[:5]}"
     print("oracle, stage by stage", flush=True)
     W = {k: (f64(w), g.astype(np.float64), b.astype(np.float64)) for k, (w, g, b) in host.items()}
     contrib = {}  # gradient buffer -> (buffer, expected sum of every contribution to its channels)
