@@ -59,21 +59,28 @@ __device__ __forceinline__ v2u_t table_read(const uint2* p) {
   return r;
 }
 
-template <int TMO, int S, int BR>
+// Output-channel tiles of BMO = 64, 128 or 192 rows take the four waves as 2 (o) x 2 (k),
+// each wave BMO/2 rows x 64 columns; 96-row tiles take them as 1 x 4, each wave all 96
+// rows x 32 columns.  dy is staged in DS = ceil(BMO / 64) sub-tiles of 64 channels (the
+// upper half of a 96-row tile's second sub-tile loads zeros).
+template <int BMO, int S, int BR>
 struct WgDmaShape {
-  static constexpr int BMO = 64 * TMO;
-  static constexpr int D_ELEMS = TMO * BR * 64;  // dy: TMO sub-tiles of [BR px][64 ch]
+  static constexpr int DS = (BMO + 63) / 64;
+  static constexpr int WM = BMO == 96 ? 1 : 2, WN = 4 / WM;  // waves along o, along k
+  static constexpr int TM = BMO / 32 / WM, TN = BNK / 32 / WN;  // 32 x 32 blocks per wave
+  static constexpr int D_ELEMS = DS * BR * 64;   // dy: DS sub-tiles of [BR px][64 ch]
   static constexpr int X_ELEMS = 2 * BR * 64;    // x: 2 sub-tiles of [BR px][64 k]
   static constexpr int RBW = BR / 32;            // 8-pixel row blocks per wave per sub-tile
-  static constexpr int LOADS = (TMO + 2) * RBW;  // load instructions per thread per step
+  static constexpr int LOADS = (DS + 2) * RBW;   // load instructions per thread per step
   static constexpr int PENDING = (S - 2) * LOADS;
   static constexpr int LDS_BYTES = S * (D_ELEMS + X_ELEMS) * 2 + 2 * BR * 8;
+  static_assert(BMO == 64 || BMO == 96 || BMO == 128 || BMO == 192, "output-channel tile");
 };
 
-template <int TMO, int S, int BR>
+template <int BMO, int S, int BR>
 __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div_wo, FastDiv div_howo) {
-  using Sh = WgDmaShape<TMO, S, BR>;
-  constexpr int BMO = Sh::BMO, TM = TMO, TN = 2, RBW = Sh::RBW;
+  using Sh = WgDmaShape<BMO, S, BR>;
+  constexpr int DS = Sh::DS, TM = Sh::TM, TN = Sh::TN, RBW = Sh::RBW;
   static_assert(BR == 32 || BR == 64, "pixels per step");
   static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
   static_assert(Sh::PENDING <= 63, "load counter range");
@@ -104,7 +111,7 @@ __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = Sh::WM == 1 ? 0 : (wave & 1), wn = Sh::WM == 1 ? wave : (wave >> 1);
   const int half = lane >> 5;
   const uint32_t gx = gridDim.x, gy = gridDim.y;
   const uint32_t lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
@@ -122,11 +129,11 @@ __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div
   const int ck = (lane & 7) ^ (4 * ((lane >> 4) & 1));
   const int prow = lane >> 3;  // pixel row within the 8-row block
   const uint32_t dpix2 = (uint32_t)a.dy_pix * 2, xpix2 = (uint32_t)a.x_pix * 2;
-  uint32_t dcol[TMO];  // dy: byte offset of this lane's 8 channels in sub-tile h (kOobW past c_out)
+  uint32_t dcol[DS];  // dy: byte offset of this lane's 8 channels in sub-tile h (kOobW past the tile or c_out)
 #pragma unroll
-  for (int h = 0; h < TMO; ++h) {
-    const int o = o0 + 64 * h + 8 * ck;
-    dcol[h] = o < a.co ? (uint32_t)o * 2 : kOobW;
+  for (int h = 0; h < DS; ++h) {
+    const int ol = 64 * h + 8 * ck, o = o0 + ol;
+    dcol[h] = (o < a.co && ol < BMO) ? (uint32_t)o * 2 : kOobW;
   }
   uint32_t xcol[2];  // x: tap offset + channel offset (bytes) of this lane's 8 k columns
   int xtap[2];       // their tap (31: past k_total; bit 31 of a tap mask is clear)
@@ -183,7 +190,7 @@ __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div
 #pragma unroll
     for (int u = 0; u < RBW; ++u) e[u] = table_read(&s_pix[st & 1][(wave + 4 * u) * 8 + prow]);
 #pragma unroll
-    for (int h = 0; h < TMO; ++h)
+    for (int h = 0; h < DS; ++h)
 #pragma unroll
       for (int u = 0; u < RBW; ++u) {
         const int rb = wave + 4 * u;  // row block
@@ -241,7 +248,10 @@ __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div
         af[i] = frag(D, ol >> 6, (ol >> 5) & 1, ks);
       }
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bf[j] = frag(X, wn, j, ks);
+      for (int j = 0; j < TN; ++j) {
+        const int cb = wn * TN + j;  // 32-column block of the tile
+        bf[j] = frag(X, cb >> 1, cb & 1, ks);
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -305,7 +315,7 @@ __global__ __launch_bounds__(256) void wgrad_dma_kernel(WgradArgs a, FastDiv div
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int k = k0 + wn * 64 + j * 32 + l32;
+      const int k = k0 + (wn * TN + j) * 32 + l32;
       if (k >= a.ktot) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -367,34 +377,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float4* part, 
 
 }  // namespace
 
-// Kernel configuration for a weight gradient: output-channel tile 64*tmo (1..3), pixels
-// per step br (32 or 64), LDS stages.  Chosen from the problem only, so the workspace size
-// and the launch agree.
+// Kernel configuration for a weight gradient: output-channel tile bmo (64, 96, 128 or
+// 192), pixels per step br (32 or 64), LDS stages.  Chosen from the problem only, so the
+// workspace size and the launch agree.
 struct WgCfg {
-  int tmo, stages, br;
+  int bmo, stages, br;
 };
-static WgCfg wgrad_cfg(int co) {
-  // 128-channel tiles where they pad c_out no more than 64-channel ones (fewer re-reads of
-  // x), else 64 (three blocks per CU instead of two); two stages of 64 pixels.  Fitted to
-  // a sweep of tile, stages and pixels per step over the detector's layers (32 pixels per
-  // step and 192-channel tiles lost everywhere)
-  const bool wide = co > 64 && (co + 127) / 128 * 128 == (co + 63) / 64 * 64;
-  WgCfg c{wide ? 2 : 1, 2, 64};
-#ifdef NUMBAT_TUNING
-  if (const char* e = getenv("NUMBAT_WG_TMO")) c.tmo = atoi(e);
-  if (const char* e = getenv("NUMBAT_WG_STAGES")) c.stages = atoi(e);
-  if (const char* e = getenv("NUMBAT_WG_BR")) c.br = atoi(e);
-#endif
-  return c;
-}
-int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
-  const WgCfg c = wgrad_cfg(co);
-  const int bmo = 64 * c.tmo;
-  const int tiles = (int)(((co + bmo - 1) / bmo) * ((ktot + BNK - 1) / BNK));
-  const int64_t steps = (m + kSplitQuantum - 1) / kSplitQuantum;
-  // As many splits as fill 512 block slots (two per CU; with three blocks resident per
-  // CU, 768 slots measured slower: shorter splits, more partials to reduce); at least 16
-  // quanta per split, at most 256 splits, partials at most 64 MiB
+// splits of the pixel range for `tiles` output tiles over `steps` 64-pixel quanta: as many
+// as fill 512 block slots (two per CU; with three blocks resident per CU, 768 slots
+// measured slower: shorter splits, more partials to reduce), at least 16 quanta per
+// split, at most 256 splits
+static int64_t wgrad_splits_for(int64_t tiles, int64_t steps) {
   int64_t slots = 512;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_WG_SLOTS")) slots = atoi(e);
@@ -403,6 +396,51 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
   const int64_t max_by_steps = steps / 16 > 0 ? steps / 16 : 1;
   if (splits > max_by_steps) splits = max_by_steps;
   if (splits > 256) splits = 256;
+  return splits < 1 ? 1 : splits;
+}
+static WgCfg wgrad_cfg(int64_t m, int co, int ktot) {
+  // The output-channel tile among 64, 96 and 128 rows: where the split grid of a tile
+  // leaves it under 350 blocks (small pixel counts cap the splits), the one with the most
+  // blocks; otherwise the one that pads c_out least, then has the fewest tiles (fewer
+  // re-reads of x).  Two stages of 64 pixels.  Measured over the detector's layer shapes
+  // at batch 16 against 64 / 128-row tiles alone: 3% less weight-gradient time (96-row
+  // tiles on the 96-, 192- and 288-channel 3x3 layers and the stride-2 576-channel one);
+  // 32 pixels per step, three stages and 192-row tiles lost everywhere.
+  const int64_t steps = (m + kSplitQuantum - 1) / kSplitQuantum;
+  const int64_t kt = (ktot + BNK - 1) / BNK;
+  int best = 64;
+  int64_t bkey[3] = {INT64_MAX, INT64_MAX, INT64_MAX};
+  for (const int b : {64, 96, 128}) {
+    const int64_t ot = (co + b - 1) / b, tiles = ot * kt;
+    const int64_t blocks = tiles * wgrad_splits_for(tiles, steps);
+    const bool under = blocks < 350;
+    const int64_t key[3] = {under ? 1 : 0, under ? -blocks : ot * b - co, tiles};
+    if (key[0] < bkey[0] || (key[0] == bkey[0] && (key[1] < bkey[1] || (key[1] == bkey[1] && key[2] < bkey[2])))) {
+      best = b;
+      bkey[0] = key[0];
+      bkey[1] = key[1];
+      bkey[2] = key[2];
+    }
+  }
+  WgCfg c{best, 2, 64};
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_WG_BMO")) c.bmo = atoi(e);
+  if (const char* e = getenv("NUMBAT_WG_OLD")) {  // 64 / 128-row tiles alone
+    const bool wide = co > 64 && (co + 127) / 128 * 128 == (co + 63) / 64 * 64;
+    if (atoi(e)) c.bmo = wide ? 128 : 64;
+  }
+  if (const char* e = getenv("NUMBAT_WG_STAGES")) c.stages = atoi(e);
+  if (const char* e = getenv("NUMBAT_WG_BR")) c.br = atoi(e);
+#endif
+  return c;
+}
+int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
+  const WgCfg c = wgrad_cfg(m, co, ktot);
+  const int bmo = c.bmo;
+  const int tiles = (int)(((co + bmo - 1) / bmo) * ((ktot + BNK - 1) / BNK));
+  const int64_t steps = (m + kSplitQuantum - 1) / kSplitQuantum;
+  int64_t splits = wgrad_splits_for(tiles, steps);
+  // partials at most 64 MiB
   const int64_t part_bytes = (int64_t)co * ktot * 4;
   while (splits > 1 && splits * part_bytes > (64ll << 20)) --splits;
   if (splits < 1) splits = 1;
@@ -413,18 +451,17 @@ int wgrad_pick_splits(int64_t m, int co, int ktot, int64_t* rows_per_split) {
 }
 
 namespace {
-template <int TMO, int S, int BR>
+template <int BMO, int S, int BR>
 hipError_t launch_w(const WgradArgs& a, hipStream_t s) {
-  constexpr int BMO = 64 * TMO;
   dim3 grid((a.co + BMO - 1) / BMO, (a.ktot + BNK - 1) / BNK, a.splits);
   const FastDiv dwo = make_fastdiv((uint32_t)a.wo), dhw = make_fastdiv((uint32_t)(a.ho * a.wo));
-  NUMBAT_LAUNCH((wgrad_dma_kernel<TMO, S, BR>), grid, dim3(256), 0, s, a, dwo, dhw);
+  NUMBAT_LAUNCH((wgrad_dma_kernel<BMO, S, BR>), grid, dim3(256), 0, s, a, dwo, dhw);
   return hipGetLastError();
 }
-template <int TMO>
-hipError_t launch_w_tmo(const WgradArgs& a, const WgCfg& c, hipStream_t s) {
-  if (c.br == 32) return c.stages == 3 ? launch_w<TMO, 3, 32>(a, s) : launch_w<TMO, 2, 32>(a, s);
-  return c.stages == 3 ? launch_w<TMO, 3, 64>(a, s) : launch_w<TMO, 2, 64>(a, s);
+template <int BMO>
+hipError_t launch_w_bmo(const WgradArgs& a, const WgCfg& c, hipStream_t s) {
+  if (c.br == 32) return c.stages == 3 ? launch_w<BMO, 3, 32>(a, s) : launch_w<BMO, 2, 32>(a, s);
+  return c.stages == 3 ? launch_w<BMO, 3, 64>(a, s) : launch_w<BMO, 2, 64>(a, s);
 }
 }  // namespace
 
@@ -436,12 +473,13 @@ hipError_t wgrad_launch(const WgradArgs& args, hipStream_t s) {
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_REMAP_WG")) a.remap = atoi(e);
 #endif
-  const WgCfg c = wgrad_cfg(a.co);
+  const WgCfg c = wgrad_cfg(a.m, a.co, a.ktot);
   trace_begin(KC_WGRAD);
   hipError_t e;
-  if (c.tmo == 1) e = launch_w_tmo<1>(a, c, s);
-  else if (c.tmo == 3) e = launch_w_tmo<3>(a, c, s);
-  else e = launch_w_tmo<2>(a, c, s);
+  if (c.bmo == 64) e = launch_w_bmo<64>(a, c, s);
+  else if (c.bmo == 96) e = launch_w_bmo<96>(a, c, s);
+  else if (c.bmo == 192) e = launch_w_bmo<192>(a, c, s);
+  else e = launch_w_bmo<128>(a, c, s);
   trace_end(KC_WGRAD);
   return e;
 }
