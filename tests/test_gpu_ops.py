@@ -84,6 +84,10 @@ CONV_CASES = [
     (2, 20, 20, 256, 96, 3, 1),
     (1, 21, 19, 272, 80, 3, 1),
     (2, 41, 41, 256, 64, 3, 2),
+    # weight gradients on 96-row output-channel tiles (four waves along k): 96 and 192
+    # output channels over enough pixels that the split grid fills the GPU
+    (2, 160, 160, 96, 96, 3, 1),
+    (2, 160, 160, 64, 192, 3, 1),
 ]
 
 
