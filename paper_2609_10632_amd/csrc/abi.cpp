@@ -190,7 +190,7 @@ bool halo_geometry(const ConvDesc& d) {
 TileCfg halo_tile(const ConvDesc& d, int cs, int nout, bool bt) {
   if (!halo_geometry(d) || cs % 16 != 0 || cs < 32 || (int64_t)nout * 9 * cs * 2 >= ((int64_t)1 << 31) - 16)
     return TileCfg{0, 0, -1, kVariantGeneric};
-  return convhalo_pick(d.m, nout, d.w, bt);
+  return convhalo_pick(d.m, nout, d.h, d.w, bt);
 }
 
 TileCfg fwd_tile(const ConvDesc& d) {

@@ -1127,7 +1127,7 @@ __global__ __launch_bounds__(256) void convstem_kernel(ConvGemmArgs a) {
 // past the end of K they read zeros.  Halo buffers and weight stages are distinct LDS
 // objects selected at compile time (two chunks per loop trip), so the compiler can tell an
 // in-flight load's target from the buffer being read.
-template <int TM, int TN, int HI, int KT, int SB, bool BT>
+template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC>
 struct HaloShape {
   using G = GemmShape<TM, TN, 4>;
   static constexpr int NW = 4;
@@ -1141,12 +1141,17 @@ struct HaloShape {
   static_assert(KT == 1 || KT == 3, "one tap or one tap row per step");
   static_assert((2 * SPC) % SB == 0, "stage of a step known at compile time over two chunks");
   static_assert(SB >= 2 && SB - 1 <= SPC, "prefetch within one chunk");
+  // two-dimensional tiles (TC > 0): TR x TC output pixels of one image, whose padded halo of
+  // (TR + 2) x (TC + 2) pixels fits the buffer
+  static constexpr int TR = TC > 0 ? G::BM / TC : 0;
+  static_assert(TC == 0 || (G::BM % TC == 0 && (TR + 2) * (TC + 2) <= HPAD), "2D tile and its halo");
 };
 
-template <int TM, int TN, int HI, int KT, int SB, bool BT>
+template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC>
 __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   using G = GemmShape<TM, TN, 4>;
-  using Sh = HaloShape<TM, TN, HI, KT, SB, BT>;
+  using Sh = HaloShape<TM, TN, HI, KT, SB, BT, TC>;
+  constexpr int TR = Sh::TR;
   constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM, NW = 4, SPC = Sh::SPC, D = SB - 1;
   constexpr int BI = Sh::BI, BI_MIN = Sh::BI_MIN, BI_MAX = Sh::BI_MAX, TBYTES = Sh::TBYTES;
   static_assert((D - 1) * BI_MIN + HI <= 60, "load counter range");
@@ -1187,6 +1192,17 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   const int W = a.ws, H = a.hs, cs = a.cs, nout = a.nout;
   const int64_t pix2 = a.src_pix * 2;
   const int64_t npix = (int64_t)a.nimg * H * W;
+  // a two-dimensional tile: image img2, output rows h0 .. h0 + TR, columns w0 .. w0 + TC
+  // (the host checks that TR divides H and TC divides W, so every tile is whole)
+  int img2 = 0, h0 = 0, w0 = 0;
+  if constexpr (TC > 0) {
+    const int ncol = W / TC, nrow = H / TR;
+    img2 = T.mt / (nrow * ncol);
+    const int rem = T.mt - img2 * nrow * ncol;
+    const int tr = rem / ncol;
+    h0 = tr * TR;
+    w0 = (rem - tr * ncol) * TC;
+  }
 
   // zero rows read by out-of-image taps (never a load target)
   if (tid < 4) {
@@ -1195,8 +1211,12 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   }
 
   // ---- halo loads: instruction q of this wave fills pixels (q*NW + wave)*16 .. +16; the
-  // lane's slot is lane % 4 of pixel lane / 4, holding chunk slot ^ ((pixel >> 2) & 3)
-  const int64_t hbase_px = (int64_t)m0 - W - 1;
+  // lane's slot is lane % 4 of pixel lane / 4, holding chunk slot ^ ((pixel >> 2) & 3).
+  // Linear tiles: halo pixel j is source pixel m0 - W - 1 + j.  Two-dimensional tiles:
+  // halo pixel j is (row j / (TC + 2), column j % (TC + 2)) of the padded window whose
+  // corner is (h0 - 1, w0 - 1); its pixels outside the image load zeros (the padding).
+  const int64_t hbase_px =
+      TC > 0 ? ((int64_t)img2 * H + h0 - 1) * W + w0 - 1 : (int64_t)m0 - W - 1;
   const __amdgpu_buffer_rsrc_t rsA = buffer_rsrc(a.src + hbase_px * a.src_pix);
   uint32_t hoff[HI];
   int hc8[HI];  // channel of the lane's chunk within a 32-channel chunk
@@ -1204,10 +1224,18 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   for (int q = 0; q < HI; ++q) {
     const int j = (q * NW + wave) * 16 + (lane >> 2);
     const int lc = (lane & 3) ^ ((j >> 2) & 3);
-    const int64_t src_px = hbase_px + j;
-    const bool ok = src_px >= 0 && src_px < npix && j < BM + 2 * W + 2;
-    hoff[q] = ok ? (uint32_t)(j * pix2 + lc * 16) : kOob;
-    hc8[q] = ok ? lc * 8 : (1 << 20);
+    if constexpr (TC > 0) {
+      const int hr = j / (TC + 2), hcol = j - hr * (TC + 2);
+      const bool ok = j < (TR + 2) * (TC + 2) && (unsigned)(h0 - 1 + hr) < (unsigned)H &&
+                      (unsigned)(w0 - 1 + hcol) < (unsigned)W;
+      hoff[q] = ok ? (uint32_t)(((int64_t)hr * W + hcol) * pix2 + lc * 16) : kOob;
+      hc8[q] = ok ? lc * 8 : (1 << 20);
+    } else {
+      const int64_t src_px = hbase_px + j;
+      const bool ok = src_px >= 0 && src_px < npix && j < BM + 2 * W + 2;
+      hoff[q] = ok ? (uint32_t)(j * pix2 + lc * 16) : kOob;
+      hc8[q] = ok ? lc * 8 : (1 << 20);
+    }
   }
   // ---- weight loads: instruction u of a step covers 1 KiB of tap u / (BI / KT)'s stage
   const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
@@ -1270,11 +1298,24 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
     }
   };
 
-  // ---- this lane's A rows: the LDS address of every tap of its rows (zero row outside)
+  // ---- this lane's A rows: the LDS address of every tap of its rows (linear tiles: the
+  // zero row for taps outside the image; two-dimensional tiles: the padded window holds
+  // those zeros itself)
   uint32_t aaddr[TM][9];
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int prow = wave * WTM + i * 32 + l32;
+    if constexpr (TC > 0) {
+      const int ir = prow / TC, ic = prow - ir * TC;
+#pragma unroll
+      for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+          const int p = (ir + r) * (TC + 2) + ic + s;
+          aaddr[i][3 * r + s] = (uint32_t)(p * 64 + (((half) ^ ((p >> 2) & 3)) << 4));
+        }
+      continue;
+    }
     const int m = m0 + prow;
     uint32_t mask = 0;
     if (m < Ge.m) {
@@ -1399,7 +1440,10 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   if constexpr (D >= 4) issue_b(Ic<3>{}, 3);
   if constexpr (D >= 5) issue_b(Ic<4>{}, 4);
   // destination offsets of the tile's rows (the epilogue's), under the first loads
-  for (int r = tid; r < BM; r += NW * 64) s_dst[r] = dst_offset(a, Ge, m0 + r);
+  for (int r = tid; r < BM; r += NW * 64) {
+    const int m = TC > 0 ? (img2 * H + h0 + r / (TC > 0 ? TC : 1)) * W + w0 + r % (TC > 0 ? TC : 1) : m0 + r;
+    s_dst[r] = dst_offset(a, Ge, m);
+  }
   int c = 0;
   for (; c + 2 <= nchunk; c += 2) {
     chunk(Ic<0>{}, c);
@@ -1477,30 +1521,38 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
 }
 
 // halo kernel instantiations: (32-row tiles per wave, 32-column tiles, halo load
-// instructions per wave, taps per step, weight stages); a BM-row tile of a W-wide image
-// needs BM + 2 W + 2 halo pixels, 16 per instruction
+// instructions per wave, taps per step, weight stages, tile columns); a linear BM-row tile
+// (tile columns 0) of a W-wide image needs BM + 2 W + 2 halo pixels, a two-dimensional
+// TR x TC tile (TC tile columns) (TR + 2) x (TC + 2), 16 per instruction
 struct HInst {
-  int tm, tn, hi, kt, sb;
+  int tm, tn, hi, kt, sb, tc;
 };
 constexpr HInst kH[] = {
-    {1, 3, 4, 3, 2},  // 0: 128 x 96, W <= 63, a tap row per step, two weight stages
-    {2, 3, 7, 1, 3},  // 1: 256 x 96, W <= 95, one tap per step, three weight stages
-    {1, 2, 4, 3, 2},  // 2: 128 x 64, W <= 63
-    {2, 2, 7, 1, 3},  // 3: 256 x 64, W <= 95
+    {1, 3, 4, 3, 2, 0},   // 0: 128 x 96, W <= 63, a tap row per step, two weight stages
+    {2, 3, 7, 1, 3, 0},   // 1: 256 x 96, W <= 95, one tap per step, three weight stages
+    {1, 2, 4, 3, 2, 0},   // 2: 128 x 64, W <= 63
+    {2, 2, 7, 1, 3, 0},   // 3: 256 x 64, W <= 95
+    {2, 3, 6, 1, 3, 32},  // 4: 256 x 96 on 8 x 32 output pixels (a 10 x 34 halo), one tap per step
+    {2, 2, 6, 1, 3, 32},  // 5: 256 x 64 on 8 x 32
 #ifdef NUMBAT_TUNING
-    {1, 3, 4, 1, 3},   // 4..
-    {1, 3, 5, 1, 3},
-    {2, 3, 6, 1, 3},
-    {1, 2, 8, 1, 3},
-    {2, 2, 10, 1, 3},
-    {1, 3, 4, 1, 6},
-    {1, 3, 4, 3, 3},
-    {2, 3, 6, 1, 6},
-    {2, 3, 6, 3, 2},
-    {1, 3, 5, 1, 6},
-    {1, 3, 5, 3, 2},
-    {2, 3, 7, 1, 6},
-    {2, 3, 7, 3, 2},
+    {1, 3, 4, 1, 3, 0},   // 6..
+    {1, 3, 5, 1, 3, 0},
+    {2, 3, 6, 1, 3, 0},
+    {1, 2, 8, 1, 3, 0},
+    {2, 2, 10, 1, 3, 0},
+    {1, 3, 4, 1, 6, 0},
+    {1, 3, 4, 3, 3, 0},
+    {2, 3, 6, 1, 6, 0},
+    {2, 3, 6, 3, 2, 0},
+    {1, 3, 5, 1, 6, 0},
+    {1, 3, 5, 3, 2, 0},
+    {2, 3, 7, 1, 6, 0},
+    {2, 3, 7, 3, 2, 0},
+    {1, 2, 4, 1, 3, 32},  // 19..: two-dimensional tiles
+    {1, 2, 3, 3, 2, 16},
+    {1, 3, 3, 3, 2, 16},
+    {1, 3, 4, 3, 2, 32},
+    {1, 2, 4, 3, 2, 32},
 #endif
 };
 constexpr int kNumH = sizeof(kH) / sizeof(kH[0]);
@@ -1512,9 +1564,9 @@ hipError_t launch_h(const ConvGemmArgs& a, hipStream_t s) {
     using G = GemmShape<c.tm, c.tn, 4>;
     dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
     if (a.bt)
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc>), grid, dim3(256), 0, s, a);
     else
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -1750,31 +1802,48 @@ bool convhalo_shape(const ConvGemmArgs& a) {
   return (int64_t)a.nout * 9 * a.cs * 2 < (int64_t)kRecords;
 }
 
+// the halo pixels a tile needs: a linear BM-row tile (tc 0) of a w-wide image, or a
+// two-dimensional (BM / tc) x tc one
+static int halo_pixels(int bm, int tc, int w) { return tc > 0 ? (bm / tc + 2) * (tc + 2) : bm + 2 * w + 2; }
+
 // Halo kernel tile, from a sweep of the instantiations over the detector's 3x3 stride-1
 // layers at batch 16 (each layer alone): 96 columns when 96 divides the channel count, else
 // 64; images up to 63 pixels wide on 128-row tiles with a whole tap row (three taps) per
 // step and two weight stages (40 x 40, 192 channels: forward 33.6 -> 29.6 us, data
 // gradient 29.4 -> 24.0), up to 95 wide on 256-row tiles with one tap per step and three
-// stages (80 x 80, 96 channels: 35.4 -> 28.3 and 28.9 -> 22.6 us); wider images (the
-// 160-wide, 48-channel layers measured 30-80% slower on every instantiation) and forward
-// grids of fewer than 256 tiles (20 x 20, 288 channels: 23.6 -> 26.1 us) keep the
-// direct-to-LDS kernel.  Returns variant kVariantGeneric when the halo kernel is not used.
-TileCfg convhalo_pick(int64_t m, int nout, int w, bool bt) {
+// stages (80 x 80, 96 channels: 35.4 -> 28.3 and 28.9 -> 22.6 us); wider images on
+// two-dimensional tiles of 8 x 32 output pixels with one tap per step and three stages,
+// when 32 divides the width and 8 the height (160 x 160, 48 channels: forward 54.5 -> 51.1,
+// data gradient 44.2 -> 39.3 us against the direct-to-LDS kernel; a linear tile of a
+// 160-wide image needs 2.5 image rows of halo and measured 30-80% slower, 4 x 32 tiles
+// with a tap row per step 10-20% slower, and 8 x 16 tiles on the 80-wide layers 13-18%
+// slower than their linear 256-row tiles).  Forward grids of fewer than 256 tiles (20 x 20,
+// 288 channels: 23.6 -> 26.1 us) keep the direct-to-LDS kernel.  Returns variant
+// kVariantGeneric when the halo kernel is not used.
+TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt) {
   const int tn = nout % 96 == 0 ? 3 : 2;
-  int tm = w <= 63 ? 1 : 2, kt = w <= 63 ? 3 : 1, sb = w <= 63 ? 2 : 3;
+  int tm = w <= 63 ? 1 : 2, kt = w <= 63 ? 3 : 1, sb = w <= 63 ? 2 : 3, tc = 0;
+  if (w > 95) {
+    tm = 2;
+    kt = 1;
+    sb = 3;
+    tc = 32;
+  }
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_HALO_TM")) tm = atoi(e);
   if (const char* e = getenv("NUMBAT_HALO_KT")) kt = atoi(e);
   if (const char* e = getenv("NUMBAT_HALO_SB")) sb = atoi(e);
+  if (const char* e = getenv("NUMBAT_HALO_TC")) tc = atoi(e);
 #endif
   const TileCfg none{0, 0, -1, kVariantGeneric};
+  if (tc > 0 && (w % tc != 0 || (128 * tm) % tc != 0 || h % (128 * tm / tc) != 0)) return none;
   const int64_t tiles = ((m + 128 * tm - 1) / (128 * tm)) * ((nout + 32 * tn - 1) / (32 * tn));
   if (!bt && tiles < 256) return none;
   int best = -1;
   for (int i = 0; i < kNumH; ++i) {
     const HInst& c = kH[i];
-    if (c.tm != tm || c.tn != tn || c.kt != kt || c.sb != sb) continue;
-    if (c.hi * 64 < 128 * tm + 2 * w + 2) continue;
+    if (c.tm != tm || c.tn != tn || c.kt != kt || c.sb != sb || c.tc != tc) continue;
+    if (c.hi * 64 < halo_pixels(128 * tm, tc, w)) continue;
     if (best < 0 || c.hi < kH[best].hi) best = i;
   }
   if (best < 0) return none;
@@ -1783,7 +1852,10 @@ TileCfg convhalo_pick(int64_t m, int nout, int w, bool bt) {
 
 hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
   if (t.variant != kVariantHalo || t.id < 0 || t.id >= kNumH || !convhalo_shape(a)) return hipErrorInvalidValue;
-  if (kH[t.id].hi * 64 < t.bm + 2 * a.ws + 2) return hipErrorInvalidValue;
+  const HInst& c = kH[t.id];
+  if (c.hi * 64 < halo_pixels(t.bm, c.tc, a.ws)) return hipErrorInvalidValue;
+  // a two-dimensional tile must divide the image (every tile whole)
+  if (c.tc > 0 && (a.ws % c.tc != 0 || a.hs % (t.bm / c.tc) != 0)) return hipErrorInvalidValue;
   trace_begin(cls);
   const hipError_t e = launch_h_id<0>(t.id, a, s);
   trace_end(cls);

@@ -132,10 +132,10 @@ bool convgemm_direct(ConvGemmArgs a, const TileCfg& t);
 // 32-channel chunk (conv_gemm.hip, convhalo_kernel): the forward (K-major weights, taps in
 // off[]) and the data gradient (bt: the OHWI weights read in place, flipped; off[] unused).
 // convhalo_shape: whether the kernel takes the problem; convhalo_pick: its tile for m rows,
-// nout columns and a w-wide image, bt for the data gradient (variant kVariantGeneric when
+// nout columns and an h x w image, bt for the data gradient (variant kVariantGeneric when
 // the halo kernel is not the one to use).
 bool convhalo_shape(const ConvGemmArgs& a);
-TileCfg convhalo_pick(int64_t m, int nout, int w, bool bt);
+TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt);
 hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
 // forward convolution of a narrow input (cs = ci < 8, one phase, wt = OHWI weights with
 // K = taps * ci packed densely); rows per tile and columns per tile of narrow_pick

@@ -84,6 +84,13 @@ CONV_CASES = [
     (2, 20, 20, 256, 96, 3, 1),
     (1, 21, 19, 272, 80, 3, 1),
     (2, 41, 41, 256, 64, 3, 2),
+    # two-dimensional 8 x 32 halo tiles (images wider than 95 whose width 32 divides and
+    # height 8 divides): a non-square image, several small images with a 48-channel chunk
+    # tail (a data gradient only: the forward grid is under 256 tiles), and a height 8 does
+    # not divide (the direct-to-LDS kernel)
+    (1, 64, 128, 48, 96, 3, 1),
+    (3, 16, 96, 48, 64, 3, 1),
+    (1, 30, 128, 32, 64, 3, 1),
     # weight gradients on 96-row output-channel tiles (four waves along k): 96 and 192
     # output channels over enough pixels that the split grid fills the GPU
     (2, 160, 160, 96, 96, 3, 1),
