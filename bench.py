@@ -50,10 +50,10 @@ def parse():
     ap.add_argument("--wgrad-order", choices=("deferred", "immediate"), default="deferred",
                     help="two streams: enqueue layer L's weight gradient after layer L-1's BN backward "
                          "(deferred, default) or right after layer L's data gradient (immediate)")
-    ap.add_argument("--wgrad-group", type=int, default=2,
+    ap.add_argument("--wgrad-group", type=int, default=1,
                     help="deferred order: enqueue the weight gradients in groups of this many layers behind "
                          "one cross-stream wait (each wait costs the main queue a completion signal)")
-    ap.add_argument("--wgrad-tail", type=int, default=8,
+    ap.add_argument("--wgrad-tail", type=int, default=0,
                     help="the last this many layers of the backward pass are enqueued one by one")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None,

@@ -384,11 +384,13 @@ struct WgCfg {
   int bmo, stages, br;
 };
 // splits of the pixel range for `tiles` output tiles over `steps` 64-pixel quanta: as many
-// as fill 512 block slots (two per CU; with three blocks resident per CU, 768 slots
-// measured slower: shorter splits, more partials to reduce), at least 16 quanta per
-// split, at most 256 splits
+// as fill 448 block slots, at least 16 quanta per split, at most 256 splits.  The weight
+// gradients run beside the backward's main chain on a second stream, and a grid that
+// leaves that chain some CUs made the two-stream step faster though the kernels alone are
+// slower: 512 slots (two blocks per CU) 8.925 ms per step, 448 8.82, 384 8.80, 256 8.81 ms
+// (weight-gradient kernels alone 2.24, 2.37, 2.62, 3.15 ms); 768 slots were slower still.
 static int64_t wgrad_splits_for(int64_t tiles, int64_t steps) {
-  int64_t slots = 512;
+  int64_t slots = 448;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_WG_SLOTS")) slots = atoi(e);
 #endif

@@ -2,8 +2,8 @@
 Conv+BN+SiLU layers of the workload table connected as the case study's network (Sec. 6.1:
 CSP backbone of C2f blocks and an SPPF block, PAN-FPN neck with nearest upsampling and
 concatenations), forward and backward.  The backward runs each layer's weight gradient on
-a second stream (nothing later in the backward reads it), enqueued in small groups behind
-one wait for the last data gradient of the group, as the conv-set schedule does.
+a second stream (nothing later in the backward reads it), each enqueued after the next
+layer's BN backward behind a wait for its own data gradient, as the conv-set schedule does.
 
 Every concatenation is a buffer whose channel slices the producers write and the consumers
 read through pixel strides (no copies): a C2f block's halves live in its own concat buffer,
@@ -216,7 +216,7 @@ class Detector:
                 _, pp, src, dst, _, _ = op
                 nb.numbat_upsample2x_fwd(pp, src, dst)
 
-    def backward(self, overlap=True, group=2, tail=8):
+    def backward(self, overlap=True, group=1, tail=0):
         """The backward in reverse program order.  overlap=False keeps everything on the
         current stream; otherwise the weight gradients run on the side stream in groups of
         `group` layers behind one wait (the last `tail` convs of the backward one by one)."""

@@ -13,7 +13,8 @@ import os
 from typing import Optional
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libnumbat_conv.so")
+# the in-tree build; NUMBAT_LIB names another build of the same library (a tuning build)
+LIB_PATH = os.environ.get("NUMBAT_LIB") or os.path.join(HERE, "libnumbat_conv.so")
 
 NUMBAT_ABI_VERSION = 1
 

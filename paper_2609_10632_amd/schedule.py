@@ -122,7 +122,7 @@ class ConvSet:
             l.bind_ws(self.ws, self.ws_side)
         self.side = torch.cuda.Stream()  # default priority
 
-    def step(self, ev=None, overlap=True, defer=True, group=2, tail=8):
+    def step(self, ev=None, overlap=True, defer=True, group=1, tail=0):
         """One training step: every layer's forward, then the backward in reverse order.
         overlap=False keeps everything on the current stream; otherwise the weight gradients
         run on the side stream (`defer`: in groups of `group` layers behind one wait, the
