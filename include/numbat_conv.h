@@ -121,8 +121,8 @@ numbat_status numbat_conv_output_shape(const numbat_conv_problem* p, int32_t* ho
  * the three convolution ops, a numbat_bn_problem* for the two BN ops).  Depends only on
  * the problem, never on the device.  May be 0; then ws may be NULL.
  * Every non-empty workspace begins with a 256-byte header of counters that some kernels use
- * to synchronise all their blocks: it must hold zeros when a workspace is first used (fill
- * it with zeros once after allocating it), and every call leaves it zero again.  One
+ * to coordinate their blocks: it must hold zeros when a workspace is first used (fill it
+ * with zeros once after allocating it), and every call leaves it zero again.  One
  * workspace may serve any number of calls that run one after another; calls that may
  * overlap in time need workspaces of their own. */
 numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* bytes);
