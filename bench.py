@@ -189,6 +189,49 @@ def chain_mode(torch, steps, warmup):
     return out
 
 
+def prologue_fusion(torch, steps):
+    """A C2f bottleneck's second conv fed by its first conv's pre-BN output, at batch 16:
+    the previous layer's BN + SiLU as its own pass (writes the activation) followed by the
+    forward, against the prologue-fused forward that forms the activation in the conv's
+    operand staging (both with batch statistics, graph-replayed on one stream)."""
+    from paper_2609_10632_amd import blocks
+    from paper_2609_10632_amd import numbat as nb
+
+    out = {}
+    for name, (n, h, c) in (("b2.m0.cv2", (16, 160, 48)), ("b4.m0.cv2", (16, 80, 96)),
+                            ("b6.m0.cv2", (16, 40, 192)), ("b8.m0.cv2", (16, 20, 288))):
+        blk = blocks.ConvBlock(n, h, h, c, c, 3, 1)
+        g = torch.Generator(device="cuda").manual_seed(7)
+        yp = torch.randn((n, h, h, c), device="cuda", generator=g).to(torch.bfloat16)
+        w = (torch.randn((c, 3, 3, c), device="cuda", generator=g) * 0.03).to(torch.bfloat16)
+        prev = torch.cat([torch.zeros(c, device="cuda"), torch.ones(c, device="cuda")])
+        ga, be = torch.ones(c, device="cuda"), torch.zeros(c, device="cuda")
+        act = torch.empty_like(yp)
+        y = torch.empty((n, h, h, c), dtype=torch.bfloat16, device="cuda")
+        st = torch.empty(2 * c, device="cuda")
+        sm, sr = torch.empty(c, device="cuda"), torch.empty(c, device="cuda")
+        ws = blocks.workspace(blk.ws_fwd)
+        bnp = nb.bn_problem(n * h * h, c)
+
+        def unfused():
+            nb.numbat_bn_silu_fwd(bnp, yp, prev, ga, be, None, act, sm, sr)
+            nb.numbat_conv_fwd(blk.prob, act, w, y, st, ws)
+
+        def fused():
+            nb.numbat_conv_fwd_bn_silu_prologue(blk.prob, yp, prev, ga, be, 1e-3, w, y, st, ws)
+
+        res = {}
+        for k, f in (("unfused_ms", unfused), ("fused_ms", fused)):
+            for _ in range(3):
+                f()
+            gr = graph_of(torch, f)
+            res[k] = round(time_replays(torch, gr, max(20, steps)), 4)
+            del gr
+        res["saved_ms"] = round(res["unfused_ms"] - res["fused_ms"], 4)
+        out[name] = res
+    return out
+
+
 def optimizer_step(torch, steps):
     """The fused global-norm clip + SGD-Nesterov step over the detector's 243 parameter tensors
     (25.9M fp32 parameters, three groups)."""
@@ -558,6 +601,7 @@ def main():
         print("# extras: chain mode, optimiser step, configuration 5", file=sys.stderr, flush=True)
         out["chain_mode"] = chain_mode(torch, args.steps, args.warmup)
         out["optimizer_step"] = optimizer_step(torch, args.steps)
+        out["prologue_fusion"] = prologue_fusion(torch, args.steps)
         del graph
         torch.cuda.empty_cache()
         out["config5_batch32"] = config_set(torch, 5, 32, max(5, args.steps // 2), 2)

@@ -139,6 +139,24 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
 numbat_status numbat_conv_fwd(const numbat_conv_problem* p, const void* x, const void* w, void* y,
                               float* batch_stats, void* ws, size_t ws_bytes, void* stream);
 
+/* Prologue-fused forward: the previous layer's BN + SiLU applied inside this convolution's
+ * operand staging (Sec. 3.1: fused element-wise work around the kernels of a block chain),
+ *   y = conv(SiLU(BN(y_prev)), w),  BN(v)[c] = gamma[c] (v - mean[c]) / sqrt(var[c] + eps) + beta[c],
+ * with the previous layer's batch statistics prev_stats ([mean][variance], c_in entries
+ * each, as numbat_conv_fwd's batch_stats), so its activation is never written to memory.
+ * y_prev: bf16 NHWC [n,h,w,c_in] (x_pixel_stride); gamma, beta: fp32 [c_in]; w, y,
+ * batch_stats, ws as numbat_conv_fwd (ws sized by numbat_workspace_size(NUMBAT_OP_CONV_FWD)).
+ * The activations are formed with the same fp32 arithmetic and rounding as
+ * numbat_bn_silu_fwd, so y and batch_stats equal numbat_bn_silu_fwd (no residual) followed
+ * by numbat_conv_fwd bit for bit wherever that forward runs the same kernel (3x3 problems
+ * whose grid has at least 256 tiles).  Supported: 3x3, stride 1, pad 1, c_in a multiple of
+ * 16 in 32 .. 1024, images the 3x3 stride-1 kernel takes (up to 95 wide, or a multiple of
+ * 32 wide and 8 high); otherwise NUMBAT_ERR_UNSUPPORTED before any launch. */
+numbat_status numbat_conv_fwd_bn_silu_prologue(const numbat_conv_problem* p, const void* y_prev,
+                                               const float* prev_stats, const float* gamma, const float* beta,
+                                               float eps, const void* w, void* y, float* batch_stats, void* ws,
+                                               size_t ws_bytes, void* stream);
+
 /* Forward convolution plus a per-channel bias, y = conv(x, w) + bias[o]: the detect head's
  * 1x1 prediction convolutions, which carry a bias and no BN (Sec. 6.1 decoupled head).  Same
  * layouts and checks as numbat_conv_fwd; bias: fp32 [c_out]; no statistics, no workspace. */

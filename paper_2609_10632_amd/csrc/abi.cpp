@@ -200,9 +200,24 @@ TileCfg fwd_tile(const ConvDesc& d) {
   return convgemm_pick(d.m, d.co, d.ci, d.kh * d.kw * d.ci, 1, false);
 }
 
+// the prologue-fused forward's tile: the halo kernel on any grid (kVariantGeneric when
+// the problem is not one the halo kernel takes)
+TileCfg prologue_tile(const ConvDesc& d) {
+  if (!halo_geometry(d) || narrow(d) || d.ci % 16 != 0 || d.ci < 32 || d.ci > kProMaxC ||
+      (int64_t)d.co * 9 * d.ci * 2 >= ((int64_t)1 << 31) - 16)
+    return TileCfg{0, 0, -1, kVariantGeneric};
+  return convhalo_pick(d.m, d.co, d.h, d.w, false, true);
+}
+
+// per-tile statistics partials, sized for the forward's tile and the prologue-fused
+// forward's (one workspace serves both)
 size_t fwd_stats_bytes(const ConvDesc& d) {
-  const TileCfg t = fwd_tile(d);
-  const int64_t mt = (d.m + t.bm - 1) / t.bm;
+  const TileCfg t = fwd_tile(d), tp = prologue_tile(d);
+  int64_t mt = (d.m + t.bm - 1) / t.bm;
+  if (tp.variant == kVariantHalo) {
+    const int64_t mp = (d.m + tp.bm - 1) / tp.bm;
+    mt = mp > mt ? mp : mt;
+  }
   return round_up((size_t)mt * d.co * sizeof(float2), 256);
 }
 
@@ -319,11 +334,16 @@ struct PostOp {
   float eps = 0.f;
   const float *bias = nullptr, *gamma = nullptr, *beta = nullptr, *mean = nullptr, *var = nullptr;
 };
+// prologue of the fused forward: the previous layer's BN + SiLU applied to the source
+struct ProOp {
+  const float *gamma = nullptr, *beta = nullptr, *mean = nullptr, *var = nullptr;
+  float eps = 0.f;
+};
 
 numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, void* y, float* batch_stats, void* ws,
-                              void* stream, const PostOp& post = PostOp()) {
+                              void* stream, const PostOp& post = PostOp(), const ProOp* pro = nullptr) {
   const bool vec_in = !narrow(d);
-  const TileCfg t = fwd_tile(d);
+  const TileCfg t = pro ? prologue_tile(d) : fwd_tile(d);
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   char* wsp = static_cast<char*>(ws);
@@ -356,6 +376,13 @@ numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, v
   g.post_beta = post.beta;
   g.post_mean = post.mean;
   g.post_var = post.var;
+  if (pro) {
+    g.pro_gamma = pro->gamma;
+    g.pro_beta = pro->beta;
+    g.pro_mean = pro->mean;
+    g.pro_var = pro->var;
+    g.pro_eps = pro->eps;
+  }
   g.nphase = 1;
   GemmPhase& P = g.ph[0];
   P.wt = wt;
@@ -537,6 +564,34 @@ numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* 
     if (st != NUMBAT_OK) return st;
   }
   return conv_fwd_launch(d, x, w, y, batch_stats, ws_body(ws), stream);
+}
+
+numbat_status numbat_conv_fwd_bn_silu_prologue(const numbat_conv_problem* p, const void* y_prev,
+                                               const float* prev_stats, const float* gamma, const float* beta,
+                                               float eps, const void* w, void* y, float* batch_stats, void* ws,
+                                               size_t ws_bytes, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv_fwd(p, y_prev, w, y, batch_stats, &d);
+  if (st != NUMBAT_OK) return st;
+  if (prev_stats == nullptr || gamma == nullptr || beta == nullptr)
+    return fail(NUMBAT_ERR_NULL, "prev_stats, gamma and beta are required");
+  if ((reinterpret_cast<uintptr_t>(prev_stats) | reinterpret_cast<uintptr_t>(gamma) |
+       reinterpret_cast<uintptr_t>(beta)) & 3u)
+    return fail(NUMBAT_ERR_ALIGN, "prev_stats, gamma and beta must be 4-byte aligned");
+  if (!(eps >= 0.0f)) return fail(NUMBAT_ERR_BAD_DESC, "eps must be >= 0");
+  if (prologue_tile(d).variant != kVariantHalo)
+    return fail(NUMBAT_ERR_UNSUPPORTED,
+                "the prologue-fused forward takes 3x3 stride-1 pad-1 problems with c_in a multiple of 16 in "
+                "32 .. %d on images the halo kernel takes (%dx%d, c_in %d)", kProMaxC, d.h, d.w, d.ci);
+  st = check_ws(ws, ws_bytes, with_header(batch_stats ? fwd_stats_bytes(d) : 0));
+  if (st != NUMBAT_OK) return st;
+  ProOp pro;
+  pro.gamma = gamma;
+  pro.beta = beta;
+  pro.mean = prev_stats;
+  pro.var = prev_stats + d.ci;
+  pro.eps = eps;
+  return conv_fwd_launch(d, y_prev, w, y, batch_stats, batch_stats ? ws_body(ws) : nullptr, stream, PostOp(), &pro);
 }
 
 numbat_status numbat_conv_fwd_bias(const numbat_conv_problem* p, const void* x, const void* w, const float* bias,

@@ -125,10 +125,7 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
   // z = (y - mu) * gamma * rstd + beta, as one multiply-add per element
   float sc[8], bz[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    sc[e] = gamma[cb + e] * (1.0f / sqrtf(var_in[cb + e] + a.eps));
-    bz[e] = beta[cb + e] - mean[cb + e] * sc[e];
-  }
+  for (int e = 0; e < 8; ++e) bn_fold(gamma[cb + e], beta[cb + e], mean[cb + e], var_in[cb + e], a.eps, sc[e], bz[e]);
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
   const int64_t st = L.rows_per_iter;
@@ -149,10 +146,7 @@ __global__ __launch_bounds__(kThreads) void bn_fwd_kernel(BnArgs a, const bf16_t
       float f[8], o[8];
       unpack8(yv[j], f);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float z = __builtin_fmaf(f[e], sc[e], bz[e]);
-        o[e] = z * sigmoidf_fast(z);
-      }
+      for (int e = 0; e < 8; ++e) o[e] = bn_silu_apply(f[e], sc[e], bz[e]);
       if (res != nullptr) {
         float q[8];
         unpack8(rv[j], q);

@@ -94,6 +94,20 @@ __device__ __forceinline__ f32x16 mfma32x32x16(const u32x4& a, const u32x4& b, f
 // sigmoid with the hardware exp2 and reciprocal (about 1 ulp each)
 __device__ __forceinline__ float sigmoidf_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
+// BN with batch statistics + SiLU of one element as a multiply-add with per-channel folded
+// constants: scale = gamma / sqrt(var + eps), shift = beta - mean * scale, z = y scale +
+// shift, a = z sigmoid(z).  The BN forward kernel and the conv prologue both use these, so
+// they form bit-identical activations.
+__device__ __forceinline__ void bn_fold(float gamma, float beta, float mean, float var, float eps, float& sc,
+                                        float& sh) {
+  sc = gamma * (1.0f / sqrtf(var + eps));
+  sh = beta - mean * sc;
+}
+__device__ __forceinline__ float bn_silu_apply(float y, float sc, float sh) {
+  const float z = __builtin_fmaf(y, sc, sh);
+  return z * sigmoidf_fast(z);
+}
+
 // Workgroups are dealt round-robin to the 8 XCDs (linear id L runs on XCD L % 8), and
 // each XCD has its own L2.  Tiles that read the same data should share an XCD, so a
 // kernel whose consecutive logical tiles share data maps its linear id to the logical

@@ -1147,7 +1147,7 @@ struct HaloShape {
   static_assert(TC == 0 || (G::BM % TC == 0 && (TR + 2) * (TC + 2) <= HPAD), "2D tile and its halo");
 };
 
-template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC>
+template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC, bool PRO>
 __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   using G = GemmShape<TM, TN, 4>;
   using Sh = HaloShape<TM, TN, HI, KT, SB, BT, TC>;
@@ -1167,6 +1167,8 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   __shared__ int64_t s_dst[BM];
   __shared__ float s_red[NW][BN];
   __shared__ float s_mean[BN];
+  __shared__ float s_pro[PRO ? 2 * kProMaxC : 1];  // prologue: scale, then shift, per source channel
+  static_assert(!(PRO && BT), "the prologue is a forward's");
   auto hbuf = [&](auto hc) __attribute__((always_inline)) -> unsigned char* {
     if constexpr (decltype(hc)::value == 0) return sH0;
     else return sH1;
@@ -1208,6 +1210,14 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   if (tid < 4) {
     *reinterpret_cast<u32x4*>(sH0 + Sh::HPAD * 64 + tid * 16) = u32x4{0u, 0u, 0u, 0u};
     *reinterpret_cast<u32x4*>(sH1 + Sh::HPAD * 64 + tid * 16) = u32x4{0u, 0u, 0u, 0u};
+  }
+  // prologue: the previous layer's BN constants of every source channel (published by
+  // the barrier below, before any halo is transformed)
+  if constexpr (PRO) {
+    for (int ch = tid; ch < cs; ch += NW * 64)
+      bn_fold(a.pro_gamma[ch], a.pro_beta[ch], a.pro_mean[ch], a.pro_var[ch], a.pro_eps, s_pro[ch],
+              s_pro[kProMaxC + ch]);
+    __syncthreads();
   }
 
   // ---- halo loads: instruction q of this wave fills pixels (q*NW + wave)*16 .. +16; the
@@ -1397,13 +1407,41 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   auto sync = [&](auto nc) __attribute__((always_inline)) {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(decltype(nc)::value) : "memory");
   };
+  // prologue: this lane's own 16-byte chunks of chunk c's halo (landed: the wait before
+  // this covers them) become the previous layer's activations, SiLU(BN(y)), in place;
+  // chunks that loaded zeros (padding, past the image or the channels) stay zero
+  auto transform = [&](auto hc, int c) __attribute__((always_inline)) {
+    unsigned char* Hb = hbuf(hc);
+    const int cb = 32 * c;
+#pragma unroll
+    for (int q = 0; q < HI; ++q) {
+      if (hoff[q] != kOob && cb + hc8[q] < cs) {
+        u32x4* p = reinterpret_cast<u32x4*>(Hb + (q * NW + wave) * 1024 + lane * 16);
+        const u32x4 v = *p;
+        float f[8];
+        unpack8(uint4{v[0], v[1], v[2], v[3]}, f);
+        const int ch = cb + hc8[q];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = bn_silu_apply(f[e], s_pro[ch + e], s_pro[kProMaxC + ch + e]);
+        const uint4 o = pack8(f);
+        *p = u32x4{o.x, o.y, o.z, o.w};
+      }
+    }
+  };
   // step k (0 .. SPC-1) of a chunk c of parity h (halo buffer h): wait, issue the next
   // halo (k = 0) and the weights D steps ahead, multiply the step's KT taps
   auto step = [&](auto hc, auto kc, int c) __attribute__((always_inline)) {
     constexpr int h = decltype(hc)::value, k = decltype(kc)::value;
     constexpr int sl = h * SPC + k;  // step index within the two-chunk trip
     constexpr int waitn = (D - 1) * BI_MIN + ((k >= 1 && k <= D - 1) ? HI : 0);
-    sync(Ic<waitn>{});
+    if constexpr (PRO && k == 0) {
+      // the chunk's halo has landed for this wave: transform this lane's part, then publish
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(waitn) : "memory");
+      transform(hc, c);
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    } else {
+      sync(Ic<waitn>{});
+    }
     if constexpr (k == 0) issue_halo(Ic<1 - h>{}, c + 1);
     issue_b(Ic<(sl + D) % SB>{}, SPC * c + k + D);
     const unsigned char* Hb = hbuf(hc);
@@ -1564,9 +1602,11 @@ hipError_t launch_h(const ConvGemmArgs& a, hipStream_t s) {
     using G = GemmShape<c.tm, c.tn, 4>;
     dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
     if (a.bt)
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, false>), grid, dim3(256), 0, s, a);
+    else if (a.pro_mean != nullptr)
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, true>), grid, dim3(256), 0, s, a);
     else
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, false>), grid, dim3(256), 0, s, a);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -1820,7 +1860,7 @@ static int halo_pixels(int bm, int tc, int w) { return tc > 0 ? (bm / tc + 2) * 
 // slower than their linear 256-row tiles).  Forward grids of fewer than 256 tiles (20 x 20,
 // 288 channels: 23.6 -> 26.1 us) keep the direct-to-LDS kernel.  Returns variant
 // kVariantGeneric when the halo kernel is not used.
-TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt) {
+TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt, bool any_grid) {
   const int tn = nout % 96 == 0 ? 3 : 2;
   int tm = w <= 63 ? 1 : 2, kt = w <= 63 ? 3 : 1, sb = w <= 63 ? 2 : 3, tc = 0;
   if (w > 95) {
@@ -1838,7 +1878,7 @@ TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt) {
   const TileCfg none{0, 0, -1, kVariantGeneric};
   if (tc > 0 && (w % tc != 0 || (128 * tm) % tc != 0 || h % (128 * tm / tc) != 0)) return none;
   const int64_t tiles = ((m + 128 * tm - 1) / (128 * tm)) * ((nout + 32 * tn - 1) / (32 * tn));
-  if (!bt && tiles < 256) return none;
+  if (!bt && !any_grid && tiles < 256) return none;
   int best = -1;
   for (int i = 0; i < kNumH; ++i) {
     const HInst& c = kH[i];
@@ -1852,6 +1892,7 @@ TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt) {
 
 hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
   if (t.variant != kVariantHalo || t.id < 0 || t.id >= kNumH || !convhalo_shape(a)) return hipErrorInvalidValue;
+  if (a.pro_mean != nullptr && (a.bt || a.cs > kProMaxC)) return hipErrorInvalidValue;
   const HInst& c = kH[t.id];
   if (c.hi * 64 < halo_pixels(t.bm, c.tc, a.ws)) return hipErrorInvalidValue;
   // a two-dimensional tile must divide the image (every tile whole)

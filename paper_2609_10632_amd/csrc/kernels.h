@@ -117,8 +117,14 @@ struct ConvGemmArgs {
   float post_eps;
   const float* post_bias;
   const float *post_gamma, *post_beta, *post_mean, *post_var;
+  // prologue (halo kernel, forward): with pro_mean set, the source is the previous layer's
+  // pre-BN output, and its BN (batch statistics pro_mean / pro_var, pro_gamma, pro_beta,
+  // pro_eps) + SiLU is applied to the staged halo before the taps read it
+  const float *pro_gamma, *pro_beta, *pro_mean, *pro_var;
+  float pro_eps;
   GemmPhase ph[kMaxPhases];
 };
+constexpr int kProMaxC = 1024;  // most source channels the prologue stages constants for
 enum { kPostNone = 0, kPostBias = 1, kPostBnSilu = 2 };
 // tile and kernel for a problem with at most m_max rows per phase, nout columns, cs
 // source channels, reduction length ktot and nphase phases; bt: the weights are read in
@@ -132,10 +138,10 @@ bool convgemm_direct(ConvGemmArgs a, const TileCfg& t);
 // 32-channel chunk (conv_gemm.hip, convhalo_kernel): the forward (K-major weights, taps in
 // off[]) and the data gradient (bt: the OHWI weights read in place, flipped; off[] unused).
 // convhalo_shape: whether the kernel takes the problem; convhalo_pick: its tile for m rows,
-// nout columns and an h x w image, bt for the data gradient (variant kVariantGeneric when
-// the halo kernel is not the one to use).
+// nout columns and an h x w image, bt for the data gradient, any_grid to take small forward
+// grids too (variant kVariantGeneric when the halo kernel is not the one to use).
 bool convhalo_shape(const ConvGemmArgs& a);
-TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt);
+TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt, bool any_grid = false);
 hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls);
 // forward convolution of a narrow input (cs = ci < 8, one phase, wt = OHWI weights with
 // K = taps * ci packed densely); rows per tile and columns per tile of narrow_pick

@@ -28,6 +28,7 @@ EXPORTED = (
     "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc", "numbat_clip_sgd_nesterov",
     "numbat_conv_fwd_bias", "numbat_conv_bn_silu_infer", "numbat_bn_silu_infer",
     "numbat_maxpool5_fwd", "numbat_maxpool5_bwd", "numbat_upsample2x_fwd", "numbat_upsample2x_bwd",
+    "numbat_conv_fwd_bn_silu_prologue",
 )
 
 
@@ -90,6 +91,7 @@ def load() -> ctypes.CDLL:
                                                          ctypes.POINTER(ctypes.c_int32)]),
             "numbat_workspace_size": (ctypes.c_int, [ctypes.c_int, P, ctypes.POINTER(S)]),
             "numbat_conv_fwd": (ctypes.c_int, [CP, P, P, P, P, P, S, P]),
+            "numbat_conv_fwd_bn_silu_prologue": (ctypes.c_int, [CP, P, P, P, P, ctypes.c_float, P, P, P, P, S, P]),
             "numbat_conv_fwd_noalloc": (ctypes.c_int, [CP, P, P, P, P, P]),
             "numbat_conv_fwd_bias": (ctypes.c_int, [CP, P, P, P, P, P]),
             "numbat_conv_bn_silu_infer": (ctypes.c_int, [CP, P, P, P, P, P, P, ctypes.c_float, P, P]),
@@ -217,6 +219,15 @@ def numbat_conv_fwd(p, x, w, y, batch_stats=None, ws=None, stream=None, ws_bytes
     _check(load().numbat_conv_fwd(ctypes.byref(p), _ptr(x), _ptr(w), _ptr(y), _ptr(batch_stats), _ptr(ws),
                                   _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
            "numbat_conv_fwd")
+
+
+def numbat_conv_fwd_bn_silu_prologue(p, y_prev, prev_stats, gamma, beta, eps, w, y, batch_stats=None, ws=None,
+                                     stream=None, ws_bytes=None):
+    _check(load().numbat_conv_fwd_bn_silu_prologue(ctypes.byref(p), _ptr(y_prev), _ptr(prev_stats), _ptr(gamma),
+                                                   _ptr(beta), ctypes.c_float(eps), _ptr(w), _ptr(y),
+                                                   _ptr(batch_stats), _ptr(ws),
+                                                   _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+           "numbat_conv_fwd_bn_silu_prologue")
 
 
 def numbat_conv_fwd_noalloc(p, x, w, y, batch_stats=None, stream=None):

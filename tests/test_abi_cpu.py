@@ -21,7 +21,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 23
+    assert len(names) == 24
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -220,3 +220,25 @@ def test_pool_entry_points_refuse_before_any_launch():
     assert status_of(nb.numbat_maxpool5_bwd, good, fake, None, fake) == nb.ERR_NULL
     assert status_of(nb.numbat_upsample2x_fwd, good, fake + 2, fake) == nb.ERR_ALIGN
     assert status_of(nb.numbat_upsample2x_bwd, good, fake, None) == nb.ERR_NULL
+
+
+def test_prologue_forward_refuses_before_any_launch():
+    """The prologue-fused forward checks its extra arguments and takes only the problems the
+    3x3 stride-1 halo kernel takes, all before touching a GPU."""
+    fake = 1 << 20
+    ok = nb.conv_problem(2, 16, 16, 32, 64, 3)
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_fwd_bn_silu_prologue(ok, fake, None, fake, fake, 1e-3, fake, fake)
+    assert ei.value.status == nb.ERR_NULL
+    with pytest.raises(nb.NumbatError) as ei:
+        nb.numbat_conv_fwd_bn_silu_prologue(ok, fake, fake, fake, fake, -1.0, fake, fake)
+    assert ei.value.status == nb.ERR_BAD_DESC
+    for p in (nb.conv_problem(2, 16, 16, 32, 64, 1),           # 1x1
+              nb.conv_problem(2, 16, 16, 32, 64, 3, stride=2),  # stride 2
+              nb.conv_problem(2, 16, 16, 24, 64, 3),           # c_in not a multiple of 16
+              nb.conv_problem(2, 16, 16, 16, 64, 3),           # c_in below 32
+              nb.conv_problem(1, 8, 8, 2048, 64, 3),           # c_in above 1024
+              nb.conv_problem(1, 40, 200, 32, 64, 3)):         # 200 wide: neither halo tiling
+        with pytest.raises(nb.NumbatError) as ei:
+            nb.numbat_conv_fwd_bn_silu_prologue(p, fake, fake, fake, fake, 1e-3, fake, fake)
+        assert ei.value.status == nb.ERR_UNSUPPORTED, p
