@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libnumbat_conv.so")
-SOURCES = ["conv_gemm.hip", "conv_aux.hip", "conv_wgrad.hip", "bn_silu.hip", "optim.hip", "pool.hip", "abi.cpp"]
+SOURCES = ["conv_gemm.hip", "conv_aux.hip", "conv_wgrad.hip", "conv_wgrad_halo.hip", "bn_silu.hip", "optim.hip", "pool.hip", "abi.cpp"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

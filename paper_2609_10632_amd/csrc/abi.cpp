@@ -242,7 +242,51 @@ int64_t stem_wgrad_blocks(const ConvDesc& d) {
   return np < 512 ? np : 512;
 }
 
+// the geometry fields of a weight-gradient launch
+WgradArgs wgrad_geometry(const ConvDesc& d) {
+  WgradArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.x_pix = d.x_pix;
+  a.dy_pix = d.y_pix;
+  a.n = d.n;
+  a.h = d.h;
+  a.w = d.w;
+  a.ci = d.ci;
+  a.co = d.co;
+  a.kh = d.kh;
+  a.kw = d.kw;
+  a.sh = d.sh;
+  a.sw = d.sw;
+  a.ph = d.ph;
+  a.pw = d.pw;
+  a.ho = d.ho;
+  a.wo = d.wo;
+  a.m = d.m;
+  a.ktot = d.kh * d.kw * d.ci;
+  return a;
+}
+
+// 3x3 stride-1 layers whose weight gradient takes the patch-staged kernel: its splits and
+// patches per split
+bool halo_wgrad(const ConvDesc& d, int* splits, int64_t* pps) {
+  int s = 0;
+  int64_t p = 0;
+  if (narrow(d) || !wgrad_halo_plan(wgrad_geometry(d), &s, &p)) return false;
+  if (splits) *splits = s;
+  if (pps) *pps = p;
+  return true;
+}
+
 size_t bwd_weight_ws(const ConvDesc& d, int* splits, int64_t* rps) {
+  {
+    int s = 0;
+    int64_t p = 0;
+    if (halo_wgrad(d, &s, &p)) {  // partials [splits][c_out][9 c_in]
+      if (splits) *splits = s;
+      if (rps) *rps = p;
+      return s > 1 ? round_up((size_t)s * d.co * 9 * d.ci * sizeof(float), 256) : 0;
+    }
+  }
   if (stem_wgrad(d)) {  // per-block partials [blocks][c_out][27]
     if (splits) *splits = 0;
     if (rps) *rps = 0;
@@ -923,7 +967,7 @@ numbat_status numbat_conv_bwd_weight(const numbat_conv_problem* p, const void* x
   a.rows_per_split = rps;
   a.out = splits > 1 ? reinterpret_cast<float*>(wsp) : target;
   a.accumulate = acc;
-  e = wgrad_launch(a, s);
+  e = halo_wgrad(d, nullptr, nullptr) ? wgrad_halo_launch(a, s) : wgrad_launch(a, s);
   if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
   if (splits > 1) {
     e = splitk_reduce_launch(reinterpret_cast<const float*>(wsp), splits, (int64_t)d.co * ktot, target, acc, s);

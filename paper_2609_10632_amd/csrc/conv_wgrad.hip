@@ -342,6 +342,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float4* part, 
   const int s0 = (int)((int64_t)splits * g / G), s1 = (int)((int64_t)splits * (g + 1) / G);
   float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
   if (i < count4) {
+    // (unrolled: the loads of several partials in flight, the sums still in split order)
+#pragma unroll 8
     for (int k = s0; k < s1; ++k) {
       const float4 u = part[(int64_t)k * count4 + i];
       t.x += u.x;

@@ -95,6 +95,14 @@ CONV_CASES = [
     # output channels over enough pixels that the split grid fills the GPU
     (2, 160, 160, 96, 96, 3, 1),
     (2, 160, 160, 64, 192, 3, 1),
+    # patch-staged 3x3 stride-1 weight gradient (the cases above whose sides take 8 x 16,
+    # 20 x 8 or 20 x 4 patches run it too): 72 of 96 output rows on 20 x 8 patches, a
+    # 48-channel chunk with 40 of 64 rows on 20 x 4, one patch (a single split writes dW
+    # and accumulates in place), three 48-channel chunks of a 144-channel input
+    (3, 20, 24, 64, 72, 3, 1),
+    (2, 40, 12, 48, 40, 3, 1),
+    (1, 8, 16, 96, 32, 3, 1),
+    (4, 20, 8, 144, 64, 3, 1),
 ]
 
 
