@@ -356,8 +356,8 @@ def write_detail(torch, args, step, layers, wl):
 # figure is used only while the kernel's sources hash to the value recorded with it.
 TRAFFIC_PROFILES = {
     ("wgrad_igemm", 4, 16): ("profiles/wgrad_igemm_c4_b16_traffic.md",
-                             ("paper_2609_10632_amd/csrc/conv_wgrad.hip", "paper_2609_10632_amd/csrc/common.h",
-                              "paper_2609_10632_amd/csrc/kernels.h")),
+                             ("paper_2609_10632_amd/csrc/conv_wgrad.hip", "paper_2609_10632_amd/csrc/conv_wgrad_halo.hip",
+                              "paper_2609_10632_amd/csrc/common.h", "paper_2609_10632_amd/csrc/kernels.h")),
     ("conv_fwd_igemm", 4, 16): ("profiles/conv_fwd_igemm_c4_b16_traffic.md",
                                 ("paper_2609_10632_amd/csrc/conv_gemm.hip", "paper_2609_10632_amd/csrc/common.h",
                                  "paper_2609_10632_amd/csrc/kernels.h")),
