@@ -184,8 +184,8 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
       be[e] = beta[cb + e];
     }
     const int64_t st = L.rows_per_iter;
-    // eight rows in flight per round: with the block count bn_reduce_blocks picks, two
-    // full rounds (more on layers large enough to meet its block cap)
+    // eight rows in flight per round: with the block count bn_reduce_blocks picks, one
+    // full round (more on layers large enough to meet its block cap)
     for (int64_t r = r0 + rr; r < r1; r += 8 * st) {
       uint4 gv[8], yv[8];
 #pragma unroll
@@ -363,11 +363,13 @@ size_t reduce_smem(int c) {
 }  // namespace
 
 int bn_reduce_blocks(int64_t m, int c) {
-  // 16 rows per active thread, two full rounds of eight: a block covers 16 * rows_per_iter
-  // rows (counting all kThreads threads as active gave most layers a nearly empty last
-  // round).  Two rounds rather than one halve the partials and the CUs the kernel holds
-  // while the weight gradients run beside it: 0.5% faster over the detector's step.
-  int64_t vpt = 16;
+  // 8 rows per active thread, one round: a block covers 8 * rows_per_iter rows (counting
+  // all kThreads threads as active gave most layers a nearly empty last round).  Against
+  // two rounds of eight (half the blocks and partials) the reduce kernels take 0.875
+  // instead of 0.98 ms per step and the two-stream step is unchanged (8.54 ms; with the
+  // earlier weight-gradient kernels two rounds were 0.5% faster); four rows per thread
+  // were slower.
+  int64_t vpt = 8;
 #ifdef NUMBAT_TUNING
   if (const char* e = getenv("NUMBAT_BN_VEC")) vpt = atoi(e);
 #endif

@@ -42,6 +42,15 @@ __device__ __attribute__((aligned(16))) u32x4 kZero16 = {0u, 0u, 0u, 0u};
 template <int V>
 using Ic = std::integral_constant<int, V>;
 
+// f(Ic<I>{}), ..., f(Ic<N - 1>{})
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for_ic(F&& f) {
+  if constexpr (I < N) {
+    f(Ic<I>{});
+    static_for_ic<I + 1, N>(f);
+  }
+}
+
 template <int TM, int TN, int NW = 4>
 struct GemmShape {
   static constexpr int WTM = TM * 32;          // rows per wave
@@ -584,7 +593,7 @@ __global__ __launch_bounds__(NW * 64) void convdma_kernel(ConvGemmArgs a) {
   using Sh = DmaShape<TM, TN, S, BK, NW, BT>;
   constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM;
   constexpr int AI = Sh::AI, BI = Sh::BI, BI_MAX = Sh::BI_MAX, RPI = Sh::RPI, CPR = Sh::CPR, WIN = Sh::WIN;
-  static_assert(S >= 2 && S <= 4, "2..4 LDS stages");
+  static_assert(S >= 2 && S <= 6, "2..6 LDS stages");
   static_assert(BK == 32 || BK == 64, "stage depth");
   static_assert(Sh::PENDING <= 63, "load counter range");
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
@@ -593,10 +602,14 @@ __global__ __launch_bounds__(NW * 64) void convdma_kernel(ConvGemmArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t sA1[Sh::A_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sA2[Sh::A_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sA3[Sh::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sA4[S > 4 ? Sh::A_ELEMS : 8];
+  __shared__ __attribute__((aligned(16))) bf16_t sA5[S > 5 ? Sh::A_ELEMS : 8];
   __shared__ __attribute__((aligned(16))) bf16_t sB0[Sh::B_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sB1[Sh::B_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sB2[Sh::B_ELEMS];
   __shared__ __attribute__((aligned(16))) bf16_t sB3[Sh::B_ELEMS];
+  __shared__ __attribute__((aligned(16))) bf16_t sB4[S > 4 ? Sh::B_ELEMS : 8];
+  __shared__ __attribute__((aligned(16))) bf16_t sB5[S > 5 ? Sh::B_ELEMS : 8];
   __shared__ int64_t s_dst[BM];
   __shared__ float s_red[NW][BN];
   __shared__ float s_mean[BN];
@@ -605,14 +618,18 @@ __global__ __launch_bounds__(NW * 64) void convdma_kernel(ConvGemmArgs a) {
     if constexpr (s == 0) return sA0;
     else if constexpr (s == 1) return sA1;
     else if constexpr (s == 2) return sA2;
-    else return sA3;
+    else if constexpr (s == 3) return sA3;
+    else if constexpr (s == 4) return sA4;
+    else return sA5;
   };
   auto stage_b = [&](auto sc) __attribute__((always_inline)) -> bf16_t* {
     constexpr int s = decltype(sc)::value;
     if constexpr (s == 0) return sB0;
     else if constexpr (s == 1) return sB1;
     else if constexpr (s == 2) return sB2;
-    else return sB3;
+    else if constexpr (s == 3) return sB3;
+    else if constexpr (s == 4) return sB4;
+    else return sB5;
   };
 
   // (launch order: the XCD-aware order measured no faster for these GEMMs; a constant
@@ -838,28 +855,15 @@ __global__ __launch_bounds__(NW * 64) void convdma_kernel(ConvGemmArgs a) {
     issue(Ic<(u + S - 1) % S>{}, kt + S - 1);
     compute(uc);
   };
-  if (nk > 0) {
-    issue(Ic<0>{}, 0);
-    if constexpr (S > 2) issue(Ic<1>{}, 1);
-    if constexpr (S > 3) issue(Ic<2>{}, 2);
-  }
+  if (nk > 0) static_for_ic<0, S - 1>([&](auto ic) { issue(ic, decltype(ic)::value); });
   // destination offsets of the tile's rows, needed only by the epilogue: computed while
   // the first stages load (the first step's barrier publishes them)
   for (int r = tid; r < BM; r += NW * 64) s_dst[r] = dst_offset(a, Ge, m0 + r);
   int kb = 0;
-  for (; kb + S <= nk; kb += S) {
-    step(Ic<0>{}, kb);
-    step(Ic<1>{}, kb + 1);
-    if constexpr (S > 2) step(Ic<2 % S>{}, kb + 2);
-    if constexpr (S > 3) step(Ic<3 % S>{}, kb + 3);
-  }
-  if (kb < nk) step(Ic<0>{}, kb);
-  if constexpr (S > 2) {
-    if (kb + 1 < nk) step(Ic<1>{}, kb + 1);
-  }
-  if constexpr (S > 3) {
-    if (kb + 2 < nk) step(Ic<2>{}, kb + 2);
-  }
+  for (; kb + S <= nk; kb += S) static_for_ic<0, S>([&](auto ic) { step(ic, kb + decltype(ic)::value); });
+  static_for_ic<0, S - 1>([&](auto ic) {
+    if (kb + decltype(ic)::value < nk) step(ic, kb + decltype(ic)::value);
+  });
   // the loads issued past the last step land in LDS before stage 0 becomes staging space
   asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
   gemm_epilogue<TM, TN, NW>(a, P, T, acc, m0, n0, reinterpret_cast<unsigned char*>(sA0), s_dst, s_red, s_mean);
@@ -1549,6 +1553,12 @@ hipError_t launch_g(const ConvGemmArgs& a, int variant, hipStream_t s) {
     launch_dma<1, c.tn <= 4 ? c.tn : 4, 4, 32, 8>(a, mmax, s);
   else if (variant == 10 && c.tn <= 4)
     launch_dma<1, c.tn <= 4 ? c.tn : 4, 3, 32, 8>(a, mmax, s);
+  else if (variant == 12 && c.tm == 1 && c.tn <= 3)
+    launch_dma<1, c.tn <= 3 ? c.tn : 3, 5, 64, 4>(a, mmax, s);
+  else if (variant == 13 && c.tm == 1 && c.tn <= 2)
+    launch_dma<1, c.tn <= 2 ? c.tn : 2, 6, 64, 4>(a, mmax, s);
+  else if (variant == 14 && c.tm == 1)
+    launch_dma<1, c.tn, 6, 32, 4>(a, mmax, s);
 #endif
   else {
     dim3 grid((unsigned)((mmax + Sh::BM - 1) / Sh::BM), (unsigned)((a.nout + Sh::BN - 1) / Sh::BN),
@@ -1760,7 +1770,7 @@ TileCfg convgemm_pick(int64_t m_max, int nout, int cs, int ktot, int nphase, boo
   // timing sweeps only: force the instantiation and kernel
   if (const char* e = getenv("NUMBAT_TILE")) id = atoi(e);
   if (const char* e = getenv("NUMBAT_VARIANT")) variant = fast ? atoi(e) : kVariantGeneric;
-  if (variant >= kVariantDma3W8) id &= 3;  // eight waves of 32 rows: the 256-row instantiations
+  if (variant >= kVariantDma3W8 && variant <= 10) id &= 3;  // eight waves of 32 rows: the 256-row instantiations
   bm = kG[id].tm * 128;
   bn = kG[id].tn * 32;
 #endif
