@@ -266,8 +266,8 @@ WgradArgs wgrad_geometry(const ConvDesc& d) {
   return a;
 }
 
-// 3x3 stride-1 layers whose weight gradient takes the patch-staged kernel: its splits and
-// patches per split
+// 3x3 stride-1 and 1x1 layers whose weight gradient takes the patch-staged kernel: its
+// splits and patches (pixel steps) per split
 bool halo_wgrad(const ConvDesc& d, int* splits, int64_t* pps) {
   int s = 0;
   int64_t p = 0;
@@ -281,10 +281,10 @@ size_t bwd_weight_ws(const ConvDesc& d, int* splits, int64_t* rps) {
   {
     int s = 0;
     int64_t p = 0;
-    if (halo_wgrad(d, &s, &p)) {  // partials [splits][c_out][9 c_in]
+    if (halo_wgrad(d, &s, &p)) {  // partials [splits][c_out][kh kw c_in]
       if (splits) *splits = s;
       if (rps) *rps = p;
-      return s > 1 ? round_up((size_t)s * d.co * 9 * d.ci * sizeof(float), 256) : 0;
+      return s > 1 ? round_up((size_t)s * d.co * d.kh * d.kw * d.ci * sizeof(float), 256) : 0;
     }
   }
   if (stem_wgrad(d)) {  // per-block partials [blocks][c_out][27]

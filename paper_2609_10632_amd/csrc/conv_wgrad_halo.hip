@@ -1,6 +1,8 @@
 // Weight gradient of a 3x3, stride-1, padding-1 convolution on gfx950 MFMA, staged by
 // pixel patches:
-//   dW[o][(r, s, c)] = sum over pixels (n, p, q) of dy[n][p][q][o] * x[n][p + r - 1][q + s - 1][c].
+//   dW[o][(r, s, c)] = sum over pixels (n, p, q) of dy[n][p][q][o] * x[n][p + r - 1][q + s - 1][c],
+// and the same kernel's 1x1 form (KH = 1: dW[o][c] = sum over pixels of dy[.][o] x[.][c],
+// steps of 64 consecutive pixels, no halo, chunks of up to 288 input channels).
 //
 // A block owns one tile of output channels (64 or 96 rows) by one chunk of input channels
 // (32, or 48 for inputs whose channel count is a multiple of 48 but not of 32) across all
@@ -65,15 +67,20 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 }
 
 // Tile geometry.  OB: 32-row output-channel blocks (tile of 32 OB channels); CK: input
-// channels per chunk; PR x PC: the pixel patch of one step; S: LDS stages.
-template <int OB, int CK, int PR, int PC, int S>
+// channels per chunk; PR x PC: the pixel patch of one step (1 x 64 for the 1x1 form); S:
+// LDS stages; KH: kernel side (3, or 1).
+template <int OB, int CK, int PR, int PC, int S, int KH>
 struct WhShape {
   static constexpr int NP = PR * PC;                // pixels per step
   static constexpr int KS = NP / 16;                // 16-pixel MFMA slices per step
   static constexpr int RB = OB * 64;                // bytes per staged dy pixel
-  static constexpr int HRB = CK * 2;                // bytes per staged input pixel
-  static constexpr int HW = PC + 2, HP = (PR + 2) * HW;  // halo width, halo pixels
-  static constexpr int CB = (9 * CK + 31) / 32;     // 32-column blocks over (tap, channel)
+  // bytes per staged input pixel: CK channels; in the 1x1 form padded so that four
+  // consecutive pixels start in distinct quarters of the 256-byte bank window
+  static constexpr int HRB0 = CK * 2;
+  static constexpr int HRB = KH == 3 ? HRB0 : HRB0 % 256 == 128 ? HRB0 + 64 : HRB0 % 256 == 32 ? HRB0 + 32 : HRB0;
+  static constexpr int HW = PC + KH - 1, HP = (PR + KH - 1) * HW;  // halo width, halo pixels
+  static constexpr int NCOL = KH * KH * CK;         // columns (tap, channel)
+  static constexpr int CB = (NCOL + 31) / 32;       // 32-column blocks
   static constexpr int T = OB * CB;                 // 32 x 32 blocks of the tile
   static constexpr int R = (T + 3) / 4;             // blocks per wave
   static constexpr int NCB = (OB + R - 2) / OB + 1; // column blocks one wave's run touches
@@ -83,19 +90,20 @@ struct WhShape {
   static constexpr int STAGE = 8 * LW * 1024;       // bytes per stage (every wave's load slots)
   static constexpr int PENDING = (S - 2) * LW;      // loads of the later stages in flight at a step's wait
   static constexpr int EPS = STAGE / 4096;          // accumulator blocks of a wave one stage holds
-  static_assert(NP % 16 == 0 && (PC == 4 || PC == 8 || PC == 16), "patch");
+  static_assert(KH == 3 ? (NP % 16 == 0 && (PC == 4 || PC == 8 || PC == 16)) : (KH == 1 && PR == 1 && NP % 16 == 0),
+                "patch");
   static_assert(NP * RB % 1024 == 0, "dy stage in whole load instructions");
   static_assert(RB == 128 || RB == 192, "dy row");
-  static_assert(CK == 32 || CK == 48, "channel chunk");
+  static_assert(KH == 3 ? (CK == 32 || CK == 48) : (CK % 16 == 0 && HRB % 16 == 0), "channel chunk");
   static_assert(R <= 7, "accumulator registers");
   static_assert(S >= 3 && S <= 6 && S * EPS >= 4 * R, "stages (they also hold the halves' exchange)");
   static_assert(S * STAGE <= 160 * 1024, "LDS");
   static_assert(PENDING <= 63, "load counter");
 };
 
-template <int OB, int CK, int PR, int PC, int S>
+template <int OB, int CK, int PR, int PC, int S, int KH>
 __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) {
-  using Sh = WhShape<OB, CK, PR, PC, S>;
+  using Sh = WhShape<OB, CK, PR, PC, S, KH>;
   constexpr int KS = Sh::KS, RB = Sh::RB, HRB = Sh::HRB, HW = Sh::HW, R = Sh::R, NCB = Sh::NCB;
   constexpr int LW = Sh::LW, NDY = Sh::NDY, NHA = Sh::NHA, T = Sh::T, CB = Sh::CB;
 
@@ -128,28 +136,32 @@ __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) 
   const int nsteps = pend > pbeg ? pend - pbeg : 0;
 
   // This lane's part of load slot u of its wave (instruction n = wave + 8 u of a stage):
-  // the byte offset of its 16 bytes from the step's base (kOobH: zeros) and, for a halo
-  // pixel, its position relative to the patch origin (the dy pixels are always inside).
+  // the byte offset of its 16 bytes from the step's base (kOobH: zeros) and the position of
+  // its pixel: for a halo pixel (row + 1) | (column + 1) << 16 relative to the patch origin
+  // (the dy pixels of a patch are always inside); in the 1x1 form the pixel's index within
+  // the step (the last step may pass the last pixel).
   uint32_t loff[LW];
-  uint32_t lpos[LW];  // (row + 1) | (column + 1) << 16 of the pixel relative to the patch origin
+  uint32_t lpos[LW];
 #pragma unroll
   for (int u = 0; u < LW; ++u) {
     const int n = wave + 8 * u;
     const int bl = n * 1024 + 16 * lane;
     loff[u] = kOobH;
-    lpos[u] = 1u | (1u << 16);
+    lpos[u] = KH == 3 ? (1u | (1u << 16)) : 0u;
     if (n < NDY) {
       const int pr = bl / RB, slot = (bl % RB) / 16;
       const int ch = RB == 128 ? (slot ^ (4 * ((pr >> 1) & 1))) : slot;  // 16-byte chunk (8 channels)
       const int o = o0 + 8 * ch;
       if (o < a.co) loff[u] = (uint32_t)(((pr / PC) * a.w + pr % PC) * (uint32_t)a.dy_pix * 2u + (uint32_t)o * 2u);
+      if constexpr (KH == 1) lpos[u] = (uint32_t)pr;
     } else if (n < NDY + NHA) {
       const int hb = bl - NDY * 1024;
       const int hp = hb / HRB, ch = (hb % HRB) / 16;
       const int hr = hp / HW, hc = hp % HW;
       const int c = c0 + 8 * ch;
-      if (hp < Sh::HP && c < a.ci) loff[u] = (uint32_t)((hr * a.w + hc) * (uint32_t)a.x_pix * 2u + (uint32_t)c * 2u);
-      lpos[u] = (uint32_t)hr | ((uint32_t)hc << 16);
+      if (hp < Sh::HP && 8 * ch < CK && c < a.ci)
+        loff[u] = (uint32_t)((hr * a.w + hc) * (uint32_t)a.x_pix * 2u + (uint32_t)c * 2u);
+      lpos[u] = KH == 3 ? ((uint32_t)hr | ((uint32_t)hc << 16)) : (uint32_t)hp;
     }
   }
 
@@ -158,22 +170,33 @@ __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) 
     unsigned char* Sg = stage(sc);
     const bool live = st < nsteps;
     int img = 0, p0 = 0, q0 = 0;
-    if (live) {
-      const uint32_t P = (uint32_t)(pbeg + st);
-      img = (int)fdiv(P, g.dppi);
-      const uint32_t rem = P - (uint32_t)img * (uint32_t)g.ppi;
-      const uint32_t pri = fdiv(rem, g.dpcols);
-      p0 = (int)pri * PR;
-      q0 = (int)(rem - pri * (uint32_t)g.pcols) * PC;
+    int64_t pix0 = 0;
+    if constexpr (KH == 3) {
+      if (live) {
+        const uint32_t P = (uint32_t)(pbeg + st);
+        img = (int)fdiv(P, g.dppi);
+        const uint32_t rem = P - (uint32_t)img * (uint32_t)g.ppi;
+        const uint32_t pri = fdiv(rem, g.dpcols);
+        p0 = (int)pri * PR;
+        q0 = (int)(rem - pri * (uint32_t)g.pcols) * PC;
+      }
+      pix0 = ((int64_t)img * a.h + p0) * a.w + q0;
+    } else {
+      pix0 = live ? (int64_t)(pbeg + st) * Sh::NP : 0;
     }
-    const int64_t pix0 = ((int64_t)img * a.h + p0) * a.w + q0;
     const __amdgpu_buffer_rsrc_t rd = hrsrc(a.dy + pix0 * a.dy_pix);
-    const __amdgpu_buffer_rsrc_t rx = hrsrc(a.x + (pix0 - a.w - 1) * a.x_pix);  // halo origin (p0 - 1, q0 - 1)
+    // the halo's origin (p0 - 1, q0 - 1); the step's first pixel in the 1x1 form
+    const __amdgpu_buffer_rsrc_t rx = hrsrc(a.x + (KH == 3 ? pix0 - a.w - 1 : pix0) * a.x_pix);
 #pragma unroll
     for (int u = 0; u < LW; ++u) {
       const int n = wave + 8 * u;
-      const int pr1 = (int)(lpos[u] & 0xffffu), pc1 = (int)(lpos[u] >> 16);
-      const bool inside = live && (unsigned)(p0 + pr1 - 1) < (unsigned)a.h && (unsigned)(q0 + pc1 - 1) < (unsigned)a.w;
+      bool inside;
+      if constexpr (KH == 3) {
+        const int pr1 = (int)(lpos[u] & 0xffffu), pc1 = (int)(lpos[u] >> 16);
+        inside = live && (unsigned)(p0 + pr1 - 1) < (unsigned)a.h && (unsigned)(q0 + pc1 - 1) < (unsigned)a.w;
+      } else {
+        inside = live && pix0 + (int64_t)lpos[u] < a.m;
+      }
       const uint32_t vo = inside ? loff[u] : kOobH;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(n < NDY ? rd : rx, (hlds_void_t*)(Sg + n * 1024), 16, vo, 0, 0, 0);
     }
@@ -200,10 +223,10 @@ __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) 
   // lane's half, or twice it), so the position is a lane constant plus a compile-time
   // offset.
   const int lrow = PC == 16 ? 0 : (PC == 8 ? (lane >> 5) : 2 * (lane >> 5));
-  const uint32_t lhalo = (uint32_t)((lm + 2 * lrow) * HRB);
+  const uint32_t lhalo = (uint32_t)((lm + (KH - 1) * lrow) * HRB);
   auto hoff = [&](uint32_t lb, int ks, int rd) __attribute__((always_inline)) -> uint32_t {
     const int b = 16 * ks + 4 * rd;
-    return lb + (uint32_t)((b + 2 * (b / PC)) * HRB);
+    return lb + (uint32_t)((b + (KH - 1) * (b / PC)) * HRB);
   };
   // this wave's run of blocks t = wq R .. wq R + R - 1 (block t: output block t % OB,
   // column block t / OB); the column blocks it touches start at cb_lo
@@ -213,9 +236,9 @@ __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) 
 #pragma unroll
   for (int i = 0; i < NCB; ++i) {
     int col = (cb_lo + i) * 32 + 16 * g16;
-    if (col > 9 * CK - 16) col = 9 * CK - 16;  // past the last tap: any valid pixel (the block is not stored)
+    if (col > Sh::NCOL - 16) col = Sh::NCOL - 16;  // past the last column: any valid pixel (the block is not stored)
     const int tap = col / CK, cc = col - tap * CK;
-    boff[i] = (uint32_t)(((tap / 3) * HW + tap % 3) * HRB + (cc + 4 * (j16 & 3)) * 2);
+    boff[i] = (uint32_t)(((tap / KH) * HW + tap % KH) * HRB + (cc + 4 * (j16 & 3)) * 2);
   }
 
   // The accumulators live in the accumulation registers: an operand naming that register
@@ -371,7 +394,7 @@ __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) 
     const int ob = t % OB, cb = t / OB;
     const int col = cb * 32 + (lane & 31);
     const int tap = col / CK, cc = col - tap * CK;
-    if (tap >= 9 || c0 + cc >= a.ci) continue;
+    if (tap >= KH * KH || c0 + cc >= a.ci) continue;
     const int k = tap * a.ci + c0 + cc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -386,15 +409,48 @@ __global__ __launch_bounds__(512) void wgrad_halo_kernel(WgradArgs a, WhGeom g) 
 }
 
 struct WhCfg {
-  int ob, ck, pr, pc;
+  int ob, ck, pr, pc, kh;
 };
+
+// the output-channel tile that pads c_out least, 96 rows on a tie
+int wh_ob(int co) {
+  const int pad2 = (co + 63) / 64 * 64 - co, pad3 = (co + 95) / 96 * 96 - co;
+  return pad3 <= pad2 ? 3 : 2;
+}
 
 // The configuration for a problem, or ob = 0 where the kernel does not apply.
 WhCfg wgrad_halo_cfg(const WgradArgs& a) {
-  WhCfg c{0, 0, 0, 0};
-  if (a.kh != 3 || a.kw != 3 || a.sh != 1 || a.sw != 1 || a.ph != 1 || a.pw != 1 || a.ho != a.h || a.wo != a.w)
-    return c;
+  WhCfg c{0, 0, 0, 0, 0};
+  if (a.ho != a.h || a.wo != a.w || a.sh != 1 || a.sw != 1) return c;
   if (a.co % 8 != 0 || a.x_pix % 8 != 0 || a.dy_pix % 8 != 0 || a.ci < 32) return c;
+#ifdef NUMBAT_TUNING
+  if (const char* e = getenv("NUMBAT_WH_OFF")) {
+    if (atoi(e)) return c;
+  }
+#endif
+  if (a.kh == 1 && a.kw == 1 && a.ph == 0 && a.pw == 0) {
+    // 1x1: steps of 64 consecutive pixels; the largest chunk of 288, 192, 144 or 96 input
+    // channels that divides c_in
+    int ck = 0;
+    for (const int k : {288, 192, 144, 96})
+      if (ck == 0 && a.ci % k == 0) ck = k;
+    if (ck == 0 || a.m >= (1ll << 36)) return c;
+#ifdef NUMBAT_TUNING
+    if (const char* e = getenv("NUMBAT_WH1_OFF")) {
+      if (atoi(e)) return c;
+    }
+    if (const char* e = getenv("NUMBAT_WH1_MAXCI")) {
+      if (a.ci > atoi(e)) return c;
+    }
+#endif
+    c.ob = wh_ob(a.co);
+    c.ck = ck;
+    c.pr = 1;
+    c.pc = 64;
+    c.kh = 1;
+    return c;
+  }
+  if (a.kh != 3 || a.kw != 3 || a.ph != 1 || a.pw != 1) return c;
   int ck = 0;
   if (a.ci % 32 == 0) ck = 32;
   else if (a.ci % 48 == 0) ck = 48;
@@ -407,40 +463,46 @@ WhCfg wgrad_halo_cfg(const WgradArgs& a) {
   // offsets within one image (plus its halo) are 32-bit
   const int64_t pix = a.x_pix > a.dy_pix ? a.x_pix : a.dy_pix;
   if (((int64_t)a.h * a.w + 2 * (int64_t)a.w + 2) * pix * 2 >= (1ll << 31) - (1ll << 24)) return c;
-  int ob = 2;
-  if (ck == 32) {  // the output-channel tile that pads c_out least, 96 rows on a tie
-    const int pad2 = (a.co + 63) / 64 * 64 - a.co, pad3 = (a.co + 95) / 96 * 96 - a.co;
-    ob = pad3 <= pad2 ? 3 : 2;
-  }
-#ifdef NUMBAT_TUNING
-  if (const char* e = getenv("NUMBAT_WH_OFF")) {
-    if (atoi(e)) return c;
-  }
-#endif
-  c.ob = ob;
+  c.ob = ck == 32 ? wh_ob(a.co) : 2;
   c.ck = ck;
   c.pr = pr;
   c.pc = pc;
+  c.kh = 3;
   return c;
 }
 
-template <int OB, int CK, int PR, int PC, int S>
+int64_t wh_npatch(const WgradArgs& a, const WhCfg& c) {
+  return c.kh == 1 ? (a.m + 63) / 64 : (int64_t)a.n * (a.h / c.pr) * (a.w / c.pc);
+}
+
+template <int OB, int CK, int PR, int PC, int S, int KH>
 hipError_t launch_wh(const WgradArgs& a, const WhGeom& g, dim3 grid, hipStream_t s) {
-  NUMBAT_LAUNCH((wgrad_halo_kernel<OB, CK, PR, PC, S>), grid, dim3(512), 0, s, a, g);
+  NUMBAT_LAUNCH((wgrad_halo_kernel<OB, CK, PR, PC, S, KH>), grid, dim3(512), 0, s, a, g);
   return hipGetLastError();
 }
 
+// stages: as many as the LDS holds with one block per CU (at least enough to hold the
+// halves' exchange)
 template <int OB, int CK>
 hipError_t launch_wh_patch(const WgradArgs& a, const WhCfg& c, const WhGeom& g, dim3 grid, hipStream_t s) {
-  // stages: as many as the LDS holds with one block per CU (at least enough to hold the
-  // halves' exchange)
 #ifdef NUMBAT_TUNING
-  if (c.pr == 8 && c.pc == 16 && getenv("NUMBAT_WH_S3")) return launch_wh<OB, CK, 8, 16, 3>(a, g, grid, s);
+  if (c.pr == 8 && c.pc == 16 && getenv("NUMBAT_WH_S3")) return launch_wh<OB, CK, 8, 16, 3, 3>(a, g, grid, s);
 #endif
-  if (c.pr == 8 && c.pc == 16) return launch_wh<OB, CK, 8, 16, 4>(a, g, grid, s);
-  if (c.pr == 20 && c.pc == 8) return launch_wh<OB, CK, 20, 8, 3>(a, g, grid, s);
-  if (c.pr == 20 && c.pc == 4) return launch_wh<OB, CK, 20, 4, (OB == 3 && CK == 32) ? 5 : 6>(a, g, grid, s);
+  if (c.pr == 8 && c.pc == 16) return launch_wh<OB, CK, 8, 16, 4, 3>(a, g, grid, s);
+  if (c.pr == 20 && c.pc == 8) return launch_wh<OB, CK, 20, 8, 3, 3>(a, g, grid, s);
+  if (c.pr == 20 && c.pc == 4) return launch_wh<OB, CK, 20, 4, (OB == 3 && CK == 32) ? 5 : 6, 3>(a, g, grid, s);
   return hipErrorInvalidValue;
+}
+
+template <int OB>
+hipError_t launch_wh_1x1(const WgradArgs& a, const WhCfg& c, const WhGeom& g, dim3 grid, hipStream_t s) {
+  switch (c.ck) {
+    case 288: return launch_wh<OB, 288, 1, 64, 3, 1>(a, g, grid, s);
+    case 192: return launch_wh<OB, 192, 1, 64, 4, 1>(a, g, grid, s);
+    case 144: return launch_wh<OB, 144, 1, 64, 5, 1>(a, g, grid, s);
+    case 96: return launch_wh<OB, 96, 1, 64, 6, 1>(a, g, grid, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
@@ -448,7 +510,7 @@ hipError_t launch_wh_patch(const WgradArgs& a, const WhCfg& c, const WhGeom& g, 
 bool wgrad_halo_plan(const WgradArgs& a, int* splits, int64_t* patches_per_split) {
   const WhCfg c = wgrad_halo_cfg(a);
   if (c.ob == 0) return false;
-  const int64_t npatch = (int64_t)a.n * (a.h / c.pr) * (a.w / c.pc);
+  const int64_t npatch = wh_npatch(a, c);
   if (npatch >= (1ll << 30)) return false;
   const int64_t tiles = (int64_t)((a.co + 32 * c.ob - 1) / (32 * c.ob)) * ((a.ci + c.ck - 1) / c.ck);
   // Blocks: about 160.  One block fills a CU (all of its LDS and registers), and the
@@ -464,7 +526,7 @@ bool wgrad_halo_plan(const WgradArgs& a, int* splits, int64_t* patches_per_split
   int64_t sp = tiles < slots ? slots / tiles : 1;
   if (sp > npatch) sp = npatch;
   // partials at most 64 MiB
-  const int64_t part_bytes = (int64_t)a.co * 9 * a.ci * 4;
+  const int64_t part_bytes = (int64_t)a.co * c.kh * c.kh * a.ci * 4;
   while (sp > 1 && sp * part_bytes > (64ll << 20)) --sp;
   const int64_t pps = (npatch + sp - 1) / sp;
   *patches_per_split = pps;
@@ -475,12 +537,12 @@ bool wgrad_halo_plan(const WgradArgs& a, int* splits, int64_t* patches_per_split
 hipError_t wgrad_halo_launch(const WgradArgs& args, hipStream_t s) {
   WgradArgs a = args;
   const WhCfg c = wgrad_halo_cfg(a);
-  if (c.ob == 0 || a.ktot != 9 * a.ci || a.rows_per_split < 1) return hipErrorInvalidValue;
+  if (c.ob == 0 || a.ktot != c.kh * c.kh * a.ci || a.rows_per_split < 1) return hipErrorInvalidValue;
   a.remap = 1;
   WhGeom g;
-  g.pcols = a.w / c.pc;
-  g.ppi = (a.h / c.pr) * g.pcols;
-  g.npatch = (int32_t)((int64_t)a.n * g.ppi);
+  g.pcols = c.kh == 3 ? a.w / c.pc : 1;
+  g.ppi = c.kh == 3 ? (a.h / c.pr) * g.pcols : 1;
+  g.npatch = (int32_t)wh_npatch(a, c);
   g.pps = (int32_t)a.rows_per_split;
   g.dppi = make_fastdiv((uint32_t)g.ppi);
   g.dpcols = make_fastdiv((uint32_t)g.pcols);
@@ -489,7 +551,8 @@ hipError_t wgrad_halo_launch(const WgradArgs& args, hipStream_t s) {
                   (unsigned)a.splits);
   trace_begin(KC_WGRAD);
   hipError_t e;
-  if (c.ck == 48) e = launch_wh_patch<2, 48>(a, c, g, grid, s);
+  if (c.kh == 1) e = c.ob == 3 ? launch_wh_1x1<3>(a, c, g, grid, s) : launch_wh_1x1<2>(a, c, g, grid, s);
+  else if (c.ck == 48) e = launch_wh_patch<2, 48>(a, c, g, grid, s);
   else if (c.ob == 3) e = launch_wh_patch<3, 32>(a, c, g, grid, s);
   else e = launch_wh_patch<2, 32>(a, c, g, grid, s);
   trace_end(KC_WGRAD);

@@ -206,10 +206,12 @@ bool wgrad_stem_shape(const WgradArgs& a);
 int wgrad_stem_blocks(const WgradArgs& a);
 hipError_t wgrad_stem_launch(const WgradArgs& a, float* part, hipStream_t s);
 // weight gradient of a 3x3, stride-1, padding-1 convolution staged by pixel patches (c_in a
-// multiple of 32 or 48, c_out of 8, pixel strides of 8, image sides the patch divides):
+// multiple of 32 or 48, c_out of 8, pixel strides of 8, image sides the patch divides), and
+// of a 1x1 stride-1 one in steps of 64 pixels (c_in a multiple of 96, 144, 192 or 288):
 // wgrad_halo_plan says whether it applies and fills in its split count and patches per
 // split; wgrad_halo_launch takes those in a.splits and a.rows_per_split and writes
-// partials [splits][c_out][9 c_in] to a.out when splits > 1, else dW (accumulate honoured)
+// partials [splits][c_out][kh kw c_in] to a.out when splits > 1, else dW (accumulate
+// honoured)
 struct WhGeom {
   int32_t pcols, ppi;   // patches per image row band, per image
   int32_t pps, npatch;  // patches per split, in all

@@ -103,6 +103,14 @@ CONV_CASES = [
     (2, 40, 12, 48, 40, 3, 1),
     (1, 8, 16, 96, 32, 3, 1),
     (4, 20, 8, 144, 64, 3, 1),
+    # its 1x1 form (steps of 64 pixels; the 13 x 11 and 9 x 7 cases above too): 144- and
+    # 192-channel chunks (input rows padded in LDS), five 192-channel chunks into four
+    # 96-row tiles, 100 steps split over many blocks, a ragged last step
+    (2, 16, 16, 144, 96, 1, 1),
+    (1, 20, 20, 384, 192, 1, 1),
+    (1, 10, 10, 960, 384, 1, 1),
+    (4, 40, 40, 288, 96, 1, 1),
+    (3, 7, 5, 192, 40, 1, 1),
 ]
 
 
