@@ -165,10 +165,13 @@ __device__ __forceinline__ float wave_sum(const float* r, int ld, int c) {
   else return s4 + ((r[4 * ld + c] + r[5 * ld + c]) + (r[6 * ld + c] + r[7 * ld + c]));
 }
 
+// `active` false: a wave that holds no accumulators of its own (the second half of a
+// block whose halves split the reduction) and only takes the block's barriers.
 template <int TM, int TN, int NW = 4>
 __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmPhase& P, const TileId& T,
                                               f32x16 (&acc)[TM][TN], int m0, int n0, unsigned char* smem,
-                                              const int64_t* s_dst, float (*s_red)[TN * 32], float* s_mean) {
+                                              const int64_t* s_dst, float (*s_red)[TN * 32], float* s_mean,
+                                              bool active = true) {
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   using S = GemmShape<TM, TN, NW>;
   constexpr int BM = S::BM, BN = S::BN, WTM = S::WTM;
@@ -188,7 +191,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
 #pragma unroll
         for (int r = 0; r < 16; ++r) s += acc[i][j][r];
       s += __shfl_xor(s, 32);
-      if (lane < 32) s_red[wave][j * 32 + lane] = s;
+      if (lane < 32 && active) s_red[wave][j * 32 + lane] = s;
     }
     __syncthreads();
     if (tid < BN) s_mean[tid] = wave_sum<NW>(&s_red[0][0], BN, tid) / (float)count;
@@ -206,7 +209,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
           q += (row < count) ? d * d : 0.f;
         }
       q += __shfl_xor(q, 32);
-      if (lane < 32) s_red[wave][j * 32 + lane] = q;
+      if (lane < 32 && active) s_red[wave][j * 32 + lane] = q;
     }
     __syncthreads();
     if (tid < BN && n0 + tid < a.nout) {
@@ -246,6 +249,7 @@ __device__ __forceinline__ void gemm_epilogue(const ConvGemmArgs& a, const GemmP
   };
 
   // ---- output
+  if (!active) return;  // (no block barrier follows)
   if ((a.nout & 7) == 0) {
     // stage 8 rows per wave in LDS as fp32 (register group g = r/4 of every 32-row block),
     // then write 16-byte vectors of 8 channels
@@ -1151,8 +1155,11 @@ struct HaloShape {
   static_assert(TC == 0 || (G::BM % TC == 0 && (TR + 2) * (TC + 2) <= HPAD), "2D tile and its halo");
 };
 
-template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC, bool PRO>
-__global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
+// KV = 2: eight waves in two halves of four; half 0 issues every load, half k multiplies
+// reduction slice k (16 channels) of every tap, and the halves add their sums through LDS
+// before the epilogue (twice the waves per SIMD to cover a step's latencies, same LDS).
+template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC, bool PRO, int KV>
+__global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
   using G = GemmShape<TM, TN, 4>;
   using Sh = HaloShape<TM, TN, HI, KT, SB, BT, TC>;
   constexpr int TR = Sh::TR;
@@ -1173,6 +1180,7 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   __shared__ float s_mean[BN];
   __shared__ float s_pro[PRO ? 2 * kProMaxC : 1];  // prologue: scale, then shift, per source channel
   static_assert(!(PRO && BT), "the prologue is a forward's");
+  static_assert(KV == 1 || KV == 2, "one or two reduction halves");
   auto hbuf = [&](auto hc) __attribute__((always_inline)) -> unsigned char* {
     if constexpr (decltype(hc)::value == 0) return sH0;
     else return sH1;
@@ -1193,7 +1201,9 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   const int m0 = T.mt * BM;
   const int n0 = T.nt * BN;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = KV == 2 ? (wv & 3) : wv;  // the wave's rows (and load slots)
+  const int kh = KV == 2 ? (wv >> 2) : 0;     // its reduction half
   const int l32 = lane & 31, half = lane >> 5;
   const int W = a.ws, H = a.hs, cs = a.cs, nout = a.nout;
   const int64_t pix2 = a.src_pix * 2;
@@ -1218,7 +1228,7 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   // prologue: the previous layer's BN constants of every source channel (published by
   // the barrier below, before any halo is transformed)
   if constexpr (PRO) {
-    for (int ch = tid; ch < cs; ch += NW * 64)
+    for (int ch = tid; ch < cs; ch += NW * 64 * KV)
       bn_fold(a.pro_gamma[ch], a.pro_beta[ch], a.pro_mean[ch], a.pro_var[ch], a.pro_eps, s_pro[ch],
               s_pro[kProMaxC + ch]);
     __syncthreads();
@@ -1284,6 +1294,7 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   const int nsteps = SPC * nchunk;
 
   auto issue_halo = [&](auto hc, int c) __attribute__((always_inline)) {
+    if (KV == 2 && kh != 0) return;
     unsigned char* Hb = hbuf(hc);
     const int cb = 32 * c;
 #pragma unroll
@@ -1295,6 +1306,7 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   };
   // weights of step s (chunk s / SPC, taps KT * (s % SPC) ..) into stage bc
   auto issue_b = [&](auto bc, int s) __attribute__((always_inline)) {
+    if (KV == 2 && kh != 0) return;
     unsigned char* Bb = bstage(bc);
     const int c = s / SPC, t0 = KT * (s - SPC * c), cb = 32 * c;
     const bool live = s < nsteps;
@@ -1375,10 +1387,12 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // multiply one tap (t, within the step's stage at tap slot tk) from halo buffer hc
-  auto compute_tap = [&](const unsigned char* Hb, const unsigned char* Bb, auto tc) __attribute__((always_inline)) {
-    constexpr int t = decltype(tc)::value;
+  auto compute_tap = [&](const unsigned char* Hb, const unsigned char* Bb, auto tc, auto khc)
+                         __attribute__((always_inline)) {
+    constexpr int t = decltype(tc)::value, KH = decltype(khc)::value;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
+      if (KV == 2 && ks != KH) continue;  // (compile-time after unrolling)
       u32x4 af[TM], bf[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const u32x4*>(Hb + (aaddr[i][t] ^ (uint32_t)(32 * ks)));
@@ -1415,6 +1429,7 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   // this covers them) become the previous layer's activations, SiLU(BN(y)), in place;
   // chunks that loaded zeros (padding, past the image or the channels) stay zero
   auto transform = [&](auto hc, int c) __attribute__((always_inline)) {
+    if (KV == 2 && kh != 0) return;  // (the chunks are half 0's loads)
     unsigned char* Hb = hbuf(hc);
     const int cb = 32 * c;
 #pragma unroll
@@ -1434,7 +1449,7 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
   };
   // step k (0 .. SPC-1) of a chunk c of parity h (halo buffer h): wait, issue the next
   // halo (k = 0) and the weights D steps ahead, multiply the step's KT taps
-  auto step = [&](auto hc, auto kc, int c) __attribute__((always_inline)) {
+  auto step = [&](auto hc, auto kc, int c, auto khc) __attribute__((always_inline)) {
     constexpr int h = decltype(hc)::value, k = decltype(kc)::value;
     constexpr int sl = h * SPC + k;  // step index within the two-chunk trip
     constexpr int waitn = (D - 1) * BI_MIN + ((k >= 1 && k <= D - 1) ? HI : 0);
@@ -1453,25 +1468,25 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
 #pragma unroll
     for (int tt = 0; tt < KT; ++tt) {
       // (compile-time tap index: KT * k + tt)
-      if constexpr (KT == 1) compute_tap(Hb, Bb, Ic<k>{});
+      if constexpr (KT == 1) compute_tap(Hb, Bb, Ic<k>{}, khc);
       else {
-        if (tt == 0) compute_tap(Hb, Bb, Ic<3 * k + 0>{});
-        if (tt == 1) compute_tap(Hb, Bb + TBYTES, Ic<3 * k + 1>{});
-        if (tt == 2) compute_tap(Hb, Bb + 2 * TBYTES, Ic<3 * k + 2>{});
+        if (tt == 0) compute_tap(Hb, Bb, Ic<3 * k + 0>{}, khc);
+        if (tt == 1) compute_tap(Hb, Bb + TBYTES, Ic<3 * k + 1>{}, khc);
+        if (tt == 2) compute_tap(Hb, Bb + 2 * TBYTES, Ic<3 * k + 2>{}, khc);
       }
     }
   };
-  auto chunk = [&](auto hc, int c) __attribute__((always_inline)) {
-    step(hc, Ic<0>{}, c);
-    step(hc, Ic<1>{}, c);
-    step(hc, Ic<2>{}, c);
+  auto chunk = [&](auto hc, int c, auto khc) __attribute__((always_inline)) {
+    step(hc, Ic<0>{}, c, khc);
+    step(hc, Ic<1>{}, c, khc);
+    step(hc, Ic<2>{}, c, khc);
     if constexpr (SPC == 9) {
-      step(hc, Ic<3>{}, c);
-      step(hc, Ic<4>{}, c);
-      step(hc, Ic<5>{}, c);
-      step(hc, Ic<6>{}, c);
-      step(hc, Ic<7>{}, c);
-      step(hc, Ic<8>{}, c);
+      step(hc, Ic<3>{}, c, khc);
+      step(hc, Ic<4>{}, c, khc);
+      step(hc, Ic<5>{}, c, khc);
+      step(hc, Ic<6>{}, c, khc);
+      step(hc, Ic<7>{}, c, khc);
+      step(hc, Ic<8>{}, c, khc);
     }
   };
 
@@ -1486,15 +1501,52 @@ __global__ __launch_bounds__(256) void convhalo_kernel(ConvGemmArgs a) {
     const int m = TC > 0 ? (img2 * H + h0 + r / (TC > 0 ? TC : 1)) * W + w0 + r % (TC > 0 ? TC : 1) : m0 + r;
     s_dst[r] = dst_offset(a, Ge, m);
   }
-  int c = 0;
-  for (; c + 2 <= nchunk; c += 2) {
-    chunk(Ic<0>{}, c);
-    chunk(Ic<1>{}, c + 1);
-  }
-  if (c < nchunk) chunk(Ic<0>{}, c);
+  // the main loop, one copy per reduction half (a compile-time slice choice)
+  auto main_loop = [&](auto khc) __attribute__((always_inline)) {
+    int c = 0;
+    for (; c + 2 <= nchunk; c += 2) {
+      chunk(Ic<0>{}, c, khc);
+      chunk(Ic<1>{}, c + 1, khc);
+    }
+    if (c < nchunk) chunk(Ic<0>{}, c, khc);
+  };
+  if (KV == 1 || kh == 0) main_loop(Ic<0>{});
+  else main_loop(Ic<1>{});
   // the loads issued past the last step land before the halo buffer becomes staging space
   asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-  gemm_epilogue<TM, TN, NW>(a, P, T, acc, m0, n0, sH0, s_dst, s_red, s_mean);
+  if constexpr (KV == 2) {
+    // half 1 hands its sums to half 0, one 32 x 32 block of each wave at a time through
+    // halo buffer 0 (16 KiB: 4 waves x 64 lanes x 16 floats); the sum is half 0 + half 1
+    f32x4* xb = reinterpret_cast<f32x4*>(sH0);
+    static_assert(Sh::H0BYTES >= 4 * 64 * 64, "exchange space");
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        if (kh == 1) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            f32x4 v;
+            v[0] = acc[i][j][4 * q];
+            v[1] = acc[i][j][4 * q + 1];
+            v[2] = acc[i][j][4 * q + 2];
+            v[3] = acc[i][j][4 * q + 3];
+            xb[(wave * 4 + q) * 64 + lane] = v;
+          }
+        }
+        __syncthreads();
+        if (kh == 0) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = xb[(wave * 4 + q) * 64 + lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+          }
+        }
+        __syncthreads();
+      }
+  }
+  gemm_epilogue<TM, TN, NW>(a, P, T, acc, m0, n0, sH0, s_dst, s_red, s_mean, kh == 0);
 }
 
 template <int TN>
@@ -1611,12 +1663,28 @@ hipError_t launch_h(const ConvGemmArgs& a, hipStream_t s) {
     constexpr HInst c = kH[I];
     using G = GemmShape<c.tm, c.tn, 4>;
     dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
+    // 128-row tiles: two reduction halves (eight waves; at two blocks per CU their
+    // registers fit; the first halo buffer holds their exchange); 256-row tiles keep four
+    // waves
+    constexpr int KV = (c.tm == 1 && HaloShape<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc>::H0BYTES >= 4 * 64 * 64) ? 2 : 1;
+    const dim3 block(256 * KV);
+#ifdef NUMBAT_TUNING
+    if (KV == 2 && getenv("NUMBAT_HALO_KV1")) {
+      if (a.bt)
+        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, false, 1>), grid, dim3(256), 0, s, a);
+      else if (a.pro_mean != nullptr)
+        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, true, 1>), grid, dim3(256), 0, s, a);
+      else
+        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, false, 1>), grid, dim3(256), 0, s, a);
+      return hipGetLastError();
+    }
+#endif
     if (a.bt)
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, false>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, false, KV>), grid, block, 0, s, a);
     else if (a.pro_mean != nullptr)
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, true>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, true, KV>), grid, block, 0, s, a);
     else
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, false>), grid, dim3(256), 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, false, KV>), grid, block, 0, s, a);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
