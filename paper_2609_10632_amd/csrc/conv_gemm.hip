@@ -2,23 +2,31 @@
 //
 // Computes the GEMM family described with ConvGemmArgs: the forward convolution (one
 // phase) and all stride phases of a data gradient (one launch, blockIdx.z = phase).
-// Three kernels:
+// Kernels:
 //  * convdma_kernel, for source channel counts that are multiples of 16 and at least 32
 //    (every layer of the detector but the image input): both operands reach LDS through
-//    loads that write LDS directly, in 2 or 3 stages;
+//    loads that write LDS directly, in 2 or 3 stages (up to 6 supported);
+//  * convhalo_kernel, 3x3 stride-1 padding-1 forwards and data gradients: the input halo
+//    of a tile is staged once per 32-channel chunk and all nine taps read out of it
+//    (linear tiles, or two-dimensional tiles of one image), optionally with the previous
+//    layer's BN + SiLU applied to the staged halo (the prologue form);
 //  * convgemm_kernel, for any other channel count that is a multiple of 8 (and tiles
 //    whose address span exceeds 31 bits): each wave loads its own MFMA A fragments (16
 //    contiguous bytes per lane) from global memory into a register ring several steps
 //    deep; only the weight tile B, shared by the four waves, goes through LDS;
-//  * convnarrow_kernel, forward only, for fewer than 8 channels (the RGB image): the
+//  * convstem_kernel, the RGB image layer's forward (3 channels, 3x3, stride 2): a patch's
+//    input pixels staged once in LDS;
+//  * convnarrow_kernel, forward only, for other inputs of fewer than 8 channels: the
 //    reduction (tap, channel) is packed densely and gathered element by element.  Every row keeps a
 //    pointer to its source pixel and a bitmask of the taps that land inside the image;
 //    padding lanes read a zero constant, so every step issues the same loads and waits
 //    are counted exactly.
-// All use 32x32x16 MFMAs (the full-rate bf16 form on gfx950) with 4 waves split along M,
-// and share one epilogue: optional per-tile batch-statistics partials, then fp32 results
-// staged through LDS and written as 16-byte vectors of 8 channels (bf16, rounded once,
-// after the optional accumulate).
+// All use 32x32x16 MFMAs (the full-rate bf16 form on gfx950) with 4 waves split along M
+// (an 8-wave direct-to-LDS variant takes 256-row tiles; the halo kernel's 128-row tiles
+// run as two halves of four waves that split the reduction), and share one epilogue:
+// optional per-tile batch-statistics partials, then fp32 results staged through LDS and
+// written as 16-byte vectors of 8 channels (bf16, rounded once, after the optional
+// accumulate, and the inference post-op where asked).
 #include <cstdlib>
 #include <type_traits>
 

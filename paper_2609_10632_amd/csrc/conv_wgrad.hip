@@ -1,5 +1,8 @@
 // Weight gradient dW[o][k] = sum_m dy[m][o] * X[m][k] on gfx950 MFMA, where m runs over
-// the n*ho*wo output pixels and X[m][(tap, c)] is the input pixel that tap reads.
+// the n*ho*wo output pixels and X[m][(tap, c)] is the input pixel that tap reads: the
+// general kernel (every shape; the 3x3 stride-1 and 1x1 layers whose sizes suit it take
+// the patch-staged kernel of conv_wgrad_halo.hip instead), the image layer's kernel and the
+// split reduction.
 //
 // In NHWC both operands are contiguous along o / k and strided along the reduction
 // dimension m, while an MFMA lane needs 8 consecutive reduction elements.  The loads
