@@ -72,7 +72,9 @@ typedef enum {
   NUMBAT_OP_CONV_BWD_WEIGHT = 2,
   NUMBAT_OP_BN_SILU_FWD = 3,
   NUMBAT_OP_BN_SILU_BWD = 4,
-  NUMBAT_OP_CLIP_SGD_NESTEROV = 5 /* problem ignored (may be NULL) */
+  NUMBAT_OP_CLIP_SGD_NESTEROV = 5, /* problem ignored (may be NULL) */
+  NUMBAT_OP_CONV_BWD_DATA_BN_SILU = 6 /* numbat_conv_bwd_data_bn_silu_prologue: 0 bytes, or
+                                         NUMBAT_ERR_UNSUPPORTED for a problem it does not take */
 } numbat_op;
 
 /* One 2-D convolution (dilation 1, one group).  Output size
@@ -200,6 +202,29 @@ numbat_status numbat_conv_fwd_noalloc(const numbat_conv_problem* p, const void* 
 numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
                                    int accumulate, void* ws, size_t ws_bytes, void* stream);
 
+/* The data gradient with this layer's BN + SiLU backward applied inside its operand
+ * staging: the backward half of fusing the element-wise work around a kernel into it
+ * (Sec. 3.1, the fusion templates' pre/post element-wise stages).  For a 3x3 stride-1 pad-1
+ * convolution whose output y went through numbat_bn_silu_fwd, given g = dL/d(out) and the
+ * dgamma, dbeta that numbat_bn_silu_bwd formed (it may be called with dy = NULL for that):
+ *   dy = gamma * save_rstd * (dz - dbeta / m - xhat * dgamma / m)   (numbat_bn_silu_bwd's dy)
+ *   dx = the data gradient of dy                                       (numbat_conv_bwd_data's)
+ * with m = n * ho * wo.  dy is formed once per element from g and y as the kernel stages
+ * its input halo and is also written out (bf16), for the weight gradient; dx and dy equal
+ * numbat_bn_silu_bwd followed by numbat_conv_bwd_data bit for bit.
+ * g: bf16 [n,ho,wo,c_out] with g_pixel_stride (0 means c_out); y and dy: bf16 with the
+ * problem's y_pixel_stride; dx: bf16 with x_pixel_stride, accumulate as numbat_conv_bwd_data;
+ * save_mean, save_rstd, gamma, beta, dgamma, dbeta: fp32 [c_out].  g, y, dy, dx 16-byte
+ * aligned with pixel strides multiples of 8.  No workspace.  Returns NUMBAT_ERR_UNSUPPORTED
+ * unless the problem is 3x3, stride 1, padding 1, c_out a multiple of 16 in 32 .. 1024,
+ * c_in a multiple of 8, on an image the halo kernel takes (numbat_workspace_size with
+ * NUMBAT_OP_CONV_BWD_DATA_BN_SILU answers that without a launch). */
+numbat_status numbat_conv_bwd_data_bn_silu_prologue(const numbat_conv_problem* p, const void* g,
+                                                    int64_t g_pixel_stride, const void* y, const float* save_mean,
+                                                    const float* save_rstd, const float* gamma, const float* beta,
+                                                    const float* dgamma, const float* dbeta, const void* w, void* dx,
+                                                    void* dy, int accumulate, void* stream);
+
 /* Weight gradient of the forward convolution (its adjoint in w), fp32 (gradients of the
  * fp32 master weights, Table 1 precision row):
  *   dw[o,r,s,c] = sum_{n,p,q} dy[n,p,q,o] * x[n, p*stride_h - pad_h + r, q*stride_w - pad_w + s, c].
@@ -243,7 +268,9 @@ numbat_status numbat_bn_silu_infer(const numbat_bn_problem* p, const void* y, co
  *   dbeta = sum_rows dz,  dgamma = sum_rows dz * xhat                      (fp32 [c])
  *   dy = gamma * save_rstd * (dz - dbeta / m - xhat * dgamma / m)            (bf16, RNE)
  * residual_grad: NULL, or bf16 [m][c] (r_pixel_stride) that receives += g, the gradient of
- * a residual added in the forward.  g, y, dy: bf16 with their pixel strides. */
+ * a residual added in the forward.  g, y, dy: bf16 with their pixel strides.  dy NULL: only
+ * dgamma and dbeta are formed (for numbat_conv_bwd_data_bn_silu_prologue, which forms dy
+ * itself); residual_grad must then be NULL. */
 numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, const void* y,
                                  const float* save_mean, const float* save_rstd, const float* gamma,
                                  const float* beta, void* dy, float* dgamma, float* dbeta, void* residual_grad,

@@ -209,6 +209,13 @@ TileCfg prologue_tile(const ConvDesc& d) {
   return convhalo_pick(d.m, d.co, d.h, d.w, false, true);
 }
 
+// the data gradient with the BN + SiLU backward prologue: the halo kernel's tile for the
+// problem (kVariantGeneric when the kernel does not take it)
+TileCfg bwd_prologue_tile(const ConvDesc& d) {
+  if (d.co > kProMaxC || narrow(d)) return TileCfg{0, 0, -1, kVariantGeneric};
+  return halo_tile(d, d.co, d.ci, true);
+}
+
 // per-tile statistics partials, sized for the forward's tile and the prologue-fused
 // forward's (one workspace serves both)
 size_t fwd_stats_bytes(const ConvDesc& d) {
@@ -342,7 +349,7 @@ size_t bn_fwd_ws(const BnDesc& d) {
 
 size_t bn_bwd_ws(const BnDesc& d) {
   const int nb = bn_reduce_blocks(d.a.m, d.a.c);
-  return round_up((size_t)nb * d.a.c * sizeof(float2), 256) + round_up(3 * d.a.c * sizeof(float), 256);
+  return round_up((size_t)nb * d.a.c * sizeof(float2), 256);
 }
 
 numbat_status check_ws(void* ws, size_t have, size_t need) {
@@ -421,6 +428,7 @@ numbat_status conv_fwd_launch(const ConvDesc& d, const void* x, const void* w, v
   g.post_mean = post.mean;
   g.post_var = post.var;
   if (pro) {
+    g.pro_kind = kProFwd;
     g.pro_gamma = pro->gamma;
     g.pro_beta = pro->beta;
     g.pro_mean = pro->mean;
@@ -570,6 +578,15 @@ numbat_status numbat_workspace_size(numbat_op op, const void* problem, size_t* b
     case NUMBAT_OP_CLIP_SGD_NESTEROV:
       *bytes = with_header(round_up((size_t)kOptBlocks * sizeof(double), 256));
       return ok();
+    case NUMBAT_OP_CONV_BWD_DATA_BN_SILU: {
+      ConvDesc d;
+      numbat_status st = check_conv(static_cast<const numbat_conv_problem*>(problem), &d);
+      if (st != NUMBAT_OK) return st;
+      if (bwd_prologue_tile(d).variant != kVariantHalo)
+        return fail(NUMBAT_ERR_UNSUPPORTED, "the BN + SiLU backward prologue does not take this problem");
+      *bytes = 0;
+      return ok();
+    }
     case NUMBAT_OP_BN_SILU_FWD:
     case NUMBAT_OP_BN_SILU_BWD: {
       BnDesc d;
@@ -673,6 +690,40 @@ numbat_status numbat_conv_bn_silu_infer(const numbat_conv_problem* p, const void
   return conv_fwd_launch(d, x, w, y, nullptr, nullptr, stream, op);
 }
 
+// a 3x3 stride-1 data gradient is the forward convolution of dy (src, pixel stride src_pix)
+// with the flipped, transposed weights, which the halo kernel reads in place
+static ConvGemmArgs halo_dgrad_args(const ConvDesc& d, const void* src, int64_t src_pix, const void* w, void* dx,
+                                    int accumulate) {
+  ConvGemmArgs g;
+  std::memset(&g, 0, sizeof g);
+  g.src = static_cast<const bf16_t*>(src);
+  g.src_pix = src_pix;
+  g.hs = d.ho;
+  g.ws = d.wo;
+  g.cs = d.co;
+  g.nout = d.ci;
+  g.nimg = d.n;
+  g.gstride_h = g.gstride_w = 1;
+  g.dst = static_cast<bf16_t*>(dx);
+  g.dst_pix = d.x_pix;
+  g.hd = d.h;
+  g.wd = d.w;
+  g.dstep_h = g.dstep_w = 1;
+  g.accumulate = accumulate ? 1 : 0;
+  g.nphase = 1;
+  g.bt = 1;
+  GemmPhase& P = g.ph[0];
+  P.wt = static_cast<const bf16_t*>(w);
+  P.taps = 9;
+  P.ktot = 9 * d.co;
+  P.gh = d.h;
+  P.gw = d.w;
+  P.m = (int32_t)((int64_t)d.n * d.h * d.w);
+  P.div_gw = make_fastdiv((uint32_t)d.w);
+  P.div_ghw = make_fastdiv((uint32_t)(d.h * d.w));
+  return g;
+}
+
 numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy, const void* w, void* dx,
                                    int accumulate, void* ws, size_t ws_bytes, void* stream) {
   ConvDesc d;
@@ -716,35 +767,7 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
 
   const TileCfg ht = halo_tile(d, d.co, d.ci, true);
   if (ht.variant == kVariantHalo) {
-    // a 3x3 stride-1 data gradient is the forward convolution of dy with the flipped,
-    // transposed weights, which the halo kernel reads in place
-    ConvGemmArgs g;
-    std::memset(&g, 0, sizeof g);
-    g.src = static_cast<const bf16_t*>(dy);
-    g.src_pix = d.y_pix;
-    g.hs = d.ho;
-    g.ws = d.wo;
-    g.cs = d.co;
-    g.nout = d.ci;
-    g.nimg = d.n;
-    g.gstride_h = g.gstride_w = 1;
-    g.dst = static_cast<bf16_t*>(dx);
-    g.dst_pix = d.x_pix;
-    g.hd = d.h;
-    g.wd = d.w;
-    g.dstep_h = g.dstep_w = 1;
-    g.accumulate = accumulate ? 1 : 0;
-    g.nphase = 1;
-    g.bt = 1;
-    GemmPhase& P = g.ph[0];
-    P.wt = static_cast<const bf16_t*>(w);
-    P.taps = 9;
-    P.ktot = 9 * d.co;
-    P.gh = d.h;
-    P.gw = d.w;
-    P.m = (int32_t)((int64_t)d.n * d.h * d.w);
-    P.div_gw = make_fastdiv((uint32_t)d.w);
-    P.div_ghw = make_fastdiv((uint32_t)(d.h * d.w));
+    ConvGemmArgs g = halo_dgrad_args(d, dy, d.y_pix, w, dx, accumulate);
     e = convhalo_launch(g, ht, s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
     return ok();
@@ -869,6 +892,50 @@ numbat_status numbat_conv_bwd_data(const numbat_conv_problem* p, const void* dy,
     e = convgemm_launch(groups[i], tiles[i], s, KC_CONV_DGRAD);
     if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
   }
+  return ok();
+}
+
+numbat_status numbat_conv_bwd_data_bn_silu_prologue(const numbat_conv_problem* p, const void* g,
+                                                    int64_t g_pixel_stride, const void* y, const float* save_mean,
+                                                    const float* save_rstd, const float* gamma, const float* beta,
+                                                    const float* dgamma, const float* dbeta, const void* w, void* dx,
+                                                    void* dy, int accumulate, void* stream) {
+  ConvDesc d;
+  numbat_status st = check_conv(p, &d);
+  if (st != NUMBAT_OK) return st;
+  if (g == nullptr || y == nullptr || w == nullptr || dx == nullptr || dy == nullptr)
+    return fail(NUMBAT_ERR_NULL, "g, y, w, dx and dy are required");
+  if (save_mean == nullptr || save_rstd == nullptr || gamma == nullptr || beta == nullptr || dgamma == nullptr ||
+      dbeta == nullptr)
+    return fail(NUMBAT_ERR_NULL, "save_mean, save_rstd, gamma, beta, dgamma and dbeta are required");
+  const int64_t g_pix = g_pixel_stride == 0 ? d.co : g_pixel_stride;
+  if (g_pix < d.co) return fail(NUMBAT_ERR_BAD_DESC, "g_pixel_stride %lld < c_out %d", (long long)g_pix, d.co);
+  if (bwd_prologue_tile(d).variant != kVariantHalo)
+    return fail(NUMBAT_ERR_UNSUPPORTED,
+                "the BN + SiLU backward prologue takes 3x3 stride-1 pad-1 problems with c_out a multiple of 16 in "
+                "32 .. %d on images the halo kernel takes (%dx%d, c_out %d)", kProMaxC, d.ho, d.wo, d.co);
+  if (!aligned16(g) || !aligned16(y) || !aligned16(dy) || !aligned16(dx) || g_pix % 8 != 0 || d.y_pix % 8 != 0)
+    return fail(NUMBAT_ERR_ALIGN, "g, y, dy and dx must be 16-byte aligned with pixel strides multiples of 8");
+  if (reinterpret_cast<uintptr_t>(w) & 1u) return fail(NUMBAT_ERR_ALIGN, "w must be 2-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(save_mean) | reinterpret_cast<uintptr_t>(save_rstd) |
+       reinterpret_cast<uintptr_t>(gamma) | reinterpret_cast<uintptr_t>(beta) | reinterpret_cast<uintptr_t>(dgamma) |
+       reinterpret_cast<uintptr_t>(dbeta)) & 3u)
+    return fail(NUMBAT_ERR_ALIGN, "save_mean, save_rstd, gamma, beta, dgamma and dbeta must be 4-byte aligned");
+  ConvGemmArgs a = halo_dgrad_args(d, g, g_pix, w, dx, accumulate);
+  a.pro_kind = kProBwd;
+  a.pro_gamma = gamma;
+  a.pro_beta = beta;
+  a.pro_mean = save_mean;
+  a.pro_rstd = save_rstd;
+  a.pro_dgamma = dgamma;
+  a.pro_dbeta = dbeta;
+  a.pro_y = static_cast<const bf16_t*>(y);
+  a.pro_y_pix = d.y_pix;
+  a.pro_dy = static_cast<bf16_t*>(dy);
+  a.pro_dy_pix = d.y_pix;
+  a.pro_m = d.m;
+  const hipError_t e = convhalo_launch(a, bwd_prologue_tile(d), static_cast<hipStream_t>(stream), KC_CONV_DGRAD);
+  if (e != hipSuccess) return hip_fail(e, "data-gradient launch");
   return ok();
 }
 
@@ -1041,20 +1108,21 @@ numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, cons
   numbat_status st = check_bn(p, &d);
   if (st != NUMBAT_OK) return st;
   if (g == nullptr || y == nullptr || save_mean == nullptr || save_rstd == nullptr || gamma == nullptr ||
-      beta == nullptr || dy == nullptr || dgamma == nullptr || dbeta == nullptr)
-    return fail(NUMBAT_ERR_NULL, "g, y, save_mean, save_rstd, gamma, beta, dy, dgamma and dbeta are required");
-  if (!aligned16(g) || !aligned16(y) || !aligned16(dy) || (residual_grad && !aligned16(residual_grad)))
+      beta == nullptr || dgamma == nullptr || dbeta == nullptr)
+    return fail(NUMBAT_ERR_NULL, "g, y, save_mean, save_rstd, gamma, beta, dgamma and dbeta are required");
+  if (dy == nullptr && residual_grad != nullptr)
+    return fail(NUMBAT_ERR_NULL, "residual_grad needs dy (without dy only dgamma and dbeta are formed)");
+  if (!aligned16(g) || !aligned16(y) || (dy && !aligned16(dy)) || (residual_grad && !aligned16(residual_grad)))
     return fail(NUMBAT_ERR_ALIGN, "g, y, dy and residual_grad must be 16-byte aligned");
   st = check_ws(ws, ws_bytes, with_header(bn_bwd_ws(d)));
   if (st != NUMBAT_OK) return st;
   ws = ws_body(ws);
   const int nb = bn_reduce_blocks(d.a.m, d.a.c);
   float* part = static_cast<float*>(ws);
-  float* coef = reinterpret_cast<float*>(static_cast<char*>(ws) + round_up((size_t)nb * d.a.c * sizeof(float2), 256));
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = bn_bwd_launch(d.a, static_cast<const bf16_t*>(g), static_cast<const bf16_t*>(y), save_mean, save_rstd,
                                gamma, beta, static_cast<bf16_t*>(dy), dgamma, dbeta, static_cast<bf16_t*>(residual_grad),
-                               part, nb, coef, s);
+                               part, nb, s);
   if (e != hipSuccess) return hip_fail(e, "BN+SiLU backward launch");
   return ok();
 }

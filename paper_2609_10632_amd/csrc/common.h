@@ -108,6 +108,29 @@ __device__ __forceinline__ float bn_silu_apply(float y, float sc, float sh) {
   return z * sigmoidf_fast(z);
 }
 
+// The backward of the above with batch statistics, for one element, as multiply-adds with
+// per-channel folded constants.  With a = gamma rstd, xhat = (y - mean) rstd:
+//   z  = y a + b,  b = beta - mean a                  (the forward's z)
+//   dz = g sigmoid(z) (1 + z (1 - sigmoid(z)))
+//   dy = a (dz - dbeta / m - xhat dgamma / m) = a dz + (y c + d),
+//        c = -a rstd dgamma / m,  d = -a dbeta / m - mean c
+// The BN backward kernel and the data gradient's prologue both use these, so they form
+// bit-identical dy.
+__device__ __forceinline__ void bn_bwd_fold(float gamma, float beta, float mean, float rstd, float dgamma,
+                                            float dbeta, int64_t m, float& a, float& b, float& c, float& d) {
+  a = gamma * rstd;
+  b = beta - mean * a;
+  const float gm = (float)((double)dgamma / (double)m), bm = (float)((double)dbeta / (double)m);
+  c = -(a * rstd) * gm;
+  d = -(a * bm) - mean * c;
+}
+__device__ __forceinline__ float bn_silu_bwd_apply(float g, float y, float a, float b, float c, float d) {
+  const float z = __builtin_fmaf(y, a, b);
+  const float sg = sigmoidf_fast(z);
+  const float dz = g * sg * (1.0f + z * (1.0f - sg));
+  return __builtin_fmaf(a, dz, __builtin_fmaf(y, c, d));
+}
+
 // Workgroups are dealt round-robin to the 8 XCDs (linear id L runs on XCD L % 8), and
 // each XCD has its own L2.  Tiles that read the same data should share an XCD, so a
 // kernel whose consecutive logical tiles share data maps its linear id to the logical

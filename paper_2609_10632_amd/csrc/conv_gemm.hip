@@ -1161,19 +1161,33 @@ struct HaloShape {
   // (TR + 2) x (TC + 2) pixels fits the buffer
   static constexpr int TR = TC > 0 ? G::BM / TC : 0;
   static_assert(TC == 0 || (G::BM % TC == 0 && (TR + 2) * (TC + 2) <= HPAD), "2D tile and its halo");
+  // waves of the plain kernel: 128-row tiles take two reduction halves of four waves (the
+  // first halo buffer holds their exchange), 256-row tiles four waves
+  static constexpr int KV = (TM == 1 && H0BYTES >= 4 * 64 * 64) ? 2 : 1;
 };
 
 // KV = 2: eight waves in two halves of four; half 0 issues every load, half k multiplies
 // reduction slice k (16 channels) of every tap, and the halves add their sums through LDS
 // before the epilogue (twice the waves per SIMD to cover a step's latencies, same LDS).
-template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC, bool PRO, int KV>
+//
+// PRO (kProFwd, kProBwd): an element-wise prologue on each 32-channel chunk of the staged
+// halo, once per element, before any tap reads it; its per-channel constants sit in dynamic
+// LDS (2 or 4 floats per source channel, sized at launch), and the loading lanes transform
+// their own chunks between their load wait and the barrier.  kProBwd (the data gradient,
+// four waves): the halo holds g, each lane also loads y for its own halo chunks (into
+// registers, a chunk ahead), and dy = BN + SiLU backward (g, y) replaces g in place; dy of
+// the tile's own pixels is also stored (first column tile only).
+template <int TM, int TN, int HI, int KT, int SB, bool BT, int TC, int PRO, int KV>
 __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
   using G = GemmShape<TM, TN, 4>;
   using Sh = HaloShape<TM, TN, HI, KT, SB, BT, TC>;
   constexpr int TR = Sh::TR;
   constexpr int BM = G::BM, BN = G::BN, WTM = G::WTM, NW = 4, SPC = Sh::SPC, D = SB - 1;
   constexpr int BI = Sh::BI, BI_MIN = Sh::BI_MIN, BI_MAX = Sh::BI_MAX, TBYTES = Sh::TBYTES;
-  static_assert((D - 1) * BI_MIN + HI <= 60, "load counter range");
+  // memory operations a chunk's first step issues besides the weights: the next halo, and
+  // with the backward prologue also the chunk's dy stores and the next chunk's y loads
+  constexpr int XB = PRO == kProBwd ? 3 * HI : HI;
+  static_assert((D - 1) * BI_MIN + XB <= 60, "load counter range");
 
   __shared__ __attribute__((aligned(16))) unsigned char sH0[Sh::H0BYTES];
   __shared__ __attribute__((aligned(16))) unsigned char sH1[Sh::HBYTES];
@@ -1186,8 +1200,10 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
   __shared__ int64_t s_dst[BM];
   __shared__ float s_red[NW][BN];
   __shared__ float s_mean[BN];
-  __shared__ float s_pro[PRO ? 2 * kProMaxC : 1];  // prologue: scale, then shift, per source channel
-  static_assert(!(PRO && BT), "the prologue is a forward's");
+  // prologue constants, [2 or 4][cs]: forward scale, shift; backward a, b, c, d (bn_bwd_fold)
+  extern __shared__ __attribute__((aligned(16))) float s_pro[];
+  static_assert(PRO != kProFwd || !BT, "the BN + SiLU prologue is a forward's");
+  static_assert(PRO != kProBwd || (BT && KV == 1), "the BN + SiLU backward prologue: a data gradient, four waves");
   static_assert(KV == 1 || KV == 2, "one or two reduction halves");
   auto hbuf = [&](auto hc) __attribute__((always_inline)) -> unsigned char* {
     if constexpr (decltype(hc)::value == 0) return sH0;
@@ -1233,12 +1249,16 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
     *reinterpret_cast<u32x4*>(sH0 + Sh::HPAD * 64 + tid * 16) = u32x4{0u, 0u, 0u, 0u};
     *reinterpret_cast<u32x4*>(sH1 + Sh::HPAD * 64 + tid * 16) = u32x4{0u, 0u, 0u, 0u};
   }
-  // prologue: the previous layer's BN constants of every source channel (published by
-  // the barrier below, before any halo is transformed)
-  if constexpr (PRO) {
+  // prologue: the BN constants of every source channel (published by the barrier below,
+  // before any halo is transformed)
+  if constexpr (PRO == kProFwd) {
     for (int ch = tid; ch < cs; ch += NW * 64 * KV)
-      bn_fold(a.pro_gamma[ch], a.pro_beta[ch], a.pro_mean[ch], a.pro_var[ch], a.pro_eps, s_pro[ch],
-              s_pro[kProMaxC + ch]);
+      bn_fold(a.pro_gamma[ch], a.pro_beta[ch], a.pro_mean[ch], a.pro_var[ch], a.pro_eps, s_pro[ch], s_pro[cs + ch]);
+    __syncthreads();
+  } else if constexpr (PRO == kProBwd) {
+    for (int ch = tid; ch < cs; ch += NW * 64 * KV)
+      bn_bwd_fold(a.pro_gamma[ch], a.pro_beta[ch], a.pro_mean[ch], a.pro_rstd[ch], a.pro_dgamma[ch],
+                  a.pro_dbeta[ch], a.pro_m, s_pro[ch], s_pro[cs + ch], s_pro[2 * cs + ch], s_pro[3 * cs + ch]);
     __syncthreads();
   }
 
@@ -1269,6 +1289,32 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
       hc8[q] = ok ? lc * 8 : (1 << 20);
     }
   }
+  // backward prologue: byte offset of the lane's chunk of halo instruction q in a tensor of
+  // pixel stride pix (relative to that tensor's halo base pixel; valid where hoff[q] is),
+  // and whether its pixel is one of the tile's own output pixels (the halo's interior)
+  auto chunk_off = [&](int q, int64_t pix) __attribute__((always_inline)) -> uint32_t {
+    const int j = (q * NW + wave) * 16 + (lane >> 2);
+    const int lc = (lane & 3) ^ ((j >> 2) & 3);
+    if constexpr (TC > 0) {
+      const int hr = j / (TC + 2), hcol = j - hr * (TC + 2);
+      return (uint32_t)(((int64_t)hr * W + hcol) * pix * 2 + lc * 16);
+    } else {
+      return (uint32_t)(j * pix * 2 + lc * 16);
+    }
+  };
+  auto interior = [&](int q) __attribute__((always_inline)) -> bool {
+    const int j = (q * NW + wave) * 16 + (lane >> 2);
+    if constexpr (TC > 0) {
+      const int hr = j / (TC + 2), hcol = j - hr * (TC + 2);
+      return hr >= 1 && hr <= TR && hcol >= 1 && hcol <= TC;
+    } else {
+      return j >= W + 1 && j < W + 1 + BM;
+    }
+  };
+  const __amdgpu_buffer_rsrc_t rsY = buffer_rsrc(PRO == kProBwd ? a.pro_y + hbase_px * a.pro_y_pix : a.src);
+  const __amdgpu_buffer_rsrc_t rsD = buffer_rsrc(PRO == kProBwd ? a.pro_dy + hbase_px * a.pro_dy_pix : a.dst);
+  u32x4 yv[PRO == kProBwd ? HI : 1];  // y of the lane's chunks of the next chunk to transform
+
   // ---- weight loads: instruction u of a step covers 1 KiB of tap u / (BI / KT)'s stage
   const __amdgpu_buffer_rsrc_t rsB = buffer_rsrc(P.wt);
   constexpr int BPT = BN / 16;  // load instructions per tap
@@ -1393,6 +1439,19 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  // the backward prologue on a tile whose plain kernel has two reduction halves: the second
+  // 16-channel slice of every step goes to accumulators of its own, added last, so the sums
+  // (and dx) equal the plain kernel's bit for bit
+  constexpr bool SPLIT = PRO == kProBwd && Sh::KV == 2;
+  f32x16 acc2[SPLIT ? TM : 1][SPLIT ? TN : 1];
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc2[i][j][r] = 0.f;
+  }
 
   // multiply one tap (t, within the step's stage at tap slot tk) from halo buffer hc
   auto compute_tap = [&](const unsigned char* Hb, const unsigned char* Bb, auto tc, auto khc)
@@ -1426,17 +1485,93 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) {
+          if constexpr (SPLIT) {
+            if (ks == 0) acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
+            else acc2[SPLIT ? i : 0][SPLIT ? j : 0] = mfma32x32x16(af[i], bf[j], acc2[SPLIT ? i : 0][SPLIT ? j : 0]);
+          } else {
+            acc[i][j] = mfma32x32x16(af[i], bf[j], acc[i][j]);
+          }
+        }
     }
   };
   // wait for this wave's loads of the step (N later loads stay in flight), then every wave's
   auto sync = [&](auto nc) __attribute__((always_inline)) {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(decltype(nc)::value) : "memory");
   };
+  // backward prologue: y of this lane's chunks of chunk c, into registers (zeros past the
+  // channels and outside the image)
+  auto issue_y = [&](int c) __attribute__((always_inline)) {
+    if constexpr (PRO == kProBwd) {
+      const int cb = 32 * c;
+#pragma unroll
+      for (int q = 0; q < HI; ++q) {
+        const uint32_t v = (hoff[q] != kOob && cb + hc8[q] < cs) ? chunk_off(q, a.pro_y_pix) : kOob;
+        yv[q] = __builtin_amdgcn_raw_buffer_load_b128(rsY, v, (uint32_t)(cb * 2), 0);
+      }
+    }
+  };
+  // backward prologue: the chunks of chunk c's halo that halo wave `wave` loaded (landed
+  // and visible) become dy in place, from g there and y in yv.  A lane's chunks are the same
+  // 8 channels for every halo instruction (slot (lane & 3) ^ ((lane >> 4) & 3)); they are
+  // done in two passes of 4 channels, each with its 16 constants in registers (the
+  // accumulators stay live, so the working set is kept small), the second pass storing the
+  // whole chunk.  One dy store per halo instruction, issued by every wave whatever its
+  // lanes hold (out of range where the chunk is not the tile's own pixel, or in another
+  // column tile's block), so the wave's count of memory operations is fixed.
+  auto transform_bwd = [&](auto hc, int c) __attribute__((always_inline)) {
+    unsigned char* Hb = hbuf(hc);
+    const int cb = 32 * c;
+    const int c8 = 8 * ((lane & 3) ^ ((lane >> 4) & 3));
+    const int ch = cb + c8 < cs ? cb + c8 : 0;
+#pragma unroll
+    for (int ps = 0; ps < 2; ++ps) {
+      float ka[4], kb[4], kc[4], kd[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ka[e] = s_pro[ch + 4 * ps + e];
+        kb[e] = s_pro[cs + ch + 4 * ps + e];
+        kc[e] = s_pro[2 * cs + ch + 4 * ps + e];
+        kd[e] = s_pro[3 * cs + ch + 4 * ps + e];
+      }
+#pragma unroll
+      for (int q = 0; q < HI; ++q) {
+        const bool live = hoff[q] != kOob && cb + hc8[q] < cs;
+        unsigned char* p = Hb + (q * NW + wave) * 1024 + lane * 16;
+        // pass 0: the first 4 channels; pass 1: the last 4, with the first 4 as pass 0 left them
+        u32x4 v;
+        if (ps == 0) {
+          const uint2 h = *reinterpret_cast<const uint2*>(p);
+          v = u32x4{h.x, h.y, 0u, 0u};
+        } else {
+          v = *reinterpret_cast<const u32x4*>(p);
+        }
+        const uint32_t g0 = v[2 * ps], g1 = v[2 * ps + 1];
+        const uint32_t y0 = yv[q][2 * ps], y1 = yv[q][2 * ps + 1];
+        const float o0 = bn_silu_bwd_apply(bf2f(g0 & 0xffffu), bf2f(y0 & 0xffffu), ka[0], kb[0], kc[0], kd[0]);
+        const float o1 = bn_silu_bwd_apply(bf2f(g0 >> 16), bf2f(y0 >> 16), ka[1], kb[1], kc[1], kd[1]);
+        const float o2 = bn_silu_bwd_apply(bf2f(g1 & 0xffffu), bf2f(y1 & 0xffffu), ka[2], kb[2], kc[2], kd[2]);
+        const float o3 = bn_silu_bwd_apply(bf2f(g1 >> 16), bf2f(y1 >> 16), ka[3], kb[3], kc[3], kd[3]);
+        const uint2 oh = make_uint2(pack2(o0, o1), pack2(o2, o3));
+        if (live) *reinterpret_cast<uint2*>(p + 8 * ps) = oh;
+        if (ps == 1) {
+          const uint32_t so = (live && T.nt == 0 && interior(q)) ? chunk_off(q, a.pro_dy_pix) : kOob;
+          __builtin_amdgcn_raw_buffer_store_b128(u32x4{v[0], v[1], oh.x, oh.y}, rsD, so, (uint32_t)(cb * 2), 0);
+          // wait states before anything rewrites the store's data registers: with the
+          // scheduling barrier right after it, the compiler issued a VALU write to the first
+          // data register on the next cycle, and about one 16-byte store in 20000 then wrote
+          // that register's new value (measured; none with this pause)
+          asm volatile("s_nop 4");
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
   // prologue: this lane's own 16-byte chunks of chunk c's halo (landed: the wait before
   // this covers them) become the previous layer's activations, SiLU(BN(y)), in place;
   // chunks that loaded zeros (padding, past the image or the channels) stay zero
   auto transform = [&](auto hc, int c) __attribute__((always_inline)) {
+    if constexpr (PRO != kProFwd) return;
     if (KV == 2 && kh != 0) return;  // (the chunks are half 0's loads)
     unsigned char* Hb = hbuf(hc);
     const int cb = 32 * c;
@@ -1449,7 +1584,7 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
         unpack8(uint4{v[0], v[1], v[2], v[3]}, f);
         const int ch = cb + hc8[q];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = bn_silu_apply(f[e], s_pro[ch + e], s_pro[kProMaxC + ch + e]);
+        for (int e = 0; e < 8; ++e) f[e] = bn_silu_apply(f[e], s_pro[ch + e], s_pro[cs + ch + e]);
         const uint4 o = pack8(f);
         *p = u32x4{o.x, o.y, o.z, o.w};
       }
@@ -1460,12 +1595,19 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
   auto step = [&](auto hc, auto kc, int c, auto khc) __attribute__((always_inline)) {
     constexpr int h = decltype(hc)::value, k = decltype(kc)::value;
     constexpr int sl = h * SPC + k;  // step index within the two-chunk trip
-    constexpr int waitn = (D - 1) * BI_MIN + ((k >= 1 && k <= D - 1) ? HI : 0);
-    if constexpr (PRO && k == 0) {
+    constexpr int waitn = (D - 1) * BI_MIN + ((k >= 1 && k <= D - 1) ? XB : 0);
+    if constexpr (PRO == kProFwd && k == 0) {
       // the chunk's halo has landed for this wave: transform this lane's part, then publish
       asm volatile("s_waitcnt vmcnt(%0)" ::"n"(waitn) : "memory");
       transform(hc, c);
       asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    } else if constexpr (PRO == kProBwd && k == 0) {
+      // as the forward's (the wait also covers this chunk's y, loaded before its halo), then
+      // this wave's y loads of the next chunk
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(waitn) : "memory");
+      transform_bwd(hc, c);
+      asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+      issue_y(c + 1);
     } else {
       sync(Ic<waitn>{});
     }
@@ -1498,6 +1640,7 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
     }
   };
 
+  issue_y(0);  // (before the halo, as at every chunk's first step)
   issue_halo(Ic<0>{}, 0);
   issue_b(Ic<0>{}, 0);
   if constexpr (D >= 2) issue_b(Ic<1>{}, 1);
@@ -1553,6 +1696,14 @@ __global__ __launch_bounds__(256 * KV) void convhalo_kernel(ConvGemmArgs a) {
         }
         __syncthreads();
       }
+  }
+  if constexpr (SPLIT) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += acc2[SPLIT ? i : 0][SPLIT ? j : 0][r];
   }
   gemm_epilogue<TM, TN, NW>(a, P, T, acc, m0, n0, sH0, s_dst, s_red, s_mean, kh == 0);
 }
@@ -1671,28 +1822,35 @@ hipError_t launch_h(const ConvGemmArgs& a, hipStream_t s) {
     constexpr HInst c = kH[I];
     using G = GemmShape<c.tm, c.tn, 4>;
     dim3 grid((unsigned)((a.ph[0].m + G::BM - 1) / G::BM), (unsigned)((a.nout + G::BN - 1) / G::BN), 1);
-    // 128-row tiles: two reduction halves (eight waves; at two blocks per CU their
-    // registers fit; the first halo buffer holds their exchange); 256-row tiles keep four
-    // waves
-    constexpr int KV = (c.tm == 1 && HaloShape<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc>::H0BYTES >= 4 * 64 * 64) ? 2 : 1;
+    constexpr int KV = HaloShape<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc>::KV;
+    // the backward prologue keeps four waves: its y registers and transform do not fit the
+    // eight-wave form's 128 registers per lane
     const dim3 block(256 * KV);
+    // the prologue's per-channel constants (dynamic LDS, sized to the channels so that the
+    // blocks per CU stay those of the plain kernel wherever the channels allow)
+    const size_t fwd_smem = (size_t)2 * a.cs * sizeof(float), bwd_smem = (size_t)4 * a.cs * sizeof(float);
 #ifdef NUMBAT_TUNING
-    if (KV == 2 && getenv("NUMBAT_HALO_KV1")) {
+    if (KV == 2 && getenv("NUMBAT_HALO_KV1") && a.pro_kind != kProBwd) {
       if (a.bt)
-        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, false, 1>), grid, dim3(256), 0, s, a);
-      else if (a.pro_mean != nullptr)
-        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, true, 1>), grid, dim3(256), 0, s, a);
+        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, kProNone, 1>), grid, dim3(256), 0, s, a);
+      else if (a.pro_kind == kProFwd)
+        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, kProFwd, 1>), grid, dim3(256),
+                      fwd_smem, s, a);
       else
-        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, false, 1>), grid, dim3(256), 0, s, a);
+        NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, kProNone, 1>), grid, dim3(256), 0, s, a);
       return hipGetLastError();
     }
 #endif
-    if (a.bt)
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, false, KV>), grid, block, 0, s, a);
-    else if (a.pro_mean != nullptr)
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, true, KV>), grid, block, 0, s, a);
+    if (a.bt && a.pro_kind == kProBwd)
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, kProBwd, 1>), grid, dim3(256), bwd_smem,
+                    s, a);
+    else if (a.bt)
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, true, c.tc, kProNone, KV>), grid, block, 0, s, a);
+    else if (a.pro_kind == kProFwd)
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, kProFwd, KV>), grid, block, fwd_smem, s,
+                    a);
     else
-      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, false, KV>), grid, block, 0, s, a);
+      NUMBAT_LAUNCH((convhalo_kernel<c.tm, c.tn, c.hi, c.kt, c.sb, false, c.tc, kProNone, KV>), grid, block, 0, s, a);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -1978,7 +2136,10 @@ TileCfg convhalo_pick(int64_t m, int nout, int h, int w, bool bt, bool any_grid)
 
 hipError_t convhalo_launch(const ConvGemmArgs& a, const TileCfg& t, hipStream_t s, int cls) {
   if (t.variant != kVariantHalo || t.id < 0 || t.id >= kNumH || !convhalo_shape(a)) return hipErrorInvalidValue;
-  if (a.pro_mean != nullptr && (a.bt || a.cs > kProMaxC)) return hipErrorInvalidValue;
+  if (a.pro_kind == kProFwd && (a.bt || a.cs > kProMaxC || a.pro_mean == nullptr)) return hipErrorInvalidValue;
+  if (a.pro_kind == kProBwd && (!a.bt || a.cs > kProMaxC || a.pro_y == nullptr || a.pro_dy == nullptr))
+    return hipErrorInvalidValue;
+  if (a.pro_kind != kProNone && a.pro_kind != kProFwd && a.pro_kind != kProBwd) return hipErrorInvalidValue;
   const HInst& c = kH[t.id];
   if (c.hi * 64 < halo_pixels(t.bm, c.tc, a.ws)) return hipErrorInvalidValue;
   // a two-dimensional tile must divide the image (every tile whole)

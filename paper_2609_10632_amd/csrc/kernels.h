@@ -117,13 +117,26 @@ struct ConvGemmArgs {
   float post_eps;
   const float* post_bias;
   const float *post_gamma, *post_beta, *post_mean, *post_var;
-  // prologue (halo kernel, forward): with pro_mean set, the source is the previous layer's
-  // pre-BN output, and its BN (batch statistics pro_mean / pro_var, pro_gamma, pro_beta,
-  // pro_eps) + SiLU is applied to the staged halo before the taps read it
+  // prologue (halo kernel), pro_kind:
+  //  kProNone
+  //  kProFwd (forward): the source is the previous layer's pre-BN output, and its BN (batch
+  //    statistics pro_mean / pro_var, pro_gamma, pro_beta, pro_eps) + SiLU is applied to the
+  //    staged halo before the taps read it
+  //  kProBwd (data gradient): the source is g = dL/d(activation) of this layer's BN + SiLU,
+  //    and the staged halo becomes dy = that backward of (g, pro_y) with the batch statistics
+  //    pro_mean / pro_rstd, pro_gamma, pro_beta and the reduced pro_dgamma / pro_dbeta over
+  //    pro_m rows; dy of every tile's own pixels is also written to pro_dy (the first column
+  //    tile's blocks write it)
+  int32_t pro_kind;
   const float *pro_gamma, *pro_beta, *pro_mean, *pro_var;
   float pro_eps;
+  const float *pro_rstd, *pro_dgamma, *pro_dbeta;
+  const bf16_t* pro_y;
+  bf16_t* pro_dy;
+  int64_t pro_y_pix, pro_dy_pix, pro_m;
   GemmPhase ph[kMaxPhases];
 };
+enum { kProNone = 0, kProFwd = 1, kProBwd = 2 };
 constexpr int kProMaxC = 1024;  // most source channels the prologue stages constants for
 enum { kPostNone = 0, kPostBias = 1, kPostBnSilu = 2 };
 // tile and kernel for a problem with at most m_max rows per phase, nout columns, cs
@@ -234,9 +247,10 @@ hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int n
 hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, const float* var, const float* gamma,
                          const float* beta, const bf16_t* res, bf16_t* out, float* save_mean, float* save_rstd,
                          float* run_mean, float* run_var, hipStream_t s);
+// dy == nullptr: the reduce and finalize only (dgamma, dbeta), no apply
 hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,
                          const float* save_rstd, const float* gamma, const float* beta, bf16_t* dy, float* dgamma,
-                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, float* coef, hipStream_t s);
+                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, hipStream_t s);
 
 // SPPF max pool (5x5, stride 1, padding 2) and nearest 2x upsampling (pool.hip): n, h, w
 // of the pooled / low-resolution tensor, c channels (a multiple of 8), pixel strides of x

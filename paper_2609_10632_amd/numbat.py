@@ -19,7 +19,8 @@ LIB_PATH = os.environ.get("NUMBAT_LIB") or os.path.join(HERE, "libnumbat_conv.so
 NUMBAT_ABI_VERSION = 1
 
 OK, ERR_NULL, ERR_BAD_DESC, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE, ERR_DEVICE, ERR_VERSION = range(8)
-OP_CONV_FWD, OP_CONV_BWD_DATA, OP_CONV_BWD_WEIGHT, OP_BN_SILU_FWD, OP_BN_SILU_BWD, OP_CLIP_SGD_NESTEROV = range(6)
+(OP_CONV_FWD, OP_CONV_BWD_DATA, OP_CONV_BWD_WEIGHT, OP_BN_SILU_FWD, OP_BN_SILU_BWD, OP_CLIP_SGD_NESTEROV,
+ OP_CONV_BWD_DATA_BN_SILU) = range(7)
 
 EXPORTED = (
     "numbat_abi_version", "numbat_last_error", "numbat_status_string", "numbat_conv_output_shape",
@@ -28,7 +29,7 @@ EXPORTED = (
     "numbat_timing_enable", "numbat_timing_read", "numbat_conv_fwd_noalloc", "numbat_clip_sgd_nesterov",
     "numbat_conv_fwd_bias", "numbat_conv_bn_silu_infer", "numbat_bn_silu_infer",
     "numbat_maxpool5_fwd", "numbat_maxpool5_bwd", "numbat_upsample2x_fwd", "numbat_upsample2x_bwd",
-    "numbat_conv_fwd_bn_silu_prologue",
+    "numbat_conv_fwd_bn_silu_prologue", "numbat_conv_bwd_data_bn_silu_prologue",
 )
 
 
@@ -103,6 +104,8 @@ def load() -> ctypes.CDLL:
             "numbat_clip_sgd_nesterov": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(numbat_sgd_group),
                                                          ctypes.c_int32, ctypes.c_float, ctypes.c_float, P, P, S, P]),
             "numbat_conv_bwd_data": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
+            "numbat_conv_bwd_data_bn_silu_prologue": (ctypes.c_int, [CP, P, ctypes.c_int64, P, P, P, P, P, P, P, P, P,
+                                                                     P, ctypes.c_int, P]),
             "numbat_conv_bwd_weight": (ctypes.c_int, [CP, P, P, P, ctypes.c_int, P, S, P]),
             "numbat_bn_silu_fwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
             "numbat_bn_silu_bwd": (ctypes.c_int, [BP, P, P, P, P, P, P, P, P, P, P, P, S, P]),
@@ -257,6 +260,15 @@ def numbat_conv_bwd_data(p, dy, w, dx, accumulate=False, ws=None, stream=None, w
     _check(load().numbat_conv_bwd_data(ctypes.byref(p), _ptr(dy), _ptr(w), _ptr(dx), int(bool(accumulate)), _ptr(ws),
                                        _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
            "numbat_conv_bwd_data")
+
+
+def numbat_conv_bwd_data_bn_silu_prologue(p, g, y, save_mean, save_rstd, gamma, beta, dgamma, dbeta, w, dx, dy,
+                                          accumulate=False, g_pixel_stride=0, stream=None):
+    _check(load().numbat_conv_bwd_data_bn_silu_prologue(ctypes.byref(p), _ptr(g), int(g_pixel_stride), _ptr(y),
+                                                        _ptr(save_mean), _ptr(save_rstd), _ptr(gamma), _ptr(beta),
+                                                        _ptr(dgamma), _ptr(dbeta), _ptr(w), _ptr(dx), _ptr(dy),
+                                                        int(bool(accumulate)), _stream(stream)),
+           "numbat_conv_bwd_data_bn_silu_prologue")
 
 
 def numbat_conv_bwd_weight(p, x, dy, dw, accumulate=False, ws=None, stream=None, ws_bytes=None):

@@ -21,7 +21,7 @@ def declared_functions():
 def test_library_exports_every_declared_symbol():
     lib = nb.load()
     names = declared_functions()
-    assert len(names) == 24
+    assert len(names) == 25
     assert set(names) == set(nb.EXPORTED)
     for name in names:
         assert getattr(lib, name) is not None
@@ -242,3 +242,43 @@ def test_prologue_forward_refuses_before_any_launch():
         with pytest.raises(nb.NumbatError) as ei:
             nb.numbat_conv_fwd_bn_silu_prologue(p, fake, fake, fake, fake, 1e-3, fake, fake)
         assert ei.value.status == nb.ERR_UNSUPPORTED, p
+
+
+def test_prologue_backward_refuses_before_any_launch():
+    """The data gradient with the BN + SiLU backward prologue checks its arguments and takes
+    only the problems the 3x3 stride-1 halo kernel takes (the workspace query answers the
+    same), all before touching a GPU; the BN backward without dy takes no residual."""
+    fake = 1 << 20
+    ok = nb.conv_problem(2, 16, 16, 64, 32, 3)
+    f = nb.numbat_conv_bwd_data_bn_silu_prologue
+    assert nb.numbat_workspace_size(nb.OP_CONV_BWD_DATA_BN_SILU, ok) == 0
+    with pytest.raises(nb.NumbatError) as ei:
+        f(ok, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, None)
+    assert ei.value.status == nb.ERR_NULL
+    with pytest.raises(nb.NumbatError) as ei:
+        f(ok, fake, fake, fake, fake, fake, fake, None, fake, fake, fake, fake)
+    assert ei.value.status == nb.ERR_NULL
+    with pytest.raises(nb.NumbatError) as ei:
+        f(ok, fake + 8, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake)
+    assert ei.value.status == nb.ERR_ALIGN
+    with pytest.raises(nb.NumbatError) as ei:
+        f(ok, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, g_pixel_stride=36)
+    assert ei.value.status == nb.ERR_ALIGN
+    with pytest.raises(nb.NumbatError) as ei:
+        f(ok, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, g_pixel_stride=16)
+    assert ei.value.status == nb.ERR_BAD_DESC
+    for p in (nb.conv_problem(2, 16, 16, 64, 32, 1),           # 1x1
+              nb.conv_problem(2, 16, 16, 64, 32, 3, stride=2),  # stride 2
+              nb.conv_problem(2, 16, 16, 64, 24, 3),           # c_out not a multiple of 16
+              nb.conv_problem(2, 16, 16, 64, 16, 3),           # c_out below 32
+              nb.conv_problem(1, 8, 8, 64, 2048, 3),           # c_out above 1024
+              nb.conv_problem(1, 40, 200, 64, 32, 3)):         # 200 wide: neither halo tiling
+        with pytest.raises(nb.NumbatError) as ei:
+            f(p, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake)
+        assert ei.value.status == nb.ERR_UNSUPPORTED, p
+        with pytest.raises(nb.NumbatError) as ei:
+            nb.numbat_workspace_size(nb.OP_CONV_BWD_DATA_BN_SILU, p)
+        assert ei.value.status == nb.ERR_UNSUPPORTED, p
+    b = nb.bn_problem(2048, 32)
+    assert status_of(nb.numbat_bn_silu_bwd, b, fake, fake, fake, fake, fake, fake, None, fake, fake, fake) \
+        == nb.ERR_NULL
