@@ -55,6 +55,10 @@ def parse():
                          "one cross-stream wait (each wait costs the main queue a completion signal)")
     ap.add_argument("--wgrad-tail", type=int, default=0,
                     help="the last this many layers of the backward pass are enqueued one by one")
+    ap.add_argument("--fuse-bwd", action="store_true",
+                    help="the 3x3 stride-1 layers form dy inside their data gradient (the BN + SiLU backward "
+                         "prologue) instead of a separate BN backward apply pass; slower on this GPU, off by "
+                         "default")
     ap.add_argument("--layers", type=str, default=None, help="comma-separated layer names (subset)")
     ap.add_argument("--detail", type=str, default=None,
                     help="write per-layer x pass timings (JSON) to this file, and a markdown table beside it")
@@ -190,10 +194,13 @@ def chain_mode(torch, steps, warmup):
 
 
 def prologue_fusion(torch, steps):
-    """A C2f bottleneck's second conv fed by its first conv's pre-BN output, at batch 16:
-    the previous layer's BN + SiLU as its own pass (writes the activation) followed by the
-    forward, against the prologue-fused forward that forms the activation in the conv's
-    operand staging (both with batch statistics, graph-replayed on one stream)."""
+    """Prologue fusion on the C2f bottleneck convs at batch 16, graph-replayed on one stream.
+    fwd: the second conv fed by the first's pre-BN output -- the first's BN + SiLU as its own
+    pass (writes the activation) followed by the forward, against the prologue-fused forward
+    that forms the activation in the conv's operand staging (both with batch statistics).
+    bwd: a conv's BN + SiLU backward (reduce, finalize, apply writing dy) followed by its data
+    gradient, against the BN backward without dy followed by the data gradient that forms dy
+    in its operand staging and writes it."""
     from paper_2609_10632_amd import blocks
     from paper_2609_10632_amd import numbat as nb
 
@@ -220,15 +227,32 @@ def prologue_fusion(torch, steps):
         def fused():
             nb.numbat_conv_fwd_bn_silu_prologue(blk.prob, yp, prev, ga, be, 1e-3, w, y, st, ws)
 
-        res = {}
-        for k, f in (("unfused_ms", unfused), ("fused_ms", fused)):
-            for _ in range(3):
-                f()
-            gr = graph_of(torch, f)
-            res[k] = round(time_replays(torch, gr, max(20, steps)), 4)
-            del gr
-        res["saved_ms"] = round(res["unfused_ms"] - res["fused_ms"], 4)
-        out[name] = res
+        gb = torch.randn((n, h, h, c), device="cuda", generator=g).to(torch.bfloat16)
+        dy = torch.empty_like(gb)
+        dx = torch.empty_like(gb)
+        dg, db = torch.empty(c, device="cuda"), torch.empty(c, device="cuda")
+        wsb = blocks.workspace(max(blk.ws_dgrad, nb.numbat_workspace_size(nb.OP_BN_SILU_BWD, bnp)))
+        nb.numbat_bn_silu_fwd(bnp, yp, None, ga, be, None, act, sm, sr, ws=blocks.workspace(blk.ws_bytes()))
+
+        def unfused_bwd():
+            nb.numbat_bn_silu_bwd(bnp, gb, yp, sm, sr, ga, be, dy, dg, db, None, ws=wsb)
+            nb.numbat_conv_bwd_data(blk.prob, dy, w, dx, False, wsb)
+
+        def fused_bwd():
+            nb.numbat_bn_silu_bwd(bnp, gb, yp, sm, sr, ga, be, None, dg, db, None, ws=wsb)
+            nb.numbat_conv_bwd_data_bn_silu_prologue(blk.prob, gb, yp, sm, sr, ga, be, dg, db, w, dx, dy)
+
+        out[name] = {}
+        for part, uf, ff in (("fwd", unfused, fused), ("bwd", unfused_bwd, fused_bwd)):
+            res = {}
+            for k, f in (("unfused_ms", uf), ("fused_ms", ff)):
+                for _ in range(3):
+                    f()
+                gr = graph_of(torch, f)
+                res[k] = round(time_replays(torch, gr, max(20, steps)), 4)
+                del gr
+            res["saved_ms"] = round(res["unfused_ms"] - res["fused_ms"], 4)
+            out[name][part] = res
     return out
 
 
@@ -304,15 +328,18 @@ def write_detail(torch, args, step, layers, wl):
     """Per layer x pass: median of five serial steps' HIP-event times (launch gaps included),
     with each pass's algorithmic work against the roofline that binds it: conv passes 2 M N K
     FLOPs and their operand bytes (fwd x + W + y, dgrad dy + W + dx in bf16, wgrad x + dy in
-    bf16 + dW in fp32); BN passes 4 (fwd) and 10 (bwd) bytes per element.  JSON to
+    bf16 + dW in fp32); BN passes 4 (fwd) and 10 (bwd) bytes per element (a layer whose data
+    gradient forms dy: BN backward 4, data gradient g + y + W in, dx + dy out).  JSON to
     args.detail, a markdown table beside it."""
     reps = []
     for _ in range(5):
         ev = {l.name: [torch.cuda.Event(enable_timing=True) for _ in range(7)] for l in layers}
         step(ev, overlap=False)
         torch.cuda.synchronize()
-        reps.append({l.name: [ev[l.name][a].elapsed_time(ev[l.name][b]) for a, b in ((0, 1), (1, 2), (3, 4), (4, 5),
-                                                                                      (5, 6))] for l in layers})
+        # (a layer whose data gradient forms dy runs it before the weight gradient)
+        pairs = lambda l: ((0, 1), (1, 2), (3, 4), (5, 6), (4, 5)) if l.fused else ((0, 1), (1, 2), (3, 4), (4, 5),
+                                                                                     (5, 6))
+        reps.append({l.name: [ev[l.name][a].elapsed_time(ev[l.name][b]) for a, b in pairs(l)] for l in layers})
     per_layer = {l.name: [sorted(r[l.name][k] for r in reps)[2] for k in range(5)] for l in layers}
     rows, tot = [], {p: 0.0 for p in PASSES}
     for l in layers:
@@ -324,6 +351,9 @@ def write_detail(torch, args, step, layers, wl):
         work = {"conv_fwd": (l.flops, xb + wb + yb), "bn_silu_fwd": (0, 4 * l.bn_elems),
                 "bn_silu_bwd": (0, 10 * l.bn_elems), "conv_bwd_weight": (l.flops, xb + yb + 2 * wb),
                 "conv_bwd_data": (l.flops, yb + wb + xb)}
+        if l.fused:  # BN backward: the reduce (g, y); data gradient: g, y and W in, dx and dy out
+            work["bn_silu_bwd"] = (0, 4 * l.bn_elems)
+            work["conv_bwd_data"] = (l.flops, 3 * yb + wb + xb)
         for k, pname in enumerate(PASSES):
             ms = per_layer[l.name][k]
             tot[pname] += ms
@@ -474,7 +504,7 @@ def main():
         specs = [l for l in specs if l.name in want]
     print(f"# setting up {len(specs)} layers of configuration {wl.index} at batch {wl.n}", file=sys.stderr, flush=True)
     cs = ConvSet(specs, wl.n, wl.index, wl.eps, wl.g_std,
-                 [wl.layers.index(l) for l in specs])
+                 [wl.layers.index(l) for l in specs], fuse_bwd=args.fuse_bwd)
     layers = cs.layers
     two = args.streams == 2 and not args.serial
     defer = args.wgrad_order == "deferred"
@@ -569,7 +599,8 @@ def main():
                    "config_index": wl.index, "batch": wl.n, "input": "640x640", "layers": len(layers),
                    "mode": "set", "step_gflop": round(step_flops / 1e9, 2),
                    "launch": "hip graph replay" if graph is not None else "eager",
-                   "streams": 2 if two else 1},
+                   "streams": 2 if two else 1,
+                   "bn_bwd_in_dgrad_layers": sum(1 for l in layers if l.fused)},
         "pct_mfma_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "roofline": roofline,
         "sclk": sclk.summary(),
@@ -590,11 +621,13 @@ def main():
         # BN + SiLU kernels: algorithmic bytes (bf16) per element of the step's activations --
         # forward apply reads y and writes a (4), backward reduce reads g and y (4), backward
         # apply reads g and y and writes dy (6) -- over their summed kernel time
+        # (the backward apply runs only for the layers whose data gradient does not form dy)
         elems = sum(l.bn_elems for l in layers)
+        apply_elems = sum(l.bn_elems for l in layers if not l.fused)
         out["bn_silu_gbs"] = {}
         for c, b in (("bn_silu_fwd_apply", 4), ("bn_silu_bwd_reduce", 4), ("bn_silu_bwd_apply", 6)):
             if c in per_cls:
-                gbs = b * elems / (per_cls[c][0] / 1e3) / 1e9
+                gbs = b * (apply_elems if c == "bn_silu_bwd_apply" else elems) / (per_cls[c][0] / 1e3) / 1e9
                 out["bn_silu_gbs"][c] = {"gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
                                          "frac_copy": round(gbs / copy_gbs, 4)}
     if not args.no_extras and not args.layers and wl.index == 4:

@@ -3,8 +3,13 @@ order in which the C-ABI calls are enqueued.
 
 One step = every layer's forward in network order (conv_fwd with fused batch statistics,
 then bn_silu_fwd), then the backward in reverse order (bn_silu_bwd, conv_bwd_data,
-conv_bwd_weight).  Two schedules give the same results bit for bit (every kernel and every
-reduction order is the same; only the streams differ):
+conv_bwd_weight).  With `fuse_bwd` (off by default: slower on this GPU), a layer whose data
+gradient takes the BN + SiLU backward prologue (the 3x3 stride-1 layers) runs bn_silu_bwd
+for dgamma and dbeta only and then numbat_conv_bwd_data_bn_silu_prologue, which forms dy
+inside the data gradient and writes it for the weight gradient; the results are the same
+bit for bit.  Two schedules
+give the same results bit for bit (every kernel and every reduction order is the same;
+only the streams differ):
 
 * serial: everything on the current stream;
 * two streams: each layer's weight gradient (which nothing later in the backward reads)
@@ -27,7 +32,7 @@ from . import numbat as nb
 class Layer:
     """Device buffers, seeded inputs and problem descriptors of one layer of a conv set."""
 
-    def __init__(self, idx, spec, n, cfg_index, eps, g_std=1.0):
+    def __init__(self, idx, spec, n, cfg_index, eps, g_std=1.0, fuse_bwd=False):
         self.spec = spec
         self.name = spec.name
         sid = lambda t: synth.stream_id(cfg_index, idx, t)
@@ -51,8 +56,31 @@ class Layer:
                                                                        f32(spec.co), f32(spec.co), f32(spec.co))
         self.bnp = self.blk.bn()
         self.ws_need = self.blk.ws_bytes()
+        self.fused = fuse_bwd and self._prologue_supported()
         self.flops = spec.gemm_flops(n)  # one pass
         self.bn_elems = self.blk.m * spec.co
+
+    def _prologue_supported(self):
+        try:
+            nb.numbat_workspace_size(nb.OP_CONV_BWD_DATA_BN_SILU, self.blk.prob)
+        except nb.NumbatError as e:
+            if e.status == nb.ERR_UNSUPPORTED:
+                return False
+            raise
+        return True
+
+    def _bn_bwd(self):
+        """BN + SiLU backward: dgamma, dbeta (and dy unless the data gradient forms it)"""
+        nb.numbat_bn_silu_bwd(self.bnp, self.g, self.y, self.smean, self.srstd, self.gamma, self.beta,
+                              None if self.fused else self.dy, self.dgamma, self.dbeta, None, ws=self.ws,
+                              ws_bytes=self.ws_len)
+
+    def _dgrad(self):
+        if self.fused:
+            nb.numbat_conv_bwd_data_bn_silu_prologue(self.blk.prob, self.g, self.y, self.smean, self.srstd, self.gamma,
+                                                     self.beta, self.dgamma, self.dbeta, self.w, self.dx, self.dy)
+        else:
+            nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
 
     def outputs(self):
         """Every tensor one step writes, by name."""
@@ -81,13 +109,12 @@ class Layer:
         weight gradients."""
         e = ev.get(self.name) if ev else None
         if e: e[3].record()
-        nb.numbat_bn_silu_bwd(self.bnp, self.g, self.y, self.smean, self.srstd, self.gamma, self.beta, self.dy,
-                              self.dgamma, self.dbeta, None, ws=self.ws, ws_bytes=self.ws_len)
+        self._bn_bwd()
         if e: e[4].record()
         if side is not None:
             if pending is not None:
                 pending()
-            nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
+            self._dgrad()
             done = torch.cuda.Event()
             done.record()
 
@@ -103,18 +130,26 @@ class Layer:
                 return wgrad
             wgrad()
             return None
+        # serial: the weight gradient, then the data gradient (events 4-5, 5-6); a fused layer
+        # forms dy in its data gradient, which then comes first (events 4-5 data, 5-6 weight)
+        if self.fused:
+            self._dgrad()
+            if e: e[5].record()
+            nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
+            if e: e[6].record()
+            return None
         nb.numbat_conv_bwd_weight(self.blk.prob, self.x, self.dy, self.dw, False, self.ws, ws_bytes=self.ws_len)
         if e: e[5].record()
-        nb.numbat_conv_bwd_data(self.blk.prob, self.dy, self.w, self.dx, False, self.ws, ws_bytes=self.ws_len)
+        self._dgrad()
         if e: e[6].record()
 
 
 class ConvSet:
     """Every layer of a conv set with shared workspaces, and the step over them."""
 
-    def __init__(self, specs, n, cfg_index, eps, g_std=1.0, layer_index=None):
+    def __init__(self, specs, n, cfg_index, eps, g_std=1.0, layer_index=None, fuse_bwd=False):
         idx = layer_index or list(range(len(specs)))
-        self.layers = [Layer(i, l, n, cfg_index, eps, g_std) for i, l in zip(idx, specs)]
+        self.layers = [Layer(i, l, n, cfg_index, eps, g_std, fuse_bwd) for i, l in zip(idx, specs)]
         need = max(l.ws_need for l in self.layers)
         self.ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
         self.ws_side = torch.zeros_like(self.ws)

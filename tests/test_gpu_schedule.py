@@ -73,3 +73,44 @@ def test_two_stream_step_matches_serial_bitwise():
         cs.step(overlap=False)
         torch.cuda.synchronize()
         compare(cs, ref, f"eager serial step after replay {rep}")
+
+
+def test_fused_backward_step_matches_unfused_bitwise():
+    """With the BN + SiLU backward formed inside the 3x3 stride-1 layers' data gradients
+    (fuse_bwd), every output of every layer equals the unfused serial step's bit for bit:
+    serial, two-stream, and graph-replayed (the weight gradients read the dy the fused data
+    gradients wrote)."""
+    from paper_2609_10632_amd.schedule import ConvSet
+
+    wl = workloads.workload(4)
+    specs = [l for l in wl.layers if l.name in NAMES]
+    idx = [wl.layers.index(l) for l in specs]
+    ref_set = ConvSet(specs, wl.n, wl.index, wl.eps, layer_index=idx)
+    ref_set.step(overlap=False)
+    torch.cuda.synchronize()
+    ref = snapshot(ref_set)
+    del ref_set
+    cs = ConvSet(specs, wl.n, wl.index, wl.eps, layer_index=idx, fuse_bwd=True)
+    fused = [l.name for l in cs.layers if l.fused]
+    print(f"fused backward parity: {len(specs)} layers, {len(fused)} fused: {fused}", flush=True)
+    assert len(fused) >= 3
+    for overlap in (False, True):
+        fill_nan(cs)
+        cs.step(overlap=overlap)
+        torch.cuda.synchronize()
+        compare(cs, ref, f"fused backward, two streams={overlap}")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        cs.step(overlap=True)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cs.step(overlap=True)
+    torch.cuda.synchronize()
+    for rep in range(2):
+        fill_nan(cs)
+        graph.replay()
+        torch.cuda.synchronize()
+        compare(cs, ref, f"fused backward graph replay {rep}")
