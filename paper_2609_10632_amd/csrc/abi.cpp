@@ -349,7 +349,7 @@ size_t bn_fwd_ws(const BnDesc& d) {
 
 size_t bn_bwd_ws(const BnDesc& d) {
   const int nb = bn_reduce_blocks(d.a.m, d.a.c);
-  return round_up((size_t)nb * d.a.c * sizeof(float2), 256);
+  return round_up((size_t)nb * d.a.c * sizeof(float2), 256) + round_up(4 * d.a.c * sizeof(float), 256);
 }
 
 numbat_status check_ws(void* ws, size_t have, size_t need) {
@@ -1119,10 +1119,11 @@ numbat_status numbat_bn_silu_bwd(const numbat_bn_problem* p, const void* g, cons
   ws = ws_body(ws);
   const int nb = bn_reduce_blocks(d.a.m, d.a.c);
   float* part = static_cast<float*>(ws);
+  float* coef = reinterpret_cast<float*>(static_cast<char*>(ws) + round_up((size_t)nb * d.a.c * sizeof(float2), 256));
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = bn_bwd_launch(d.a, static_cast<const bf16_t*>(g), static_cast<const bf16_t*>(y), save_mean, save_rstd,
                                gamma, beta, static_cast<bf16_t*>(dy), dgamma, dbeta, static_cast<bf16_t*>(residual_grad),
-                               part, nb, s);
+                               part, nb, coef, s);
   if (e != hipSuccess) return hip_fail(e, "BN+SiLU backward launch");
   return ok();
 }

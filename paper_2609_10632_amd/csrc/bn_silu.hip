@@ -230,14 +230,17 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_reduce_kernel(BnArgs a, const
   }
 }
 
-// --- backward finalize: fixed-order fp64 sums over blocks -> dbeta, dgamma.
+// --- backward finalize: fixed-order fp64 sums over blocks -> dbeta, dgamma, and the apply's
+// folded constants (bn_bwd_fold of the rounded dgamma, dbeta) as coef[4][c].
 // 8 channels per block, G groups of partial rows per channel (a few loads in flight per
 // lane); the group sums are combined by shuffles within each wave (8 groups) and then the
 // G/8 wave sums by a pairwise tree, in a fixed order that depends only on G.
 constexpr int kFinCh = 8;
 template <int G>
-__global__ __launch_bounds__(kFinCh * G) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c,
-                                                                     float* dgamma, float* dbeta) {
+__global__ __launch_bounds__(kFinCh * G) void bn_bwd_finalize_kernel(const float2* part, int nblocks, int c, int64_t m,
+                                                                     const float* save_mean, const float* save_rstd,
+                                                                     const float* gamma, const float* beta,
+                                                                     float* dgamma, float* dbeta, float* coef) {
   constexpr int NWV = G / 8;  // waves
   __shared__ double sa[NWV][kFinCh], sb[NWV][kFinCh];
   const int cl = threadIdx.x % kFinCh, gidx = threadIdx.x / kFinCh;
@@ -279,18 +282,19 @@ __global__ __launch_bounds__(kFinCh * G) void bn_bwd_finalize_kernel(const float
       }
     p = ta[0];
     q = tb[0];
-    dbeta[ch] = (float)p;
-    dgamma[ch] = (float)q;
+    const float db = (float)p, dg = (float)q;
+    dbeta[ch] = db;
+    dgamma[ch] = dg;
+    bn_bwd_fold(gamma[ch], beta[ch], save_mean[ch], save_rstd[ch], dg, db, m, coef[ch], coef[c + ch],
+                coef[2 * c + ch], coef[3 * c + ch]);
   }
 }
 
 // --- backward apply: dy = gamma * rstd * (dz - dbeta/m - xhat * dgamma/m); residual_grad += g
-// (row layout, folded constants in registers, four rows in flight)
+// (row layout, the finalize's folded constants in registers, four rows in flight)
 __global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, const bf16_t* g, const bf16_t* y,
-                                                                const float* save_mean, const float* save_rstd,
-                                                                const float* gamma, const float* beta,
-                                                                const float* dgamma, const float* dbeta, bf16_t* dy,
-                                                                bf16_t* res_grad, int64_t rows_per_block) {
+                                                                const float* coef, bf16_t* dy, bf16_t* res_grad,
+                                                                int64_t rows_per_block) {
   const int c = a.c;
   const RowLayout L = row_layout(c);
   const int t = threadIdx.x;
@@ -298,9 +302,12 @@ __global__ __launch_bounds__(kThreads) void bn_bwd_apply_kernel(BnArgs a, const 
   const int rr = t / L.cv, cb = (t - rr * L.cv) * 8;
   float ka[8], kb[8], kc[8], kd[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e)
-    bn_bwd_fold(gamma[cb + e], beta[cb + e], save_mean[cb + e], save_rstd[cb + e], dgamma[cb + e], dbeta[cb + e], a.m,
-                ka[e], kb[e], kc[e], kd[e]);
+  for (int e = 0; e < 8; ++e) {
+    ka[e] = coef[cb + e];
+    kb[e] = coef[c + cb + e];
+    kc[e] = coef[2 * c + cb + e];
+    kd[e] = coef[3 * c + cb + e];
+  }
   const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
   const int64_t r1 = r0 + rows_per_block < a.m ? r0 + rows_per_block : a.m;
   const int64_t st = L.rows_per_iter;
@@ -415,7 +422,7 @@ hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, co
 
 hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,
                          const float* save_rstd, const float* gamma, const float* beta, bf16_t* dy, float* dgamma,
-                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, hipStream_t s) {
+                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, float* coef, hipStream_t s) {
   const int64_t rpb = rows_per_block(a.m, nblocks);
   const int nb = (int)((a.m + rpb - 1) / rpb);
   float2* part = reinterpret_cast<float2*>(part2);
@@ -433,19 +440,22 @@ hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, cons
   if (const char* e = getenv("NUMBAT_BN_FING")) fg = atoi(e);
 #endif
   if (fg == 128)
-    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<128>, fgrid, dim3(kFinCh * 128), 0, s, part, nb, a.c, dgamma, dbeta);
+    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<128>, fgrid, dim3(kFinCh * 128), 0, s, part, nb, a.c, a.m, save_mean,
+                  save_rstd, gamma, beta, dgamma, dbeta, coef);
   else if (fg == 64)
-    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<64>, fgrid, dim3(kFinCh * 64), 0, s, part, nb, a.c, dgamma, dbeta);
+    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<64>, fgrid, dim3(kFinCh * 64), 0, s, part, nb, a.c, a.m, save_mean,
+                  save_rstd, gamma, beta, dgamma, dbeta, coef);
   else
-    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<32>, fgrid, dim3(kFinCh * 32), 0, s, part, nb, a.c, dgamma, dbeta);
+    NUMBAT_LAUNCH(bn_bwd_finalize_kernel<32>, fgrid, dim3(kFinCh * 32), 0, s, part, nb, a.c, a.m, save_mean,
+                  save_rstd, gamma, beta, dgamma, dbeta, coef);
   trace_end(KC_BN_BWD_FINALIZE);
   e = hipGetLastError();
   if (e != hipSuccess || dy == nullptr) return e;  // (no dy: the statistics gradients only)
   int64_t arpb = 0;
   const int anb = apply_blocks(a.m, a.c, &arpb);
   trace_begin(KC_BN_BWD_APPLY);
-  NUMBAT_LAUNCH(bn_bwd_apply_kernel, dim3(anb), dim3(kThreads), 0, s, a, g, y, save_mean, save_rstd, gamma, beta,
-                     dgamma, dbeta, dy, res_grad, arpb);
+  NUMBAT_LAUNCH(bn_bwd_apply_kernel, dim3(anb), dim3(kThreads), 0, s, a, g, y, (const float*)coef, dy, res_grad,
+                arpb);
   trace_end(KC_BN_BWD_APPLY);
   return hipGetLastError();
 }

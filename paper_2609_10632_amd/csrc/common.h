@@ -114,8 +114,8 @@ __device__ __forceinline__ float bn_silu_apply(float y, float sc, float sh) {
 //   dz = g sigmoid(z) (1 + z (1 - sigmoid(z)))
 //   dy = a (dz - dbeta / m - xhat dgamma / m) = a dz + (y c + d),
 //        c = -a rstd dgamma / m,  d = -a dbeta / m - mean c
-// The BN backward kernel and the data gradient's prologue both use these, so they form
-// bit-identical dy.
+// The BN backward kernels (the finalize folds the constants once per channel, the apply
+// uses them) and the data gradient's prologue both use these, so they form bit-identical dy.
 __device__ __forceinline__ void bn_bwd_fold(float gamma, float beta, float mean, float rstd, float dgamma,
                                             float dbeta, int64_t m, float& a, float& b, float& c, float& d) {
   a = gamma * rstd;

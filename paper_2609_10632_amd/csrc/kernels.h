@@ -247,10 +247,11 @@ hipError_t bn_stats_launch(const BnArgs& a, const bf16_t* y, float* part3, int n
 hipError_t bn_fwd_launch(const BnArgs& a, const bf16_t* y, const float* mean, const float* var, const float* gamma,
                          const float* beta, const bf16_t* res, bf16_t* out, float* save_mean, float* save_rstd,
                          float* run_mean, float* run_var, hipStream_t s);
+// coef: workspace for 4 * c folded constants (bn_bwd_fold), written by the finalize;
 // dy == nullptr: the reduce and finalize only (dgamma, dbeta), no apply
 hipError_t bn_bwd_launch(const BnArgs& a, const bf16_t* g, const bf16_t* y, const float* save_mean,
                          const float* save_rstd, const float* gamma, const float* beta, bf16_t* dy, float* dgamma,
-                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, hipStream_t s);
+                         float* dbeta, bf16_t* res_grad, float* part2, int nblocks, float* coef, hipStream_t s);
 
 // SPPF max pool (5x5, stride 1, padding 2) and nearest 2x upsampling (pool.hip): n, h, w
 // of the pooled / low-resolution tensor, c channels (a multiple of 8), pixel strides of x
